@@ -1,0 +1,212 @@
+#!/usr/bin/env python3
+"""Benchmark of OctreeNCA inference on one MI355X.
+
+One step = one whole octree inference (octree_nca_infer: pyramid, coarsest
+seed, per level upsample + inject and the level's NCA steps, readout) over one
+synthetic input already resident in HBM.  Default workload: the 184.5 MP
+pathology-scale 2D image (16384 x 11264 RGB, 6 levels, 20 steps per level,
+fp32 state).
+
+Prints one JSON line with
+* value = NCA cell-steps per second (sum over levels of cells x steps, per
+  second of wall time of the timed passes);
+* roofline of the dominant kernel (the fused NCA step): algorithmic FLOP per
+  cell-step x cell-steps of all timed step launches / their summed duration,
+  timed with HIP events on the launch stream, against the peak of the
+  arithmetic the kernel runs on;
+* cpu_baseline: the CPU oracle timed on a bounded sample of the same workload;
+* peak device memory.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+# MI355X published peaks
+HBM_PEAK_GBS = 8000.0
+FP32_VECTOR_PEAK_TFLOPS = 157.3      # packed fp32 FMA
+FP32_MFMA_PEAK_TFLOPS = 157.3
+# The library is built without packed fp32 VALU instructions: one fp32 FMA per
+# lane per clock, 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz.
+FP32_SCALAR_FMA_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+
+
+def algorithmic_flop_per_cell_step(wl) -> int:
+    """Multiply-adds the method itself needs per cell and step, x2, plus the
+    bias, ReLU and residual adds: perception C*taps MACs + C bias adds;
+    first linear 2C*H MACs + H bias adds + H ReLU; second linear
+    H*(C-n_in) MACs; residual (C-n_in) adds."""
+    c, h, taps, hid = wl.channels, wl.hidden, wl.taps(), wl.channels - wl.n_in
+    return 2 * (c * taps + 2 * c * h + h * hid) + c + h + h + hid
+
+
+def algorithmic_bytes_per_cell_step(wl) -> int:
+    """Read C channels, write the C - n_in hidden channels."""
+    eb = 2 if wl.dtype == "f16" else 4
+    return (wl.channels + wl.channels - wl.n_in) * eb
+
+
+def cpu_baseline(wl, seconds_hint=10.0):
+    """Time the CPU oracle on a crop of the finest level (random state, the
+    workload's level-0 weights), a few NCA steps."""
+    import numpy as np
+    import oracle
+    from synthetic import make_weights, storage_dtype
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:   # pragma: no cover
+        threads = 1
+    rng = np.random.default_rng(0)
+    if wl.ndim == 2:
+        shape = (1, 512, 1024)
+    else:
+        shape = (16, 128, 256)
+    steps = 4
+    dt = storage_dtype(wl)
+    state = rng.normal(0, 1, shape + (wl.channels,)).astype(dt)
+    w = make_weights(wl)[0]
+    t0 = time.perf_counter()
+    for t in range(steps):
+        state = oracle.nca_step(state, w, wl.n_in, wl.ndim, 0, t, wl.seed, wl.fire_rate, dt)
+    dt_s = time.perf_counter() - t0
+    cells = shape[0] * shape[1] * shape[2]
+    return {"value": cells * steps / dt_s, "unit": "cell-steps/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{steps} NCA steps of the finest level on a {shape[0]}x{shape[1]}x"
+                      f"{shape[2]} crop ({cells * steps} cell-steps, {dt_s:.1f} s), "
+                      f"numpy float64 arithmetic, BLAS threads={threads}, "
+                      f"affinity={len(os.sched_getaffinity(0))} cpus"}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="pathology184mp")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args(argv)
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
+              "octree inference of one image runs on a single MI355X. Use --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2508_06993_amd as octnca
+    from paper_2508_06993_amd.runtime import Inference, upload_weights, to_device_image
+    from synthetic import WORKLOADS, make_weights
+    from synthetic.cache import cached_image
+
+    wl = WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    octnca.lib()   # fail loudly if the HIP library is missing
+    print(f"# workload {wl.name}: extent {wl.extent}, levels {wl.levels}, steps {wl.steps}",
+          file=sys.stderr, flush=True)
+
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    image_np = cached_image(wl)
+    image = to_device_image(image_np, model)
+    del image_np
+    weights = upload_weights(make_weights(wl))
+    torch.cuda.reset_peak_memory_stats()
+    run = Inference(model, wl.extent, wl.factors)
+    stream = torch.cuda.current_stream()
+    L = wl.levels
+
+    def one_pass(events=None):
+        run(image, weights, wl.steps, wl.fire_rate, wl.seed,
+            level_events=[e.cuda_event for e in events] if events else None, stream=stream)
+
+    for _ in range(args.warmup):
+        one_pass()
+    torch.cuda.synchronize()
+    print("# warmup done", file=sys.stderr, flush=True)
+
+    # events: created (first record) before the timed region
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * L)] for _ in range(args.steps)]
+    for row in ev:
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        one_pass(ev[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    print("# timed passes done", file=sys.stderr, flush=True)
+
+    cells = wl.cells_per_level()
+    cell_steps = wl.cell_steps()
+    step_ms = 0.0
+    for row in ev:
+        for l in range(L):
+            if wl.steps[l] > 0:
+                step_ms += row[2 * l].elapsed_time(row[2 * l + 1])
+    launches = args.steps * sum(wl.steps)
+    avg_launch_ms = step_ms / launches
+    flop = algorithmic_flop_per_cell_step(wl) * cell_steps * args.steps
+    byts = algorithmic_bytes_per_cell_step(wl) * cell_steps * args.steps
+    achieved_tflops = flop / (step_ms * 1e-3) / 1e12
+    achieved_gbs = byts / (step_ms * 1e-3) / 1e9
+    peak = FP32_SCALAR_FMA_PEAK_TFLOPS
+    roofline = {
+        "kernel": "nca_step_valu (fused NCA step)",
+        "bound": "alu",
+        "achieved": round(achieved_tflops, 3),
+        "peak": round(peak, 1),
+        "unit": "TFLOP/s",
+        "frac": round(achieved_tflops / peak, 4),
+        "traffic": None,
+        "achieved_hbm_gbs": round(achieved_gbs, 1),
+        "hbm_frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
+        "frac_vs_packed_fp32_peak": round(achieved_tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
+        "avg_launch_ms": round(avg_launch_ms, 4),
+        "launches": launches,
+        "flop_per_cell_step": algorithmic_flop_per_cell_step(wl),
+        "bytes_per_cell_step": algorithmic_bytes_per_cell_step(wl),
+    }
+    peak_vram = torch.cuda.max_memory_allocated() / 1e9
+
+    out = {
+        "metric": "NCA cell-steps/sec",
+        "value": cell_steps * args.steps / wall,
+        "unit": "cell-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16" if wl.dtype == "f16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "extent_dhw": list(wl.extent), "levels": wl.levels,
+                   "steps_per_level": list(wl.steps), "cells_per_level": cells,
+                   "cell_steps_per_pass": cell_steps, "channels": wl.channels,
+                   "hidden": wl.hidden, "n_in": wl.n_in, "fire_rate": wl.fire_rate,
+                   "parallelism": "single GPU"},
+        "roofline": roofline,
+        "peak_vram_gb": round(peak_vram, 3),
+        "step_kernel_ms_per_pass": round(step_ms / args.steps, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,205 @@
+/*
+ * octree_nca.h -- C ABI of the MI355X (gfx950) OctreeNCA inference library.
+ *
+ * OctreeNCA (arXiv 2508.06993) segments an image (2D) or a volume / video
+ * (3D, 2D+t) by running a Neural Cellular Automaton over an octree pyramid:
+ *   - the input is average-pooled into L levels (Sec. 3.2, "Repeated hidden
+ *     channel upscaling"; supplement S7, table of octree level resolutions);
+ *   - the coarsest level starts from the image in the first n_in channels
+ *     and zeros in the hidden ones (Sec. 3.1);
+ *   - every level runs its own NCA for a number of steps, then its state is
+ *     upsampled by nearest neighbour to the next finer level, whose image is
+ *     written back into the input channels (Sec. 3.2; supplement S6,
+ *     Listings 2 and 3);
+ *   - one NCA step (Sec. 3.1; supplement S3, Listing 1) is, for every cell,
+ *     a depthwise 3x3 (2D) or 3x3x3 (3D) convolution of each channel with
+ *     zero padding plus a bias, concatenated after the cell's own state
+ *     (2C features), a linear layer to H hidden units with bias, ReLU, a
+ *     linear layer to the hidden channels without bias, multiplied by the
+ *     cell's stochastic fire bit and added to the state; input channels are
+ *     never changed; the step is computed out of place (supplement S3).
+ *
+ * Conventions shared by every entry point
+ *   - Level 0 is the finest (original resolution), level L-1 the coarsest.
+ *   - Extents are (d, h, w); a 2D model uses d = 1.  Cells are stored
+ *     row-major over (z, y, x) with the channels innermost ("channels
+ *     last"): element (z, y, x, c) of a buffer with c_n channels sits at
+ *     ((z*h + y)*w + x)*c_n + c.  State buffers have C channels, images
+ *     n_in channels, both in the model's storage type (fp32 or fp16).
+ *   - The canonical cell index idx = (z*h + y)*w + x at a level drives the
+ *     fire mask, so results do not depend on tiling or launch shape.
+ *   - Fire mask (the paper draws it with PyTorch's generator; this library
+ *     uses a counter-based generator so any implementation can reproduce
+ *     it): Philox4x64-10 (Salmon et al., SC 2011) with counter
+ *     (idx >> 2, step, level, 0) and key (seed, 0); the cell takes output
+ *     word (idx & 3) and fires iff (word >> 32) < T, where
+ *     T = min(2^32, floor(fire_rate * 2^32)), fire_rate in [0, 1].
+ *   - Weights are fp32, per level, in device memory, in the layout of
+ *     octnca_level_weights.
+ *   - All pointers to arrays are DEVICE pointers unless marked "host".
+ *     Every buffer is owned by the caller; the library allocates and frees
+ *     nothing and keeps no state between calls.
+ *   - Work is enqueued on `stream` (a hipStream_t passed as void*, NULL =
+ *     the default stream) and is asynchronous: no call synchronises the
+ *     host.  A device fault surfaces at the caller's next synchronisation.
+ *   - Every call checks its arguments before it enqueues anything; on an
+ *     invalid argument it returns a negative status, enqueues nothing and
+ *     writes nothing.  A failed launch returns OCTNCA_EHIP.
+ *   - Calls on different streams are independent.  Buffers written by one
+ *     call must not be read or written by another call running at the same
+ *     time.
+ */
+#ifndef OCTREE_NCA_H
+#define OCTREE_NCA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OCTNCA_ABI_VERSION 1
+
+typedef enum {
+    OCTNCA_OK = 0,
+    OCTNCA_EINVAL = -1,       /* null pointer, bad count, fire rate outside [0,1], aliasing */
+    OCTNCA_EUNSUPPORTED = -2, /* model (ndim, C, H, n_in, dtype) not compiled in */
+    OCTNCA_ESHAPE = -3,       /* extent <= 0, too large, or not divisible by a factor */
+    OCTNCA_EHIP = -4,         /* the HIP runtime reported an error */
+    OCTNCA_ESPACE = -5        /* workspace too small */
+} octnca_status;
+
+typedef enum { OCTNCA_F32 = 0, OCTNCA_F16 = 1 } octnca_dtype;
+
+/* Architecture of one NCA (all levels share it; supplement S3 fixes C and H
+ * at compile time).  Supported: ndim in {2, 3}, channels = 16, hidden = 64,
+ * n_in in {1, 3}, state_dtype in {OCTNCA_F32, OCTNCA_F16}. */
+typedef struct {
+    int32_t ndim;        /* 2: 3x3 taps, d must be 1; 3: 3x3x3 taps */
+    int32_t channels;    /* C: state channels per cell */
+    int32_t hidden;      /* H: hidden units of the per-cell MLP */
+    int32_t n_in;        /* input (image) channels, the first n_in of C */
+    int32_t state_dtype; /* storage type of states and images (octnca_dtype) */
+} octnca_model;
+
+typedef struct {
+    int64_t d, h, w;     /* cells along z (depth / time), y, x */
+} octnca_extent;
+
+/* One level's weights, fp32, device memory.  Sizes follow the parameter
+ * counts the paper prints (supplement S10 and S11 tables): conv weights and
+ * bias, first linear layer with bias, second linear layer without bias. */
+typedef struct {
+    const float *conv_w; /* [C][3^ndim]: taps row-major over (dz, dy, dx) in {-1,0,1};
+                            applied as a cross-correlation (tap (0,0,0) is the cell) */
+    const float *conv_b; /* [C] */
+    const float *w1;     /* [H][2C]: column k < C multiplies state channel k,
+                            column C + k multiplies perception channel k */
+    const float *b1;     /* [H] */
+    const float *w2;     /* [C][H]: row c gives the update of channel c; rows c < n_in
+                            are never read (input channels are not updated) */
+} octnca_level_weights;
+
+/* Image pyramid by node averaging (Sec. 3.2; supplement S7 table).
+ *   image          [d][h][w][n_in] finest image (level 0), storage type.
+ *   finest         extent of level 0.
+ *   levels         L >= 1.
+ *   factors        host, [(L-1)*3]: (fz, fy, fx) of the transition from level l to
+ *                  l+1 at factors[3l .. 3l+2]; each in {1, 2, 3, 4}; ndim 2 needs fz = 1.
+ *   level_images   host array of L-1 device pointers; level_images[l-1] receives
+ *                  level l, [d_l][h_l][w_l][n_in] with d_l = d_{l-1} / fz etc.
+ * I_l[z,y,x,c] = mean of I_{l-1} over the fz*fy*fx block at (fz*z, fy*y, fx*x),
+ * summed in fp32 and rounded once to the storage type.
+ * Errors: EINVAL (null pointer, L < 1), ESHAPE (indivisible extent, bad factor),
+ * EUNSUPPORTED, EHIP. */
+int octree_nca_build_pyramid(const octnca_model *model, const void *image,
+                             octnca_extent finest, int32_t levels, const int32_t *factors,
+                             void *const *level_images, void *stream);
+
+/* Upsample one level's state to the next finer level and inject its image
+ * (Sec. 3.2; supplement S6, Listings 2 and 3):
+ *   fine_state[z,y,x,c] = coarse_state[z/fz, y/fy, x/fx, c]   for c >= n_in,
+ *   fine_state[z,y,x,c] = fine_image[z,y,x,c]                  for c <  n_in.
+ *   coarse_state  [coarse][C];  factor  host, (fz, fy, fx);
+ *   fine_image    [coarse*factor][n_in];  fine_state  [coarse*factor][C], written.
+ * fine_state must not overlap coarse_state or fine_image (EINVAL).
+ * Errors: EINVAL, ESHAPE, EUNSUPPORTED, EHIP. */
+int octree_nca_upsample(const octnca_model *model, const void *coarse_state,
+                        octnca_extent coarse, const int32_t *factor, const void *fine_image,
+                        void *fine_state, void *stream);
+
+/* Run `steps` NCA steps t = 0 .. steps-1 of one level (Sec. 3.1; supplement
+ * S3, Listing 1), out of place, alternating between two buffers:
+ * step t reads bufs[t % 2] and writes bufs[(t+1) % 2].
+ *   buf0     [extent][C], the level's state on entry.
+ *   buf1     [extent][C], scratch of the same size; must not overlap buf0.
+ *   weights  host pointer to one octnca_level_weights (device arrays).
+ *   level    the level index, used only by the fire mask (0 = finest).
+ *   steps    >= 0; 0 leaves buf0 as it is.
+ *   fire_rate in [0, 1]; seed: fire-mask key.
+ *   result_in_buf1  host, may be NULL: set to steps % 2, i.e. 1 when the
+ *            final state is in buf1, 0 when it is in buf0.
+ * Errors: EINVAL, ESHAPE, EUNSUPPORTED, EHIP. */
+int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1,
+                         octnca_extent extent, const octnca_level_weights *weights,
+                         int32_t level, int32_t steps, float fire_rate, uint64_t seed,
+                         int32_t *result_in_buf1, void *stream);
+
+/* Two-class readout on the finest level (Sec. 3.2 predicts the segmentation
+ * in the last hidden channels): seg[p] = 1 if state[p, C-1] > state[p, C-2],
+ * else 0 (ties and NaNs give 0).
+ *   state [extent][C];  seg [extent] uint8, written.
+ * Errors: EINVAL, ESHAPE, EUNSUPPORTED, EHIP. */
+int octree_nca_readout(const octnca_model *model, const void *state, octnca_extent extent,
+                       uint8_t *seg, void *stream);
+
+/* Bytes of device workspace octree_nca_infer needs for this model, finest
+ * extent and pyramid: the images of levels 1..L-1, plus one finest-size state
+ * buffer when final_state is given (two when it is NULL), each 256-byte
+ * aligned.  Returns 0 on invalid arguments. */
+size_t octree_nca_workspace_bytes(const octnca_model *model, octnca_extent finest,
+                                  int32_t levels, const int32_t *factors,
+                                  int32_t with_final_state);
+
+/* Whole OctreeNCA inference (Sec. 3.2; supplement S6, Listing 3): pyramid,
+ * coarsest seed (image in channels < n_in, zeros elsewhere), then for
+ * l = L-1 .. 0: upsample + inject (l < L-1) and steps[l] NCA steps with
+ * weights[l]; finally the readout.
+ *   image        [finest][n_in], storage type.
+ *   factors      host, [(L-1)*3] as in octree_nca_build_pyramid.
+ *   weights      host, [L]; index 0 = finest level.
+ *   steps        host, [L]; steps[l] >= 0.
+ *   workspace    device, >= octree_nca_workspace_bytes(..., final_state != NULL).
+ *   final_state  [finest][C] written with the final state, or NULL.
+ *   seg          [finest] uint8 written with the readout, or NULL.
+ *   level_events host, NULL or [2*L] hipEvent_t handles (void*): event 2l is
+ *                recorded on `stream` before level l's first step and 2l+1
+ *                after its last step (timing hook; events are not created here).
+ * The final state lands directly in final_state (no copy): the buffer order is
+ * chosen from the parity of the step counts.
+ * Errors: EINVAL, ESHAPE, EUNSUPPORTED, ESPACE, EHIP. */
+int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent finest,
+                     int32_t levels, const int32_t *factors,
+                     const octnca_level_weights *weights, const int32_t *steps,
+                     float fire_rate, uint64_t seed, void *workspace, size_t workspace_bytes,
+                     void *final_state, uint8_t *seg, void *const *level_events, void *stream);
+
+/* Export the fire mask of one step of one level (test hook for the
+ * generator described above): mask[idx] = 1 if cell idx fires, else 0.
+ *   mask [extent] uint8, written.
+ * Errors: EINVAL, ESHAPE, EHIP. */
+int octree_nca_fire_mask(uint64_t seed, int32_t level, int32_t step, octnca_extent extent,
+                         float fire_rate, uint8_t *mask, void *stream);
+
+/* Static text for a status code; never NULL. */
+const char *octree_nca_strerror(int status);
+
+/* OCTNCA_ABI_VERSION of the built library. */
+int octree_nca_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OCTREE_NCA_H */

@@ -1,0 +1,340 @@
+// C ABI of the OctreeNCA inference library (include/octree_nca.h): argument
+// checks, buffer planning and the launch sequence of the octree inference
+// (Sec. 3.2; supplement S6, Listing 3).  Every entry point validates all of its
+// arguments before it enqueues any work, allocates nothing and never
+// synchronises the host.
+#include <math.h>
+#include <string.h>
+
+#include "launch.h"
+#include "octree_nca.h"
+
+using namespace octnca;
+
+namespace {
+
+constexpr int64_t kMaxDim = int64_t(1) << 30;      // per axis (kernels index with int)
+constexpr int64_t kMaxCells = int64_t(1) << 36;    // per level
+constexpr int kMaxLevels = 16;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
+
+int check_model(const octnca_model *m) {
+    if (m == nullptr) return OCTNCA_EINVAL;
+    if (m->ndim != 2 && m->ndim != 3) return OCTNCA_EUNSUPPORTED;
+    if (m->channels != kC || m->hidden != kH) return OCTNCA_EUNSUPPORTED;
+    if (m->n_in != 1 && m->n_in != 3) return OCTNCA_EUNSUPPORTED;
+    if (m->state_dtype != OCTNCA_F32 && m->state_dtype != OCTNCA_F16) return OCTNCA_EUNSUPPORTED;
+    return OCTNCA_OK;
+}
+
+int check_extent(const octnca_model *m, const octnca_extent &e) {
+    if (e.d <= 0 || e.h <= 0 || e.w <= 0) return OCTNCA_ESHAPE;
+    if (e.d > kMaxDim || e.h > kMaxDim || e.w > kMaxDim) return OCTNCA_ESHAPE;
+    if (m->ndim == 2 && e.d != 1) return OCTNCA_ESHAPE;
+    if (e.d * e.h > kMaxCells || e.d * e.h * e.w > kMaxCells) return OCTNCA_ESHAPE;
+    return OCTNCA_OK;
+}
+
+int check_factor(const octnca_model *m, const int32_t *f) {
+    for (int a = 0; a < 3; ++a)
+        if (f[a] < 1 || f[a] > 8) return OCTNCA_ESHAPE;
+    if (m->ndim == 2 && f[0] != 1) return OCTNCA_ESHAPE;
+    return OCTNCA_OK;
+}
+
+// fire_rate in [0, 1] (NaN rejected); threshold = min(2^32, floor(rate * 2^32)).
+bool fire_threshold(float rate, uint64_t *out) {
+    if (!(rate >= 0.0f && rate <= 1.0f)) return false;
+    const double t = floor((double)rate * 4294967296.0);
+    *out = t >= 4294967296.0 ? (uint64_t(1) << 32) : (uint64_t)t;
+    return true;
+}
+
+size_t elem_bytes(const octnca_model *m) { return m->state_dtype == OCTNCA_F16 ? 2 : 4; }
+
+Extent3 ext3(const octnca_extent &e) { return Extent3{e.d, e.h, e.w}; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return pa < pb + nb && pb < pa + na;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? OCTNCA_OK : OCTNCA_EHIP; }
+
+// Level extents, finest first; ESHAPE when a factor does not divide.
+int level_extents(const octnca_model *m, octnca_extent finest, int32_t levels,
+                  const int32_t *factors, octnca_extent *out) {
+    if (levels < 1 || levels > kMaxLevels) return OCTNCA_EINVAL;
+    if (levels > 1 && factors == nullptr) return OCTNCA_EINVAL;
+    int st = check_extent(m, finest);
+    if (st) return st;
+    out[0] = finest;
+    for (int l = 1; l < levels; ++l) {
+        const int32_t *f = factors + 3 * (l - 1);
+        if ((st = check_factor(m, f))) return st;
+        const octnca_extent &p = out[l - 1];
+        if (p.d % f[0] || p.h % f[1] || p.w % f[2]) return OCTNCA_ESHAPE;
+        out[l] = octnca_extent{p.d / f[0], p.h / f[1], p.w / f[2]};
+    }
+    return OCTNCA_OK;
+}
+
+bool weights_ok(const octnca_level_weights *w) {
+    return w != nullptr && w->conv_w && w->conv_b && w->w1 && w->b1 && w->w2;
+}
+
+LevelWeightsDev to_dev(const octnca_level_weights *w) {
+    return LevelWeightsDev{w->conv_w, w->conv_b, w->w1, w->b1, w->w2};
+}
+
+Dtype dtype_of(const octnca_model *m) { return m->state_dtype == OCTNCA_F16 ? Dtype::F16 : Dtype::F32; }
+
+// Enqueue `steps` steps; bufs[t % 2] -> bufs[(t + 1) % 2].
+int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
+              const octnca_level_weights *w, int32_t level, int32_t steps, uint64_t seed,
+              uint64_t threshold, hipStream_t stream) {
+    StepArgs a;
+    a.dtype = dtype_of(m);
+    a.ndim = m->ndim;
+    a.n_in = m->n_in;
+    a.ext = ext3(e);
+    a.w = to_dev(w);
+    a.level = (uint32_t)level;
+    a.seed = seed;
+    a.threshold = threshold;
+    void *bufs[2] = {b0, b1};
+    for (int32_t t = 0; t < steps; ++t) {
+        a.step = (uint32_t)t;
+        const hipError_t err = launch_step(a, bufs[t & 1], bufs[(t + 1) & 1], stream);
+        if (err != hipSuccess) return OCTNCA_EHIP;
+    }
+    return OCTNCA_OK;
+}
+
+struct Plan {
+    octnca_extent ext[kMaxLevels];
+    size_t image_off[kMaxLevels];   // workspace offsets of level images 1..L-1
+    size_t state_off[2];            // workspace offsets of the state buffers it holds
+    size_t bytes;
+};
+
+int make_plan(const octnca_model *m, octnca_extent finest, int32_t levels, const int32_t *factors,
+              bool with_final_state, Plan *p) {
+    int st = check_model(m);
+    if (st) return st;
+    if ((st = level_extents(m, finest, levels, factors, p->ext))) return st;
+    const size_t eb = elem_bytes(m);
+    size_t off = 0;
+    p->image_off[0] = 0;
+    for (int l = 1; l < levels; ++l) {
+        p->image_off[l] = off;
+        off += align_up((size_t)(p->ext[l].d * p->ext[l].h * p->ext[l].w) * m->n_in * eb);
+    }
+    const size_t state_bytes = align_up((size_t)(finest.d * finest.h * finest.w) * kC * eb);
+    p->state_off[0] = off;
+    off += state_bytes;
+    p->state_off[1] = off;
+    if (!with_final_state) off += state_bytes;
+    p->bytes = off;
+    return OCTNCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int octree_nca_abi_version(void) { return OCTNCA_ABI_VERSION; }
+
+const char *octree_nca_strerror(int status) {
+    switch (status) {
+        case OCTNCA_OK: return "ok";
+        case OCTNCA_EINVAL: return "invalid argument";
+        case OCTNCA_EUNSUPPORTED: return "model configuration not compiled into this library";
+        case OCTNCA_ESHAPE: return "invalid extent or pooling factor";
+        case OCTNCA_EHIP: return "HIP runtime error";
+        case OCTNCA_ESPACE: return "workspace too small";
+        default: return "unknown status";
+    }
+}
+
+int octree_nca_build_pyramid(const octnca_model *model, const void *image, octnca_extent finest,
+                             int32_t levels, const int32_t *factors, void *const *level_images,
+                             void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    octnca_extent ext[kMaxLevels];
+    if ((st = level_extents(model, finest, levels, factors, ext))) return st;
+    if (image == nullptr || (levels > 1 && level_images == nullptr)) return OCTNCA_EINVAL;
+    for (int l = 1; l < levels; ++l)
+        if (level_images[l - 1] == nullptr) return OCTNCA_EINVAL;
+    const hipStream_t s = (hipStream_t)stream;
+    const void *prev = image;
+    for (int l = 1; l < levels; ++l) {
+        const int32_t *f = factors + 3 * (l - 1);
+        const hipError_t e = launch_pool(dtype_of(model), prev, ext3(ext[l]), level_images[l - 1],
+                                         f[0], f[1], f[2], model->n_in, s);
+        if (e != hipSuccess) return OCTNCA_EHIP;
+        prev = level_images[l - 1];
+    }
+    return OCTNCA_OK;
+}
+
+int octree_nca_upsample(const octnca_model *model, const void *coarse_state, octnca_extent coarse,
+                        const int32_t *factor, const void *fine_image, void *fine_state,
+                        void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if (factor == nullptr || coarse_state == nullptr || fine_image == nullptr ||
+        fine_state == nullptr)
+        return OCTNCA_EINVAL;
+    if ((st = check_extent(model, coarse)) || (st = check_factor(model, factor))) return st;
+    const octnca_extent fine{coarse.d * factor[0], coarse.h * factor[1], coarse.w * factor[2]};
+    if ((st = check_extent(model, fine))) return st;
+    const size_t eb = elem_bytes(model);
+    const size_t fine_bytes = (size_t)(fine.d * fine.h * fine.w) * kC * eb;
+    if (overlap(fine_state, fine_bytes, coarse_state,
+                (size_t)(coarse.d * coarse.h * coarse.w) * kC * eb) ||
+        overlap(fine_state, fine_bytes, fine_image,
+                (size_t)(fine.d * fine.h * fine.w) * model->n_in * eb))
+        return OCTNCA_EINVAL;
+    return hip_status(launch_upsample(dtype_of(model), coarse_state, ext3(fine), factor[0],
+                                      factor[1], factor[2], fine_image, fine_state, model->n_in,
+                                      (hipStream_t)stream));
+}
+
+int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octnca_extent extent,
+                         const octnca_level_weights *weights, int32_t level, int32_t steps,
+                         float fire_rate, uint64_t seed, int32_t *result_in_buf1, void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if ((st = check_extent(model, extent))) return st;
+    uint64_t threshold;
+    if (buf0 == nullptr || buf1 == nullptr || !weights_ok(weights) || level < 0 || steps < 0 ||
+        !fire_threshold(fire_rate, &threshold))
+        return OCTNCA_EINVAL;
+    const size_t bytes = (size_t)(extent.d * extent.h * extent.w) * kC * elem_bytes(model);
+    if (overlap(buf0, bytes, buf1, bytes)) return OCTNCA_EINVAL;
+    st = run_steps(model, buf0, buf1, extent, weights, level, steps, seed, threshold,
+                   (hipStream_t)stream);
+    if (st) return st;
+    if (result_in_buf1) *result_in_buf1 = steps & 1;
+    return OCTNCA_OK;
+}
+
+int octree_nca_readout(const octnca_model *model, const void *state, octnca_extent extent,
+                       uint8_t *seg, void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if ((st = check_extent(model, extent))) return st;
+    if (state == nullptr || seg == nullptr) return OCTNCA_EINVAL;
+    return hip_status(launch_readout(dtype_of(model), state, extent.d * extent.h * extent.w, seg,
+                                     (hipStream_t)stream));
+}
+
+int octree_nca_fire_mask(uint64_t seed, int32_t level, int32_t step, octnca_extent extent,
+                         float fire_rate, uint8_t *mask, void *stream) {
+    uint64_t threshold;
+    if (mask == nullptr || level < 0 || step < 0 || !fire_threshold(fire_rate, &threshold))
+        return OCTNCA_EINVAL;
+    if (extent.d <= 0 || extent.h <= 0 || extent.w <= 0 || extent.d > kMaxDim ||
+        extent.h > kMaxDim || extent.w > kMaxDim || extent.d * extent.h > kMaxCells ||
+        extent.d * extent.h * extent.w > kMaxCells)
+        return OCTNCA_ESHAPE;
+    return hip_status(launch_fire_mask(seed, (uint32_t)level, (uint32_t)step,
+                                       extent.d * extent.h * extent.w, threshold, mask,
+                                       (hipStream_t)stream));
+}
+
+size_t octree_nca_workspace_bytes(const octnca_model *model, octnca_extent finest, int32_t levels,
+                                  const int32_t *factors, int32_t with_final_state) {
+    Plan p;
+    if (make_plan(model, finest, levels, factors, with_final_state != 0, &p)) return 0;
+    return p.bytes;
+}
+
+int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent finest,
+                     int32_t levels, const int32_t *factors, const octnca_level_weights *weights,
+                     const int32_t *steps, float fire_rate, uint64_t seed, void *workspace,
+                     size_t workspace_bytes, void *final_state, uint8_t *seg,
+                     void *const *level_events, void *stream) {
+    Plan p;
+    int st = make_plan(model, finest, levels, factors, final_state != nullptr, &p);
+    if (st) return st;
+    uint64_t threshold;
+    if (image == nullptr || weights == nullptr || steps == nullptr || workspace == nullptr ||
+        !fire_threshold(fire_rate, &threshold))
+        return OCTNCA_EINVAL;
+    int64_t total_steps = 0;
+    for (int l = 0; l < levels; ++l) {
+        if (!weights_ok(&weights[l]) || steps[l] < 0) return OCTNCA_EINVAL;
+        total_steps += steps[l];
+    }
+    if (workspace_bytes < p.bytes) return OCTNCA_ESPACE;
+    const size_t eb = elem_bytes(model);
+    const size_t state_bytes = (size_t)(finest.d * finest.h * finest.w) * kC * eb;
+    char *ws = (char *)workspace;
+    if (final_state != nullptr &&
+        (overlap(final_state, state_bytes, workspace, p.bytes) ||
+         overlap(final_state, state_bytes, image,
+                 (size_t)(finest.d * finest.h * finest.w) * model->n_in * eb)))
+        return OCTNCA_EINVAL;
+    if (overlap(workspace, p.bytes, image,
+                (size_t)(finest.d * finest.h * finest.w) * model->n_in * eb))
+        return OCTNCA_EINVAL;
+
+    // bufs[0] ends up holding the final state: the coarsest seed goes to the
+    // buffer that makes the parity of (upsamples + steps) land there.
+    void *bufs[2];
+    bufs[0] = final_state != nullptr ? final_state : (void *)(ws + p.state_off[1]);
+    bufs[1] = (void *)(ws + p.state_off[0]);
+    const void *img[kMaxLevels];
+    img[0] = image;
+    for (int l = 1; l < levels; ++l) img[l] = ws + p.image_off[l];
+
+    const hipStream_t s = (hipStream_t)stream;
+    const Dtype dt = dtype_of(model);
+    for (int l = 1; l < levels; ++l) {
+        const int32_t *f = factors + 3 * (l - 1);
+        if (launch_pool(dt, img[l - 1], ext3(p.ext[l]), (void *)img[l], f[0], f[1], f[2],
+                        model->n_in, s) != hipSuccess)
+            return OCTNCA_EHIP;
+    }
+    int cur = (int)(((int64_t)(levels - 1) + total_steps) & 1);
+    if (launch_upsample(dt, nullptr, ext3(p.ext[levels - 1]), 1, 1, 1, img[levels - 1], bufs[cur],
+                        model->n_in, s) != hipSuccess)
+        return OCTNCA_EHIP;
+    for (int l = levels - 1; l >= 0; --l) {
+        if (l < levels - 1) {
+            const int32_t *f = factors + 3 * l;
+            if (launch_upsample(dt, bufs[cur], ext3(p.ext[l]), f[0], f[1], f[2], img[l],
+                                bufs[cur ^ 1], model->n_in, s) != hipSuccess)
+                return OCTNCA_EHIP;
+            cur ^= 1;
+        }
+        if (level_events && level_events[2 * l] &&
+            hipEventRecord((hipEvent_t)level_events[2 * l], s) != hipSuccess)
+            return OCTNCA_EHIP;
+        st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, steps[l], seed,
+                       threshold, s);
+        if (st) return st;
+        cur ^= steps[l] & 1;
+        if (level_events && level_events[2 * l + 1] &&
+            hipEventRecord((hipEvent_t)level_events[2 * l + 1], s) != hipSuccess)
+            return OCTNCA_EHIP;
+    }
+    // cur == 0 here by construction of the seed buffer
+    if (seg != nullptr &&
+        launch_readout(dt, bufs[cur], finest.d * finest.h * finest.w, seg, s) != hipSuccess)
+        return OCTNCA_EHIP;
+    return OCTNCA_OK;
+}
+
+}  // extern "C"
+
+namespace octnca {
+hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+    return launch_step_valu(a, src, dst, stream);
+}
+}  // namespace octnca

@@ -1,0 +1,49 @@
+// Internal launch interface between the C ABI layer (api.hip) and the kernel
+// files.  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_common.h"
+
+namespace octnca {
+
+struct Extent3 {
+    int64_t d, h, w;
+    int64_t cells() const { return d * h * w; }
+};
+
+enum class Dtype : int { F32 = 0, F16 = 1 };
+
+// Pyramid: dst = mean of src over (fz, fy, fx) blocks; dst_ext = src_ext / f.
+hipError_t launch_pool(Dtype dt, const void *src, Extent3 dst_ext, void *dst, int fz, int fy,
+                       int fx, int n_in, hipStream_t stream);
+
+// Upsample + inject.  coarse == nullptr seeds the hidden channels with zeros
+// (coarsest level initialisation, factors then must be 1).
+hipError_t launch_upsample(Dtype dt, const void *coarse, Extent3 fine_ext, int fz, int fy, int fx,
+                           const void *fine_image, void *fine_state, int n_in, hipStream_t stream);
+
+hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, uint8_t *seg,
+                          hipStream_t stream);
+
+hipError_t launch_fire_mask(uint64_t seed, uint32_t level, uint32_t step, int64_t cells,
+                            uint64_t threshold, uint8_t *mask, hipStream_t stream);
+
+// One NCA step src -> dst over a level of extent `ext`.
+struct StepArgs {
+    Dtype dtype;
+    int ndim;
+    int n_in;
+    Extent3 ext;
+    LevelWeightsDev w;
+    uint32_t level;
+    uint32_t step;
+    uint64_t seed;
+    uint64_t threshold;
+};
+hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+
+}  // namespace octnca

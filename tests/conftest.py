@@ -4,10 +4,39 @@ import sys
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-if ROOT not in sys.path:
-    sys.path.insert(0, ROOT)
+TESTS = os.path.dirname(os.path.abspath(__file__))
+for p in (ROOT, TESTS):
+    if p not in sys.path:
+        sys.path.insert(0, p)
 
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+def _ensure_library():
+    """Load what is built; build only when no library exists yet."""
+    from paper_2508_06993_amd.build import LIB_PATH, build
+    if not os.path.exists(LIB_PATH):
+        build()
+    return LIB_PATH
+
+
+@pytest.fixture(scope="session")
+def library_path():
+    return _ensure_library()
+
+
+@pytest.fixture(scope="session")
+def gpu():
+    """The GPU tests' device.  No GPU (or no library) is an error, not a skip,
+    on a machine that runs them: the HIP path must be the one that runs."""
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this environment")
+    _ensure_library()
+    import paper_2508_06993_amd as octnca
+    octnca.lib()
+    torch.cuda.set_device(0)
+    return torch.device("cuda", 0)

@@ -1,0 +1,143 @@
+"""GPU parity of the whole OctreeNCA inference (octree_nca_infer) against the
+oracle.
+
+* Reduced workloads with the five workloads' structure (levels, pooling
+  factors, input channels, storage type) at sizes the full oracle finishes in
+  seconds, each spanning several kernel tiles with ragged tails: whole final
+  state and readout compared cell by cell.
+* The five workloads at their full sizes, in the same launch configuration the
+  benchmark times: the GPU runs the whole inference; the oracle evaluates
+  sampled boxes exactly through their light cones (corners, edges, interior).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_06993_amd as octnca
+from paper_2508_06993_amd.runtime import Inference, upload_weights, to_device_image
+from synthetic import (WORKLOADS, TINY_2D, MEDIUM_2D, VOLUME_3D, VIDEO_2DT, PATHOLOGY_184MP,
+                       Workload, make_image, make_weights, scaled, storage_dtype)
+
+from synthetic.cache import cached_image
+
+from parity import assert_seg_close, assert_state_close, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_infer(wl, image, weights, want_state=True):
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    run = Inference(model, wl.extent, wl.factors, want_state=want_state)
+    state, seg = run(to_device_image(image, model), upload_weights(weights), wl.steps,
+                     wl.fire_rate, wl.seed)
+    torch.cuda.synchronize()
+    return state, seg
+
+
+def oracle_infer(wl, image, weights):
+    return oracle.infer(image, weights, ndim=wl.ndim, n_in=wl.n_in, channels=wl.channels,
+                        factors=wl.factors, steps=wl.steps, fire_rate=wl.fire_rate, seed=wl.seed,
+                        dtype=storage_dtype(wl))
+
+
+SMALL = [
+    TINY_2D,
+    scaled(MEDIUM_2D, (1, 200, 168), steps=(6, 6, 6, 6)),
+    scaled(VOLUME_3D, (12, 40, 56), steps=(5, 5, 5)),
+    scaled(VIDEO_2DT, (16, 24, 40), steps=(4, 4, 4, 4, 4), image_kind="uniform"),
+    scaled(PATHOLOGY_184MP, (1, 96, 160), steps=(3,) * 6),
+    Workload(name="aniso3d_nin3", ndim=3, extent=(12, 20, 24), n_in=3,
+             factors=((2, 1, 2), (1, 2, 2), (3, 1, 1)), steps=(5, 0, 3, 7),
+             image_kind="uniform"),
+    Workload(name="single_level", ndim=2, extent=(1, 33, 65), n_in=3, factors=(),
+             steps=(7,), image_kind="uniform"),
+    Workload(name="odd_steps_f16_2d", ndim=2, extent=(1, 48, 36), n_in=1,
+             factors=((1, 2, 2), (1, 3, 3)), steps=(3, 1, 5), dtype="f16",
+             image_kind="uniform"),
+]
+
+
+@pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
+def test_infer_matches_oracle(gpu, wl):
+    image = make_image(wl)
+    weights = make_weights(wl)
+    state, seg = gpu_infer(wl, image, weights)
+    want_state, want_seg = oracle_infer(wl, image, weights)
+    got = to_np(state)
+    assert got.dtype == storage_dtype(wl)
+    np.testing.assert_array_equal(got[..., :wl.n_in], image)
+    assert_state_close(got, want_state, wl.dtype)
+    assert_seg_close(to_np(seg), want_seg, want_state, wl.dtype)
+
+
+def test_infer_without_final_state_buffer(gpu):
+    """final_state = NULL: both ping-pong buffers live in the workspace; the
+    readout must be the same."""
+    wl = scaled(TINY_2D, (1, 48, 80), steps=(3, 2, 5))
+    image = make_image(wl)
+    weights = make_weights(wl)
+    _, seg_a = gpu_infer(wl, image, weights, want_state=True)
+    _, seg_b = gpu_infer(wl, image, weights, want_state=False)
+    np.testing.assert_array_equal(to_np(seg_a), to_np(seg_b))
+
+
+def test_level_events_are_recorded(gpu):
+    wl = TINY_2D
+    model = octnca.Model(ndim=2, n_in=3)
+    run = Inference(model, wl.extent, wl.factors)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(2 * wl.levels)]
+    for e in evs:   # create the underlying HIP events
+        e.record()
+    torch.cuda.synchronize()
+    run(to_device_image(make_image(wl), model), upload_weights(make_weights(wl)), wl.steps,
+        wl.fire_rate, wl.seed, level_events=[e.cuda_event for e in evs])
+    torch.cuda.synchronize()
+    for l in range(wl.levels):
+        assert evs[2 * l].elapsed_time(evs[2 * l + 1]) >= 0.0
+
+
+# ---------------------------------------------------------------------------
+# full sizes: sampled light-cone boxes
+# ---------------------------------------------------------------------------
+
+def boxes_for(wl, size=3, depth=2):
+    d, h, w = wl.extent
+    dz = 1 if wl.ndim == 2 else min(depth, d)
+    zs = [(0, dz)] if wl.ndim == 2 else [(0, dz), (d - dz, d)]
+    mid = lambda n, k: (n // 2 - k // 2, n // 2 - k // 2 + k)
+    out = [
+        (zs[0], (0, size), (0, size)),                       # corner
+        (zs[-1], (h - size, h), (w // 3, w // 3 + size)),    # bottom edge (and last frame)
+        ((zs[0][0], zs[0][1]) if wl.ndim == 2 else mid(d, dz), mid(h, size), mid(w, size)),
+    ]
+    return out
+
+
+FULL = [MEDIUM_2D, VOLUME_3D, PATHOLOGY_184MP, VIDEO_2DT]
+
+
+@pytest.mark.parametrize("wl", FULL, ids=lambda w: w.name)
+def test_full_size_sampled_boxes(gpu, wl):
+    print(f"full-size parity {wl.name} extent={wl.extent}", flush=True)
+    image = np.ascontiguousarray(cached_image(wl))
+    weights = make_weights(wl)
+    state, seg = gpu_infer(wl, image, weights)
+    # input channels bit-exact everywhere, state finite everywhere
+    assert bool(torch.isfinite(state.float()).all())
+    d, h, w = wl.extent
+    for z0 in range(0, d, max(1, d // 4)):
+        sl = state[z0, :, :, :wl.n_in].cpu().numpy()
+        np.testing.assert_array_equal(sl, image[z0])
+    dt = storage_dtype(wl)
+    for box in boxes_for(wl):
+        want = oracle.infer_window(image, weights, box, ndim=wl.ndim, n_in=wl.n_in,
+                                   channels=wl.channels, factors=wl.factors, steps=wl.steps,
+                                   fire_rate=wl.fire_rate, seed=wl.seed, dtype=dt)
+        sl = tuple(slice(a, b) for a, b in box)
+        got = to_np(state[sl])
+        assert_state_close(got, want, wl.dtype, what=f"{wl.name} box {box}")
+        assert_seg_close(to_np(seg[sl]), oracle.readout(want), want, wl.dtype, min_agree=0.0,
+                         what=f"{wl.name} box {box}")
+    del state, seg
+    torch.cuda.empty_cache()

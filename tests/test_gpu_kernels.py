@@ -1,0 +1,257 @@
+"""GPU parity of the individual entry points against the oracle, through the
+C ABI: fire masks and upsampling bit-exact, pyramid values within rounding of
+the fp64 mean (exact on integer ramps), one NCA step and a level's steps
+within the storage type's bound, plus the step's invariants on the GPU."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2508_06993_amd as octnca
+from paper_2508_06993_amd.runtime import upload_weights
+from synthetic import LevelWeights
+
+from parity import to_np, max_rel_err
+
+pytestmark = pytest.mark.gpu
+
+C, H = 16, 64
+NP_DT = {"f32": np.float32, "f16": np.float16}
+T_DT = {"f32": torch.float32, "f16": torch.float16}
+
+
+def rand_weights(rng, ndim, scale=0.1):
+    taps = 3 ** ndim
+    return LevelWeights(
+        conv_w=rng.normal(0, scale, (C, taps)).astype(np.float32),
+        conv_b=rng.normal(0, scale, (C,)).astype(np.float32),
+        w1=rng.normal(0, scale, (H, 2 * C)).astype(np.float32),
+        b1=rng.normal(0, scale, (H,)).astype(np.float32),
+        w2=rng.normal(0, scale, (C, H)).astype(np.float32))
+
+
+def dev(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    return t if dtype is None else t.to(dtype)
+
+
+# ---------------------------------------------------------------------------
+# fire mask: bit-exact
+# ---------------------------------------------------------------------------
+
+MASK_CASES = [
+    ((1, 1, 1), 0, 0, 0, 0.5), ((1, 7, 9), 0, 3, 1, 0.5), ((3, 5, 6), 12345, 2, 19, 0.5),
+    ((1, 64, 64), 0, 0, 0, 0.5), ((1, 33, 257), 2 ** 63 + 5, 5, 7, 0.3),
+    ((1, 16, 16), 9, 1, 2, 0.0), ((1, 16, 16), 9, 1, 2, 1.0), ((4, 9, 11), 77, 4, 15, 0.999),
+    ((2, 100, 1000), 3, 0, 11, 0.5),
+]
+
+
+@pytest.mark.parametrize("extent,seed,level,step,rate", MASK_CASES)
+def test_fire_mask_bit_exact(gpu, extent, seed, level, step, rate):
+    mask = torch.empty(extent, dtype=torch.uint8, device=gpu)
+    octnca.octree_nca_fire_mask(seed, level, step, extent, rate, mask)
+    torch.cuda.synchronize()
+    want = oracle.fire_mask(seed, level, step, extent, rate).astype(np.uint8)
+    np.testing.assert_array_equal(to_np(mask), want)
+
+
+# ---------------------------------------------------------------------------
+# pyramid
+# ---------------------------------------------------------------------------
+
+POOL_CASES = [("f32", 2, (1, 64, 96), [(1, 2, 2)] * 3, 3), ("f32", 3, (8, 24, 20),
+              [(2, 2, 2), (1, 2, 2)], 1), ("f16", 3, (8, 24, 20), [(2, 2, 2), (2, 2, 1)], 3),
+              ("f16", 2, (1, 40, 36), [(1, 2, 2), (1, 2, 3)], 3), ("f32", 3, (6, 9, 4),
+              [(3, 3, 4)], 3)]
+
+
+@pytest.mark.parametrize("dt,ndim,extent,factors,n_in", POOL_CASES)
+def test_pyramid_matches_oracle(gpu, dt, ndim, extent, factors, n_in):
+    rng = np.random.default_rng(5)
+    img = rng.random(extent + (n_in,), dtype=np.float32).astype(NP_DT[dt])
+    model = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt)
+    want = oracle.build_pyramid(img, factors, NP_DT[dt])
+    outs = [torch.empty(w.shape, dtype=T_DT[dt], device=gpu) for w in want[1:]]
+    octnca.octree_nca_build_pyramid(model, dev(img), factors, outs)
+    torch.cuda.synchronize()
+    for lvl, (g, w) in enumerate(zip(outs, want[1:]), start=1):
+        g = to_np(g).astype(np.float64)
+        w = w.astype(np.float64)
+        if dt == "f32":
+            np.testing.assert_allclose(g, w, rtol=1e-6, atol=1e-7, err_msg=f"level {lvl}")
+        else:   # one fp16 rounding of an fp32 sum vs of an fp64 sum
+            np.testing.assert_allclose(g, w, rtol=1e-3, atol=1e-4, err_msg=f"level {lvl}")
+
+
+def test_pyramid_exact_on_coordinate_ramps(gpu):
+    """Channel k holds coordinate k of each cell; each pooled value must be the
+    exact block mean f*X + (f-1)/2 (all values are small dyadic numbers)."""
+    d, h, w = 8, 32, 48
+    z, y, x = np.meshgrid(np.arange(d), np.arange(h), np.arange(w), indexing="ij")
+    img = np.stack([x, y, z], -1).astype(np.float32)
+    factors = [(2, 2, 2), (1, 2, 2), (2, 2, 1)]
+    model = octnca.Model(ndim=3, n_in=3)
+    want = oracle.build_pyramid(img, factors, np.float32)
+    outs = [torch.empty(t.shape, dtype=torch.float32, device=gpu) for t in want[1:]]
+    octnca.octree_nca_build_pyramid(model, dev(img), factors, outs)
+    torch.cuda.synchronize()
+    cum = np.array([1, 1, 1])
+    for g, wt, f in zip(outs, want[1:], factors):
+        cum = cum * np.array(f)
+        zz, yy, xx = np.meshgrid(*(np.arange(n) for n in wt.shape[:3]), indexing="ij")
+        exact = np.stack([cum[2] * xx + (cum[2] - 1) / 2, cum[1] * yy + (cum[1] - 1) / 2,
+                          cum[0] * zz + (cum[0] - 1) / 2], -1)
+        np.testing.assert_array_equal(to_np(g), exact.astype(np.float32))
+        np.testing.assert_array_equal(to_np(g), wt)
+
+
+# ---------------------------------------------------------------------------
+# upsample + inject: bit-exact
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dt,ndim,coarse,factor,n_in",
+                         [("f32", 2, (1, 5, 7), (1, 2, 2), 3), ("f16", 3, (3, 4, 5), (2, 2, 2), 3),
+                          ("f32", 3, (2, 3, 3), (1, 2, 2), 1), ("f16", 2, (1, 9, 4), (1, 3, 2), 1),
+                          ("f32", 3, (1, 1, 1), (4, 4, 4), 3)])
+def test_upsample_bit_exact(gpu, dt, ndim, coarse, factor, n_in):
+    rng = np.random.default_rng(7)
+    cs = rng.normal(0, 1, coarse + (C,)).astype(NP_DT[dt])
+    fine_ext = tuple(a * b for a, b in zip(coarse, factor))
+    img = rng.random(fine_ext + (n_in,), dtype=np.float32).astype(NP_DT[dt])
+    model = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt)
+    out = torch.full(fine_ext + (C,), 99.0, dtype=T_DT[dt], device=gpu)
+    octnca.octree_nca_upsample(model, dev(cs), factor, dev(img), out)
+    torch.cuda.synchronize()
+    want = oracle.upsample_inject(cs, factor, img, NP_DT[dt])
+    np.testing.assert_array_equal(to_np(out), want)
+
+
+def test_upsample_parent_indices_on_coordinates(gpu):
+    """Hidden channels hold the coarse cell's coordinates as exact floats."""
+    cd, ch, cw = 3, 5, 6
+    f = (2, 2, 2)
+    cs = np.zeros((cd, ch, cw, C), np.float32)
+    z, y, x = np.meshgrid(np.arange(cd), np.arange(ch), np.arange(cw), indexing="ij")
+    cs[..., 3], cs[..., 4], cs[..., 5] = x, y, z
+    fine = (cd * 2, ch * 2, cw * 2)
+    img = np.zeros(fine + (3,), np.float32)
+    out = torch.empty(fine + (C,), dtype=torch.float32, device=gpu)
+    octnca.octree_nca_upsample(octnca.Model(ndim=3, n_in=3), dev(cs), f, dev(img), out)
+    torch.cuda.synchronize()
+    o = to_np(out)
+    fz, fy, fx = np.meshgrid(*(np.arange(n) for n in fine), indexing="ij")
+    np.testing.assert_array_equal(o[..., 3], fx // 2)
+    np.testing.assert_array_equal(o[..., 4], fy // 2)
+    np.testing.assert_array_equal(o[..., 5], fz // 2)
+
+
+def test_readout_matches_oracle(gpu):
+    rng = np.random.default_rng(3)
+    s = rng.normal(0, 1, (2, 17, 31, C)).astype(np.float32)
+    s[0, 0, :5, 14] = s[0, 0, :5, 15]      # ties -> 0
+    seg = torch.empty((2, 17, 31), dtype=torch.uint8, device=gpu)
+    octnca.octree_nca_readout(octnca.Model(ndim=3, n_in=1), dev(s), seg)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(seg), oracle.readout(s))
+
+
+# ---------------------------------------------------------------------------
+# one step / one level
+# ---------------------------------------------------------------------------
+
+STEP_CASES = [
+    ("f32", 2, 3, (1, 37, 83)), ("f32", 2, 1, (1, 8, 32)), ("f32", 2, 3, (1, 1, 1)),
+    ("f32", 2, 3, (1, 1, 70)), ("f32", 3, 1, (7, 19, 13)), ("f32", 3, 3, (5, 9, 17)),
+    ("f32", 3, 1, (1, 1, 1)), ("f16", 2, 3, (1, 21, 45)), ("f16", 3, 3, (6, 11, 10)),
+    ("f16", 3, 1, (3, 8, 8)),
+]
+
+
+def run_level_gpu(model, state, w, level, steps, rate, seed):
+    b0 = dev(state)
+    b1 = torch.empty_like(b0)
+    which = octnca.octree_nca_run_level(model, b0, b1, upload_weights([w])[0], level, steps, rate,
+                                        seed)
+    torch.cuda.synchronize()
+    return to_np(b1 if which else b0), which
+
+
+@pytest.mark.parametrize("dt,ndim,n_in,shape", STEP_CASES)
+def test_one_step_matches_oracle(gpu, dt, ndim, n_in, shape):
+    rng = np.random.default_rng(11)
+    w = rand_weights(rng, ndim)
+    s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
+    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt), s, w, 2, 1, 0.5, 42)
+    assert which == 1
+    want = oracle.nca_step(s, w, n_in, ndim, 2, 0, 42, 0.5, NP_DT[dt])
+    tol = 2e-6 if dt == "f32" else 1e-3
+    err = max_rel_err(got, want)
+    assert err <= tol, err
+    np.testing.assert_array_equal(got[..., :n_in], s[..., :n_in])
+    # cells that did not fire are copied bit for bit
+    mask = oracle.fire_mask(42, 2, 0, shape, 0.5)
+    np.testing.assert_array_equal(got[~mask], s[~mask])
+
+
+@pytest.mark.parametrize("dt,ndim,n_in,shape", [("f32", 2, 3, (1, 40, 70)),
+                                                ("f32", 3, 1, (6, 20, 18)),
+                                                ("f16", 3, 3, (8, 12, 20))])
+def test_level_steps_match_oracle(gpu, dt, ndim, n_in, shape):
+    rng = np.random.default_rng(12)
+    w = rand_weights(rng, ndim)
+    s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
+    steps = 9
+    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt), s, w, 1, steps,
+                               0.5, 3)
+    assert which == steps % 2
+    want = oracle.run_level(s, w, n_in, ndim, 1, steps, 3, 0.5, NP_DT[dt])
+    tol = 1e-4 if dt == "f32" else 1e-2
+    assert max_rel_err(got, want) <= tol
+
+
+def test_zero_steps_leave_state(gpu):
+    rng = np.random.default_rng(1)
+    s = rng.normal(0, 1, (1, 9, 9, C)).astype(np.float32)
+    got, which = run_level_gpu(octnca.Model(ndim=2, n_in=3), s, rand_weights(rng, 2), 0, 0, 0.5, 0)
+    assert which == 0
+    np.testing.assert_array_equal(got, s)
+
+
+@pytest.mark.parametrize("ndim", [2, 3])
+def test_fire_rate_zero_and_zero_w2_are_identity(gpu, ndim):
+    rng = np.random.default_rng(2)
+    shape = (1, 23, 41) if ndim == 2 else (5, 10, 12)
+    s = rng.normal(0, 1, shape + (C,)).astype(np.float32)
+    w = rand_weights(rng, ndim)
+    m = octnca.Model(ndim=ndim, n_in=3)
+    got, _ = run_level_gpu(m, s, w, 0, 3, 0.0, 5)
+    np.testing.assert_array_equal(got, s)
+    w.w2[:] = 0
+    got, _ = run_level_gpu(m, s, w, 0, 3, 1.0, 5)
+    np.testing.assert_array_equal(got, s)
+
+
+def test_translation_equivariance_on_gpu(gpu):
+    """With every cell firing, shifting the input shifts the output (cells far
+    enough from the border)."""
+    rng = np.random.default_rng(4)
+    w = rand_weights(rng, 2)
+    m = octnca.Model(ndim=2, n_in=3)
+    base = rng.normal(0, 1, (1, 48, 64, C)).astype(np.float32)
+    shifted = np.roll(base, (5, 9), axis=(1, 2))
+    a, _ = run_level_gpu(m, base, w, 0, 4, 1.0, 0)
+    b, _ = run_level_gpu(m, shifted, w, 0, 4, 1.0, 0)
+    r = 4
+    np.testing.assert_allclose(b[:, 5 + r:48 - r, 9 + r:64 - r],
+                               a[:, r:48 - 5 - r, r:64 - 9 - r], rtol=0, atol=0)
+
+
+def test_step_is_deterministic(gpu):
+    rng = np.random.default_rng(6)
+    w = rand_weights(rng, 3)
+    s = rng.normal(0, 1, (9, 17, 19, C)).astype(np.float32)
+    m = octnca.Model(ndim=3, n_in=1)
+    a, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
+    b, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
+    np.testing.assert_array_equal(a, b)
