@@ -33,6 +33,8 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 FP32_VECTOR_PEAK_TFLOPS = 157.3      # packed fp32 FMA
 FP32_MFMA_PEAK_TFLOPS = 157.3
+BF16_MFMA_PEAK_TFLOPS = 2500.0     # dense
+FP16_MFMA_PEAK_TFLOPS = 2500.0     # dense
 # The library is built without packed fp32 VALU instructions: one fp32 FMA per
 # lane per clock, 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz.
 FP32_SCALAR_FMA_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
@@ -51,6 +53,20 @@ def algorithmic_bytes_per_cell_step(wl) -> int:
     """Read C channels, write the C - n_in hidden channels."""
     eb = 2 if wl.dtype == "f16" else 4
     return (wl.channels + wl.channels - wl.n_in) * eb
+
+
+def step_kernel_arithmetic(wl):
+    """(kernel name, arithmetic of its MLP contraction, that arithmetic's
+    MI355X peak in TFLOP/s) for the step kernel OCTREE_NCA_STEP_KERNEL selects."""
+    sel = os.environ.get("OCTREE_NCA_STEP_KERNEL", "mfma")
+    if sel == "valu":
+        return "nca_step_valu", "fp32 vector FMA", FP32_SCALAR_FMA_PEAK_TFLOPS
+    if sel == "mfma_f32":
+        return "nca_step_mfma / fp32 MFMA", "fp32 MFMA", FP32_MFMA_PEAK_TFLOPS
+    if sel == "mfma_f16" or (sel == "mfma" and wl.dtype == "f16"):
+        return "nca_step_mfma / fp16 MFMA", "fp16 MFMA", FP16_MFMA_PEAK_TFLOPS
+    return "nca_step_mfma / split-bf16 MFMA", "bf16 MFMA (3 products per fp32 product)", \
+        BF16_MFMA_PEAK_TFLOPS
 
 
 def cpu_baseline(wl, seconds_hint=10.0):
@@ -161,18 +177,30 @@ def main(argv=None):
     byts = algorithmic_bytes_per_cell_step(wl) * cell_steps * args.steps
     achieved_tflops = flop / (step_ms * 1e-3) / 1e12
     achieved_gbs = byts / (step_ms * 1e-3) / 1e9
-    peak = FP32_SCALAR_FMA_PEAK_TFLOPS
+    kname, arith, arith_peak = step_kernel_arithmetic(wl)
+    # binding roof: the larger of the two floors (bytes at HBM peak, FLOPs at
+    # the peak of the arithmetic the kernel's contraction runs on)
+    t_hbm = byts / (HBM_PEAK_GBS * 1e9)
+    t_arith = flop / (arith_peak * 1e12)
+    if t_arith >= t_hbm:
+        bound = "alu" if arith == "fp32 vector FMA" else "mfma"
+        achieved, peak, unit = achieved_tflops, arith_peak, "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", achieved_gbs, HBM_PEAK_GBS, "GB/s"
     roofline = {
-        "kernel": "nca_step_valu (fused NCA step)",
-        "bound": "alu",
-        "achieved": round(achieved_tflops, 3),
+        "kernel": kname,
+        "bound": bound,
+        "achieved": round(achieved, 3),
         "peak": round(peak, 1),
-        "unit": "TFLOP/s",
-        "frac": round(achieved_tflops / peak, 4),
+        "unit": unit,
+        "frac": round(achieved / peak, 4),
         "traffic": None,
+        "arithmetic": arith,
+        "achieved_tflops": round(achieved_tflops, 3),
+        "arith_peak_tflops": round(arith_peak, 1),
+        "arith_frac": round(achieved_tflops / arith_peak, 4),
         "achieved_hbm_gbs": round(achieved_gbs, 1),
         "hbm_frac": round(achieved_gbs / HBM_PEAK_GBS, 4),
-        "frac_vs_packed_fp32_peak": round(achieved_tflops / FP32_VECTOR_PEAK_TFLOPS, 4),
         "avg_launch_ms": round(avg_launch_ms, 4),
         "launches": launches,
         "flop_per_cell_step": algorithmic_flop_per_cell_step(wl),

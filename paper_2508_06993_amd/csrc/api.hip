@@ -4,6 +4,7 @@
 // arguments before it enqueues any work, allocates nothing and never
 // synchronises the host.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "launch.h"
@@ -334,7 +335,22 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
 }  // extern "C"
 
 namespace octnca {
+// Step kernel selection, read at every launch from OCTREE_NCA_STEP_KERNEL:
+//   unset / "mfma"  matrix-core kernel, MLP operands split bf16 (x3) for fp32
+//                   states and fp16 for fp16 states;
+//   "mfma_f32"      matrix-core kernel with fp32 MLP operands;
+//   "mfma_bf16x3"   matrix-core kernel with split bf16 operands (any storage);
+//   "mfma_f16"      matrix-core kernel with fp16 operands (fp16 states only);
+//   "valu"          one thread per cell, fp32 FMAs on the vector ALUs.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
-    return launch_step_valu(a, src, dst, stream);
+    const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
+    if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0)
+        return launch_step_mfma(a, MfmaMlp::Default, src, dst, stream);
+    if (strcmp(sel, "valu") == 0) return launch_step_valu(a, src, dst, stream);
+    if (strcmp(sel, "mfma_f32") == 0) return launch_step_mfma(a, MfmaMlp::F32, src, dst, stream);
+    if (strcmp(sel, "mfma_bf16x3") == 0)
+        return launch_step_mfma(a, MfmaMlp::Bf16x3, src, dst, stream);
+    if (strcmp(sel, "mfma_f16") == 0) return launch_step_mfma(a, MfmaMlp::F16, src, dst, stream);
+    return hipErrorInvalidValue;
 }
 }  // namespace octnca

@@ -45,5 +45,10 @@ struct StepArgs {
 };
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+// MLP operand precision of the MFMA step kernel.  Default: split bf16 (x3)
+// for fp32 states, fp16 for fp16 states.
+enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3 };
+hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, const void *src, void *dst,
+                            hipStream_t stream);
 
 }  // namespace octnca

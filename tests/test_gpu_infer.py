@@ -45,7 +45,7 @@ SMALL = [
     TINY_2D,
     scaled(MEDIUM_2D, (1, 200, 168), steps=(6, 6, 6, 6)),
     scaled(VOLUME_3D, (12, 40, 56), steps=(5, 5, 5)),
-    scaled(VIDEO_2DT, (16, 24, 40), steps=(4, 4, 4, 4, 4), image_kind="uniform"),
+    scaled(VIDEO_2DT, (16, 32, 48), steps=(4, 4, 4, 4, 4), image_kind="uniform"),
     scaled(PATHOLOGY_184MP, (1, 96, 160), steps=(3,) * 6),
     Workload(name="aniso3d_nin3", ndim=3, extent=(12, 20, 24), n_in=3,
              factors=((2, 1, 2), (1, 2, 2), (3, 1, 1)), steps=(5, 0, 3, 7),
@@ -59,7 +59,7 @@ SMALL = [
 
 
 @pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
-def test_infer_matches_oracle(gpu, wl):
+def test_infer_matches_oracle(gpu, step_kernel, wl):
     image = make_image(wl)
     weights = make_weights(wl)
     state, seg = gpu_infer(wl, image, weights)

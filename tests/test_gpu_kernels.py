@@ -168,6 +168,19 @@ STEP_CASES = [
 ]
 
 
+# Max relative error bounds (max |g - o| / max |o|) after one step and after
+# nine steps of one level, per storage type and step kernel.  fp32 operands
+# (vector FMAs or fp32 MFMA) differ from the fp64 oracle by fp32 rounding only;
+# split-bf16 operands keep products to about 2^-16 relative; with fp16 states
+# the storage rounding (2^-11) dominates, plus fp16 MLP operands on "mfma".
+STEP_TOL = {
+    ("f32", "valu"): (2e-6, 1e-4), ("f32", "mfma_f32"): (2e-6, 1e-4),
+    ("f32", "mfma"): (5e-5, 5e-4),
+    ("f16", "valu"): (1e-3, 1e-2), ("f16", "mfma_f32"): (1e-3, 1e-2),
+    ("f16", "mfma"): (3e-3, 1e-2),
+}
+
+
 def run_level_gpu(model, state, w, level, steps, rate, seed):
     b0 = dev(state)
     b1 = torch.empty_like(b0)
@@ -178,14 +191,14 @@ def run_level_gpu(model, state, w, level, steps, rate, seed):
 
 
 @pytest.mark.parametrize("dt,ndim,n_in,shape", STEP_CASES)
-def test_one_step_matches_oracle(gpu, dt, ndim, n_in, shape):
+def test_one_step_matches_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     rng = np.random.default_rng(11)
     w = rand_weights(rng, ndim)
     s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
     got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt), s, w, 2, 1, 0.5, 42)
     assert which == 1
     want = oracle.nca_step(s, w, n_in, ndim, 2, 0, 42, 0.5, NP_DT[dt])
-    tol = 2e-6 if dt == "f32" else 1e-3
+    tol = STEP_TOL[(dt, step_kernel)][0]
     err = max_rel_err(got, want)
     assert err <= tol, err
     np.testing.assert_array_equal(got[..., :n_in], s[..., :n_in])
@@ -197,7 +210,7 @@ def test_one_step_matches_oracle(gpu, dt, ndim, n_in, shape):
 @pytest.mark.parametrize("dt,ndim,n_in,shape", [("f32", 2, 3, (1, 40, 70)),
                                                 ("f32", 3, 1, (6, 20, 18)),
                                                 ("f16", 3, 3, (8, 12, 20))])
-def test_level_steps_match_oracle(gpu, dt, ndim, n_in, shape):
+def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     rng = np.random.default_rng(12)
     w = rand_weights(rng, ndim)
     s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
@@ -206,7 +219,7 @@ def test_level_steps_match_oracle(gpu, dt, ndim, n_in, shape):
                                0.5, 3)
     assert which == steps % 2
     want = oracle.run_level(s, w, n_in, ndim, 1, steps, 3, 0.5, NP_DT[dt])
-    tol = 1e-4 if dt == "f32" else 1e-2
+    tol = STEP_TOL[(dt, step_kernel)][1]
     assert max_rel_err(got, want) <= tol
 
 
@@ -219,7 +232,7 @@ def test_zero_steps_leave_state(gpu):
 
 
 @pytest.mark.parametrize("ndim", [2, 3])
-def test_fire_rate_zero_and_zero_w2_are_identity(gpu, ndim):
+def test_fire_rate_zero_and_zero_w2_are_identity(gpu, step_kernel, ndim):
     rng = np.random.default_rng(2)
     shape = (1, 23, 41) if ndim == 2 else (5, 10, 12)
     s = rng.normal(0, 1, shape + (C,)).astype(np.float32)
@@ -232,7 +245,7 @@ def test_fire_rate_zero_and_zero_w2_are_identity(gpu, ndim):
     np.testing.assert_array_equal(got, s)
 
 
-def test_translation_equivariance_on_gpu(gpu):
+def test_translation_equivariance_on_gpu(gpu, step_kernel):
     """With every cell firing, shifting the input shifts the output (cells far
     enough from the border)."""
     rng = np.random.default_rng(4)
@@ -247,7 +260,7 @@ def test_translation_equivariance_on_gpu(gpu):
                                a[:, r:48 - 5 - r, r:64 - 9 - r], rtol=0, atol=0)
 
 
-def test_step_is_deterministic(gpu):
+def test_step_is_deterministic(gpu, step_kernel):
     rng = np.random.default_rng(6)
     w = rand_weights(rng, 3)
     s = rng.normal(0, 1, (9, 17, 19, C)).astype(np.float32)
@@ -255,3 +268,25 @@ def test_step_is_deterministic(gpu):
     a, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
     b, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
     np.testing.assert_array_equal(a, b)
+
+
+def test_split_bf16_kernel_on_fp16_states(gpu, monkeypatch):
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_bf16x3")
+    rng = np.random.default_rng(13)
+    w = rand_weights(rng, 3)
+    s = rng.normal(0, 1, (6, 11, 35, C)).astype(np.float16)
+    got, _ = run_level_gpu(octnca.Model(ndim=3, n_in=3, dtype="f16"), s, w, 0, 4, 0.5, 8)
+    want = oracle.run_level(s, w, 3, 3, 0, 4, 8, 0.5, np.float16)
+    assert max_rel_err(got, want) <= 5e-3
+
+
+def test_fp16_operands_refused_for_fp32_states(gpu, monkeypatch):
+    """fp16 MLP operands are not offered for fp32 states: the launch is
+    refused before anything is enqueued."""
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_f16")
+    s = np.zeros((1, 8, 8, C), np.float32)
+    b0 = dev(s)
+    b1 = torch.empty_like(b0)
+    w = upload_weights([rand_weights(np.random.default_rng(0), 2)])[0]
+    with pytest.raises(octnca.OctreeNCAError):
+        octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=3), b0, b1, w, 0, 1, 0.5, 0)
