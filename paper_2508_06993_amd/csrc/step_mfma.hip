@@ -60,6 +60,12 @@ __device__ __forceinline__ int feature_of(int slot, int g) {
 // its 8 features (update).  All accumulate in fp32.
 // ---------------------------------------------------------------------------
 
+// ReLU as an integer max on the float's bits: negative floats (sign bit set)
+// are negative integers and become +0; one instruction, no NaN quieting.
+__device__ __forceinline__ float relu(float x) {
+    return __int_as_float(max(__float_as_int(x), 0));
+}
+
 // fp32 operands: v_mfma_f32_16x16x4_f32, 32 + 16 MFMAs per 16 cells.
 struct MlpF32 {
     float w1[4][8];   // [jt][kc] = W1[jt*16 + n][feature(kc, g)]
@@ -95,7 +101,7 @@ struct MlpF32 {
         for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float h = fmaxf(acc[jt][i], 0.f);
+                const float h = relu(acc[jt][i]);
                 if ((jt * 4 + i) & 1)
                     u1 = __builtin_amdgcn_mfma_f32_16x16x4f32(w2[jt][i], h, u1, 0, 0, 0);
                 else
@@ -114,10 +120,24 @@ struct MlpF32 {
 // 12 + 6 MFMAs per 16 cells.  A and B use the same (lane group, slot) -> K
 // correspondence, so the feature / hidden order only has to agree between
 // the weights gathered here and the activations.
+typedef float v2f __attribute__((ext_vector_type(2)));
+typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
+
+// hi = bf16(x) (round to nearest even, two values per conversion), hi read
+// back as fp32 by bit shifts, lo = bf16(x - hi).
 __device__ __forceinline__ void split_bf16(const v8f &x, v8bf &hi, v8bf &lo) {
-    hi = __builtin_convertvector(x, v8bf);
-    const v8f back = __builtin_convertvector(hi, v8f);
-    lo = __builtin_convertvector(x - back, v8bf);
+    uint32_t h[4], l[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        const v2bf hp = __builtin_convertvector(v2f{x[2 * p], x[2 * p + 1]}, v2bf);
+        h[p] = __builtin_bit_cast(uint32_t, hp);
+        const float back0 = __uint_as_float(h[p] << 16);
+        const float back1 = __uint_as_float(h[p] & 0xffff0000u);
+        const v2bf lp = __builtin_convertvector(v2f{x[2 * p] - back0, x[2 * p + 1] - back1}, v2bf);
+        l[p] = __builtin_bit_cast(uint32_t, lp);
+    }
+    hi = __builtin_bit_cast(v8bf, h);
+    lo = __builtin_bit_cast(v8bf, l);
 }
 
 struct MlpBf16x3 {
@@ -172,7 +192,7 @@ struct MlpBf16x3 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = fmaxf(acc[2 * p + s / 4][s % 4], 0.f);
+            for (int s = 0; s < 8; ++s) x[s] = relu(acc[2 * p + s / 4][s % 4]);
             split_bf16(x, hh[p], hl[p]);
         }
         v4f u[2];
@@ -231,7 +251,7 @@ struct MlpF16 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = fmaxf(acc[2 * p + s / 4][s % 4], 0.f);
+            for (int s = 0; s < 8; ++s) x[s] = relu(acc[2 * p + s / 4][s % 4]);
             u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2[p], __builtin_convertvector(x, v8h), u,
                                                        0, 0, 0);
         }
@@ -265,7 +285,78 @@ __device__ __forceinline__ bool fire_bit(const FireBallots &b, int row_slot, uin
     return (w >> (16 * row_slot + o)) & 1;
 }
 
-// Store 4 channels (fp32 values) of one cell in the storage type.
+// ---------------------------------------------------------------------------
+// Halo tiles: a tile of cells (plus a one-cell halo) is read from HBM in
+// 16-byte chunks, consecutive threads taking consecutive chunks (coalesced),
+// and kept in LDS as fp32 in four channel-quad planes, so that the 16 lanes
+// of a quad read 16 consecutive 16-byte words (no bank conflicts).  The plane
+// stride is 2 mod 8 (in 16-byte words) so the four planes of one cell sit in
+// different bank groups.  Loads go through registers: the next tile's loads
+// are issued before the current tile is computed and written to LDS after it
+// (software pipelining), so HBM latency overlaps the compute.
+// ---------------------------------------------------------------------------
+template <typename T> struct CellChunks;
+template <> struct CellChunks<float> { static constexpr int N = 4; };    // 16 B = 4 channels
+template <> struct CellChunks<__half> { static constexpr int N = 2; };   // 16 B = 8 channels
+
+constexpr int plane_stride(int cells) { return (cells + 7) / 8 * 8 + 2; }
+
+template <typename T, int HY, int HX>
+struct HaloLoader {
+    static constexpr int kCells = HY * HX;
+    static constexpr int NQ = CellChunks<T>::N;
+    static constexpr int kChunks = kCells * NQ;
+    static constexpr int NCH = (kChunks + kThreads - 1) / kThreads;
+    static constexpr int PS = plane_stride(kCells);
+    uint4 v[NCH];
+
+    // Halo plane z (ignored for 2D: pass z = 0, dd = 1) of the tile whose
+    // interior starts at (y0, x0); cells outside the grid read as zero.
+    __device__ __forceinline__ void issue(const T *__restrict__ src, int z, int dd, int dh, int dw,
+                                          int y0, int x0) {
+        const bool zin = z >= 0 && z < dd;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int i = (int)threadIdx.x + c * kThreads;
+            const int q = i % NQ;
+            const int cell = i / NQ;
+            const int ly = cell / HX, lx = cell - (cell / HX) * HX;
+            const int gy = y0 + ly - 1, gx = x0 + lx - 1;
+            const bool valid = i < kChunks && zin && gy >= 0 && gy < dh && gx >= 0 && gx < dw;
+            v[c] = make_uint4(0u, 0u, 0u, 0u);
+            if (valid) {
+                const int64_t gcell = ((int64_t)z * dh + gy) * dw + gx;
+                v[c] = reinterpret_cast<const uint4 *>(src + gcell * kC)[q];
+            }
+        }
+    }
+
+    __device__ __forceinline__ void commit(float4 *planes) const {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int i = (int)threadIdx.x + c * kThreads;
+            if (i < kChunks) {
+                const int q = i % NQ;
+                const int cell = i / NQ;
+                if constexpr (NQ == 4) {
+                    planes[q * PS + cell] = make_float4(__uint_as_float(v[c].x),
+                                                        __uint_as_float(v[c].y),
+                                                        __uint_as_float(v[c].z),
+                                                        __uint_as_float(v[c].w));
+                } else {
+                    float f[8];
+                    Storage<__half>::unpack(v[c], f);
+                    planes[(2 * q) * PS + cell] = make_float4(f[0], f[1], f[2], f[3]);
+                    planes[(2 * q + 1) * PS + cell] = make_float4(f[4], f[5], f[6], f[7]);
+                }
+            }
+        }
+    }
+};
+
+// Residual update and store of the lane's 4 channels (fp32 values, stored in
+// the storage type).  upd[k] is 0 for input channels, 1 otherwise; with
+// m * upd = 0 the fma returns the state bit for bit (u is finite).
 __device__ __forceinline__ void store_quad(float *dst, int64_t cell, int g, v4f v) {
     *reinterpret_cast<float4 *>(dst + cell * kC + 4 * g) = make_float4(v[0], v[1], v[2], v[3]);
 }
@@ -275,48 +366,23 @@ __device__ __forceinline__ void store_quad(__half *dst, int64_t cell, int g, v4f
     *reinterpret_cast<uint2 *>(dst + cell * kC + 4 * g) = make_uint2(lo, hi);
 }
 
-// Load one cell (all C channels, 16 bytes per thread-chunk) into 4 fp32 quad
-// planes of LDS.  For fp32 storage chunk q is quad q; for fp16 storage chunk q
-// holds quads 2q and 2q+1.
-template <typename T> struct CellChunks;
-template <> struct CellChunks<float> { static constexpr int N = 4; };
-template <> struct CellChunks<__half> { static constexpr int N = 2; };
-
 template <typename T>
-__device__ __forceinline__ void stage_chunk(float4 *planes, int plane_stride, int cell, int q,
-                                            const T *src_cell, bool valid);
-
-template <>
-__device__ __forceinline__ void stage_chunk<float>(float4 *planes, int ps, int cell, int q,
-                                                   const float *src_cell, bool valid) {
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (valid) v = reinterpret_cast<const float4 *>(src_cell)[q];
-    planes[q * ps + cell] = v;
+__device__ __forceinline__ void update_store(T *dst, int64_t idx, int g, const float f[8],
+                                             const v4f &u, const float upd[4], bool fire) {
+    const float m = fire ? 1.f : 0.f;
+    v4f out;
+    out[0] = fmaf(m * upd[0], u[0], f[0]);
+    out[1] = fmaf(m * upd[1], u[1], f[1]);
+    out[2] = fmaf(m * upd[2], u[2], f[2]);
+    out[3] = fmaf(m * upd[3], u[3], f[3]);
+    store_quad(dst, idx, g, out);
 }
-
-template <>
-__device__ __forceinline__ void stage_chunk<__half>(float4 *planes, int ps, int cell, int q,
-                                                    const __half *src_cell, bool valid) {
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (valid) v = reinterpret_cast<const uint4 *>(src_cell)[q];
-    float f[8];
-    Storage<__half>::unpack(v, f);
-    planes[(2 * q) * ps + cell] = make_float4(f[0], f[1], f[2], f[3]);
-    planes[(2 * q + 1) * ps + cell] = make_float4(f[4], f[5], f[6], f[7]);
-}
-
-// Plane stride (in float4) with stride % 8 == 2: the four planes start in
-// different bank groups, so 16-byte LDS writes of consecutive chunks do not
-// collide.
-constexpr int plane_stride(int cells) { return (cells + 7) / 8 * 8 + 2; }
 
 // ---------------------------------------------------------------------------
-// 2D
+// 2D: persistent blocks loop over 16 x 32 tiles (tile index row-major).
 // ---------------------------------------------------------------------------
 constexpr int k2TY = 16, k2TX = 32;
 constexpr int k2HY = k2TY + 2, k2HX = k2TX + 2;
-constexpr int k2Cells = k2HY * k2HX;
-constexpr int k2PS = plane_stride(k2Cells);
 
 template <typename T, int NIN, class Mlp>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
@@ -324,8 +390,8 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
     const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
-    __shared__ float4 planes[4 * k2PS];
-    constexpr int NQ = CellChunks<T>::N;
+    using Loader = HaloLoader<T, k2HY, k2HX>;
+    __shared__ float4 planes[4 * Loader::PS];
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -336,54 +402,51 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
     mlp.load(w1, b1, w2, n, g);
     float cw[9][4];
     float cb[4];
+    float upd[4];   // channels < NIN are copied, never updated
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         cb[k] = conv_b[4 * g + k];
+        upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
 #pragma unroll
         for (int t = 0; t < 9; ++t) cw[t][k] = conv_w[(4 * g + k) * 9 + t];
     }
-    // channels < NIN are copied, never updated
-    float upd[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
 
-    for (int tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
-        const int ty = tile / tiles_x, tx = tile - (tile / tiles_x) * tiles_x;
-        const int y0 = ty * k2TY, x0 = tx * k2TX;
-
-        for (int i = threadIdx.x; i < k2Cells * NQ; i += kThreads) {
-            const int q = i % NQ;
-            const int cell = i / NQ;
-            const int ly = cell / k2HX, lx = cell - (cell / k2HX) * k2HX;
-            const int gy = y0 + ly - 1, gx = x0 + lx - 1;
-            const bool valid = gy >= 0 && gy < dh && gx >= 0 && gx < dw;
-            const int64_t gcell = valid ? (int64_t)gy * dw + gx : 0;
-            stage_chunk<T>(planes, k2PS, cell, q, src + gcell * kC, valid);
-        }
-
+    Loader ld;
+    int tile = blockIdx.x;
+    if (tile < tiles) {
+        const int ty = tile / tiles_x;
+        ld.issue(src, 0, 1, dh, dw, ty * k2TY, (tile - ty * tiles_x) * k2TX);
+    }
+    for (; tile < tiles; tile += gridDim.x) {
+        const int ty = tile / tiles_x;
+        const int y0 = ty * k2TY, x0 = (tile - ty * tiles_x) * k2TX;
+        ld.commit(planes);
         // fire bits of the wave's 4 rows (rows 4*wave .. 4*wave+3 of the tile)
-        const int brow = lane >> 4;
-        const uint64_t brow_idx = (uint64_t)(y0 + 4 * wave + brow) * dw + x0;
+        const uint64_t brow_idx = (uint64_t)(y0 + 4 * wave + (lane >> 4)) * dw + x0;
         const FireBallots fb =
             fire_ballots((brow_idx >> 2) + (lane & 15), step, level, seed, threshold);
         __syncthreads();
+        const int next = tile + (int)gridDim.x;
+        if (next < tiles) {
+            const int nty = next / tiles_x;
+            ld.issue(src, 0, 1, dh, dw, nty * k2TY, (next - nty * tiles_x) * k2TX);
+        }
 
+        const float4 *pl = planes + g * Loader::PS;
 #pragma unroll 1
         for (int grp = 0; grp < 8; ++grp) {
             const int r = grp >> 1;                 // row slot within the wave
             const int cx = (grp & 1) * 16 + n;      // column within the tile
             const int ly = 4 * wave + r;
             const int centre = (ly + 1) * k2HX + cx + 1;
-            const float4 *pl = planes + g * k2PS;
 
             float f[8];
-            const float4 s = pl[centre];
-            f[0] = s.x; f[1] = s.y; f[2] = s.z; f[3] = s.w;
+            const float4 sv = pl[centre];
+            f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
             float p[4] = {cb[0], cb[1], cb[2], cb[3]};
 #pragma unroll
             for (int t = 0; t < 9; ++t) {
-                const int off = (t / 3 - 1) * k2HX + (t % 3 - 1);
-                const float4 v = pl[centre + off];
+                const float4 v = pl[centre + (t / 3 - 1) * k2HX + (t % 3 - 1)];
                 p[0] = fmaf(cw[t][0], v.x, p[0]);
                 p[1] = fmaf(cw[t][1], v.y, p[1]);
                 p[2] = fmaf(cw[t][2], v.z, p[2]);
@@ -397,13 +460,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
             if (y < dh && x < dw) {
                 const uint64_t idx = (uint64_t)y * dw + x;
                 const uint64_t row_q0 = ((uint64_t)y * dw + x0) >> 2;
-                const float m = fire_bit(fb, r, idx, row_q0) ? 1.f : 0.f;
-                v4f out;
-                out[0] = fmaf(m * upd[0], u[0], f[0]);
-                out[1] = fmaf(m * upd[1], u[1], f[1]);
-                out[2] = fmaf(m * upd[2], u[2], f[2]);
-                out[3] = fmaf(m * upd[3], u[3], f[3]);
-                store_quad(dst, (int64_t)idx, g, out);
+                update_store(dst, (int64_t)idx, g, f, u, upd, fire_bit(fb, r, idx, row_q0));
             }
         }
         __syncthreads();
@@ -411,29 +468,13 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
 }
 
 // ---------------------------------------------------------------------------
-// 3D: 8 x 32 (y, x) column, z planes streamed through a ring of 3 halo planes
+// 3D: a work item is an 8 x 32 (y, x) column and a run of z planes; planes
+// stream through a ring of three halo planes in LDS, the plane after next
+// being loaded while the current one is computed.
 // ---------------------------------------------------------------------------
 constexpr int k3TY = 8, k3TX = 32;
 constexpr int k3HY = k3TY + 2, k3HX = k3TX + 2;
-constexpr int k3Cells = k3HY * k3HX;
-constexpr int k3PS = plane_stride(k3Cells);
 constexpr int k3ZRun = 16;    // z planes per work item
-
-template <typename T>
-__device__ __forceinline__ void stage_plane_3d(float4 *ring_slot, const T *__restrict__ src,
-                                               int z, int dd, int dh, int dw, int y0, int x0) {
-    constexpr int NQ = CellChunks<T>::N;
-    const bool zin = z >= 0 && z < dd;
-    for (int i = threadIdx.x; i < k3Cells * NQ; i += kThreads) {
-        const int q = i % NQ;
-        const int cell = i / NQ;
-        const int ly = cell / k3HX, lx = cell - (cell / k3HX) * k3HX;
-        const int gy = y0 + ly - 1, gx = x0 + lx - 1;
-        const bool valid = zin && gy >= 0 && gy < dh && gx >= 0 && gx < dw;
-        const int64_t gcell = valid ? ((int64_t)z * dh + gy) * dw + gx : 0;
-        stage_chunk<T>(ring_slot, k3PS, cell, q, src + gcell * kC, valid);
-    }
-}
 
 template <typename T, int NIN, class Mlp>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
@@ -441,9 +482,9 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     int tiles_y, int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
-    __shared__ float4 ring[3][4 * k3PS];
+    using Loader = HaloLoader<T, k3HY, k3HX>;
+    __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
-    constexpr int NQ = CellChunks<T>::N;
 
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -465,6 +506,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
     }
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
+    Loader ld;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         int rest = item;
@@ -476,22 +518,26 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         const int z_begin = zr * k3ZRun;
         const int z_end = min(dd, z_begin + k3ZRun);
 
-        __syncthreads();   // previous item's readers are done with the ring
-        stage_plane_3d<T>(ring[(z_begin + 2) % 3], src, z_begin - 1, dd, dh, dw, y0, x0);
-        stage_plane_3d<T>(ring[z_begin % 3], src, z_begin, dd, dh, dw, y0, x0);
+        __syncthreads();   // the previous item's readers are done with the ring
+        ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
+        ld.commit(ring[(z_begin + 2) % 3]);
+        ld.issue(src, z_begin, dd, dh, dw, y0, x0);
+        ld.commit(ring[z_begin % 3]);
+        ld.issue(src, z_begin + 1, dd, dh, dw, y0, x0);
 
         for (int z = z_begin; z < z_end; ++z) {
-            stage_plane_3d<T>(ring[(z + 1) % 3], src, z + 1, dd, dh, dw, y0, x0);
+            ld.commit(ring[(z + 1) % 3]);
             // fire bits of the wave's 2 rows of this plane
-            const int brow = (lane >> 4) & 1;
-            const uint64_t brow_idx = ((uint64_t)z * dh + (y0 + 2 * wave + brow)) * dw + x0;
+            const uint64_t brow_idx =
+                ((uint64_t)z * dh + (y0 + 2 * wave + ((lane >> 4) & 1))) * dw + x0;
             const FireBallots fb =
                 fire_ballots((brow_idx >> 2) + (lane & 15), step, level, seed, threshold);
             __syncthreads();
+            if (z + 2 <= z_end) ld.issue(src, z + 2, dd, dh, dw, y0, x0);
 
-            const float4 *pm = ring[(z + 2) % 3] + g * k3PS;   // plane z - 1
-            const float4 *pc = ring[z % 3] + g * k3PS;         // plane z
-            const float4 *pp = ring[(z + 1) % 3] + g * k3PS;   // plane z + 1
+            const float4 *pm = ring[(z + 2) % 3] + g * Loader::PS;   // plane z - 1
+            const float4 *pc = ring[z % 3] + g * Loader::PS;         // plane z
+            const float4 *pp = ring[(z + 1) % 3] + g * Loader::PS;   // plane z + 1
 #pragma unroll 1
             for (int grp = 0; grp < 4; ++grp) {
                 const int r = grp >> 1;
@@ -499,20 +545,23 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 const int ly = 2 * wave + r;
                 const int centre = (ly + 1) * k3HX + cx + 1;
                 float f[8];
-                const float4 s = pc[centre];
-                f[0] = s.x; f[1] = s.y; f[2] = s.z; f[3] = s.w;
+                const float4 sv = pc[centre];
+                f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
                 float p[4] = {cb[0], cb[1], cb[2], cb[3]};
+                // taps in order (dz, dy, dx); one plane at a time keeps the
+                // number of LDS values in flight (and registers) bounded
+#pragma unroll 1
+                for (int pz = 0; pz < 3; ++pz) {
+                    const float4 *pl = pz == 0 ? pm : pz == 1 ? pc : pp;
 #pragma unroll
-                for (int t = 0; t < 27; ++t) {
-                    const float4 *pl = t < 9 ? pm : t < 18 ? pc : pp;
-                    const int tt = t % 9;
-                    const int off = (tt / 3 - 1) * k3HX + (tt % 3 - 1);
-                    const float4 v = pl[centre + off];
-                    const float4 w = tapw[t][g];
-                    p[0] = fmaf(w.x, v.x, p[0]);
-                    p[1] = fmaf(w.y, v.y, p[1]);
-                    p[2] = fmaf(w.z, v.z, p[2]);
-                    p[3] = fmaf(w.w, v.w, p[3]);
+                    for (int tt = 0; tt < 9; ++tt) {
+                        const float4 v = pl[centre + (tt / 3 - 1) * k3HX + (tt % 3 - 1)];
+                        const float4 w = tapw[pz * 9 + tt][g];
+                        p[0] = fmaf(w.x, v.x, p[0]);
+                        p[1] = fmaf(w.y, v.y, p[1]);
+                        p[2] = fmaf(w.z, v.z, p[2]);
+                        p[3] = fmaf(w.w, v.w, p[3]);
+                    }
                 }
                 f[4] = p[0]; f[5] = p[1]; f[6] = p[2]; f[7] = p[3];
 
@@ -522,13 +571,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 if (y < dh && x < dw) {
                     const uint64_t idx = ((uint64_t)z * dh + y) * dw + x;
                     const uint64_t row_q0 = (((uint64_t)z * dh + y) * dw + x0) >> 2;
-                    const float m = fire_bit(fb, r, idx, row_q0) ? 1.f : 0.f;
-                    v4f out;
-                    out[0] = fmaf(m * upd[0], u[0], f[0]);
-                    out[1] = fmaf(m * upd[1], u[1], f[1]);
-                    out[2] = fmaf(m * upd[2], u[2], f[2]);
-                    out[3] = fmaf(m * upd[3], u[3], f[3]);
-                    store_quad(dst, (int64_t)idx, g, out);
+                    update_store(dst, (int64_t)idx, g, f, u, upd, fire_bit(fb, r, idx, row_q0));
                 }
             }
             __syncthreads();   // plane z - 1's slot is refilled next
