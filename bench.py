@@ -69,6 +69,36 @@ def step_kernel_arithmetic(wl):
         BF16_MFMA_PEAK_TFLOPS
 
 
+STEP_SOURCES = ("paper_2508_06993_amd/csrc/step_mfma.hip", "paper_2508_06993_amd/csrc/device_common.h")
+
+
+def step_source_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in STEP_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(wl, selector: str):
+    """HBM bytes per step launch from the profiler's FETCH_SIZE / WRITE_SIZE
+    counters (each scaled by what it reads for a plain copy of known size),
+    recorded in profiles/ together with the hash of the step kernel's sources;
+    None when no record matches this workload, selector and source."""
+    path = os.path.join(ROOT, "profiles", f"step_kernel_traffic_{wl.name}.md")
+    if not os.path.exists(path):
+        return None
+    rec = {}
+    for line in open(path):
+        if ":" in line and line.strip().startswith("- `"):
+            k, v = line.strip()[3:].split("`:", 1)
+            rec[k.strip()] = v.strip().strip("`")
+    if rec.get("source_sha256") != step_source_sha256() or rec.get("kernel_selector") != selector:
+        return None
+    return float(rec["traffic_bytes_per_launch"])
+
+
 def cpu_baseline(wl, seconds_hint=10.0):
     """Time the CPU oracle on a crop of the finest level (random state, the
     workload's level-0 weights), a few NCA steps."""
@@ -109,6 +139,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="pathology184mp")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer 3 times (calibrates the HBM "
+                         "byte counters of a profiler against a kernel of known traffic)")
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
@@ -119,6 +152,17 @@ def main(argv=None):
 
     import numpy as np
     import torch
+
+    if args.copy_probe:
+        n = args.copy_probe * (1 << 20)
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(1)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 3}))
+        return 0
 
     import paper_2508_06993_amd as octnca
     from paper_2508_06993_amd.runtime import Inference, upload_weights, to_device_image
@@ -194,7 +238,8 @@ def main(argv=None):
         "peak": round(peak, 1),
         "unit": unit,
         "frac": round(achieved / peak, 4),
-        "traffic": None,
+        "traffic": measured_traffic(wl, os.environ.get("OCTREE_NCA_STEP_KERNEL", "mfma")),
+        "traffic_unit": "bytes per launch (HBM, profiler counters)",
         "arithmetic": arith,
         "achieved_tflops": round(achieved_tflops, 3),
         "arith_peak_tflops": round(arith_peak, 1),

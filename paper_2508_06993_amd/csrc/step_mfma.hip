@@ -54,10 +54,22 @@ __device__ __forceinline__ int feature_of(int slot, int g) {
     return slot < 4 ? 4 * g + slot : kC + 4 * g + (slot - 4);
 }
 
+// Marks a register value as produced here (an empty asm that reads and
+// rewrites it): loads of kernel-wide constants then complete in the prologue
+// instead of being sunk into the tile loop, where the compiler would have to
+// wait for all outstanding memory operations at their first use.
+template <typename V>
+__device__ __forceinline__ void pin(V &x) {
+    asm volatile("" : "+v"(x));
+}
+
 // ---------------------------------------------------------------------------
 // MLP policies.  Each gathers its weights into lane registers once per block
 // (load) and computes the update of channels 4g..4g+3 of the lane's cell from
-// its 8 features (update).  All accumulate in fp32.
+// its 8 features in two halves: layer1 (features -> hidden accumulators, all
+// MFMA) and layer2 (ReLU, hidden -> update).  Splitting them lets a wave
+// issue the next group's perception while layer 1's MFMAs run.  All
+// accumulate in fp32.
 // ---------------------------------------------------------------------------
 
 // ReLU as an integer max on the float's bits: negative floats (sign bit set)
@@ -71,6 +83,17 @@ struct MlpF32 {
     float w1[4][8];   // [jt][kc] = W1[jt*16 + n][feature(kc, g)]
     v4f b1[4];        // [jt][i]  = b1[jt*16 + 4g + i]
     float w2[4][4];   // [jt][i]  = W2[n][jt*16 + 4g + i]   (n = output channel)
+
+    __device__ __forceinline__ void pin_all() {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) pin(w1[jt][k]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) pin(w2[jt][i]);
+            pin(b1[jt]);
+        }
+    }
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
                                          const float *__restrict__ W2, int n, int g) {
@@ -86,8 +109,7 @@ struct MlpF32 {
         }
     }
 
-    __device__ __forceinline__ v4f update(const float f[8]) const {
-        v4f acc[4];
+    __device__ __forceinline__ void layer1(const float f[8], v4f acc[4]) const {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[jt][0], f[0], b1[jt], 0, 0, 0);
@@ -96,6 +118,9 @@ struct MlpF32 {
 #pragma unroll
             for (int jt = 0; jt < 4; ++jt)
                 acc[jt] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1[jt][kc], f[kc], acc[jt], 0, 0, 0);
+    }
+
+    __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
         v4f u0 = {0.f, 0.f, 0.f, 0.f}, u1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
@@ -145,6 +170,20 @@ struct MlpBf16x3 {
     v4f b1[4];
     v8bf w2h[2], w2l[2];   // [p] slot s: W2[n][hidden(p, s, g)]
 
+    __device__ __forceinline__ void pin_all() {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            pin(w1h[jt]);
+            pin(w1l[jt]);
+            pin(b1[jt]);
+        }
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            pin(w2h[p]);
+            pin(w2l[p]);
+        }
+    }
+
     // hidden unit in K slot s of layer-2 MFMA p for lane group g: it is the
     // layer-1 accumulator register (jt = 2p + s/4, i = s%4) of the lane.
     __device__ static __forceinline__ int hidden_of(int p, int s, int g) {
@@ -171,13 +210,12 @@ struct MlpBf16x3 {
         }
     }
 
-    __device__ __forceinline__ v4f update(const float f[8]) const {
+    __device__ __forceinline__ void layer1(const float f[8], v4f acc[4]) const {
         v8f fx;
 #pragma unroll
         for (int s = 0; s < 8; ++s) fx[s] = f[s];
         v8bf fh, fl;
         split_bf16(fx, fh, fl);
-        v4f acc[4];
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1l[jt], fh, b1[jt], 0, 0, 0);
@@ -187,6 +225,9 @@ struct MlpBf16x3 {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w1h[jt], fh, acc[jt], 0, 0, 0);
+    }
+
+    __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
         v8bf hh[2], hl[2];
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -217,6 +258,16 @@ struct MlpF16 {
     v4f b1[4];
     v8h w2[2];
 
+    __device__ __forceinline__ void pin_all() {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            pin(w1[jt]);
+            pin(b1[jt]);
+        }
+        pin(w2[0]);
+        pin(w2[1]);
+    }
+
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
                                          const float *__restrict__ W2, int n, int g) {
 #pragma unroll
@@ -237,15 +288,17 @@ struct MlpF16 {
         }
     }
 
-    __device__ __forceinline__ v4f update(const float f[8]) const {
+    __device__ __forceinline__ void layer1(const float f[8], v4f acc[4]) const {
         v8f fx;
 #pragma unroll
         for (int s = 0; s < 8; ++s) fx[s] = f[s];
         const v8h fh = __builtin_convertvector(fx, v8h);
-        v4f acc[4];
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1[jt], fh, b1[jt], 0, 0, 0);
+    }
+
+    __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
         v4f u = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -259,9 +312,14 @@ struct MlpF16 {
     }
 };
 
-// Fire bits for the quads of up to four rows of cells (16 quads per row).
-// Lane L evaluates quad q0[L / 16] + L % 16; bit (word k, quad offset o of
-// row r) is bit 16 r + o of ballot k.
+// Fire bits.  One Philox4x64-10 evaluation gives the bits of a quad of 4
+// consecutive cells, so a wave evaluates one quad per lane and spreads the
+// bits with four ballots (one per output word).  Lanes are assigned to row
+// slots of `qpr` quads each: bit (slot, quad offset o) of ballot k holds the
+// bit of cell 4 (q0(slot) + o) + k, q0(slot) = (canonical index of the slot's
+// first cell) >> 2.  When rows start on a quad boundary (w % 4 == 0) a row of
+// 32 cells is exactly 8 quads and one evaluation covers 8 row slots (2 tiles
+// in 2D, 4 planes in 3D); otherwise rows use 16 quads and 4 slots.
 struct FireBallots {
     uint64_t w[4];
 };
@@ -277,97 +335,175 @@ __device__ __forceinline__ FireBallots fire_ballots(uint64_t quad, uint32_t step
     return b;
 }
 
-__device__ __forceinline__ bool fire_bit(const FireBallots &b, int row_slot, uint64_t idx,
+__device__ __forceinline__ bool fire_bit(const FireBallots &b, int slot, int qpr, uint64_t idx,
                                          uint64_t row_quad0) {
     const int o = (int)((idx >> 2) - row_quad0);
-    const int k = (int)(idx & 3);
-    const uint64_t w = k == 0 ? b.w[0] : k == 1 ? b.w[1] : k == 2 ? b.w[2] : b.w[3];
-    return (w >> (16 * row_slot + o)) & 1;
+    const uint32_t k = (uint32_t)idx & 3u;
+    // word k of the quad, selected without branches
+    const uint64_t lo = (k & 1u) ? b.w[1] : b.w[0];
+    const uint64_t hi = (k & 1u) ? b.w[3] : b.w[2];
+    const uint64_t w = (k & 2u) ? hi : lo;
+    return (w >> (slot * qpr + o)) & 1;
 }
 
 // ---------------------------------------------------------------------------
-// Halo tiles: a tile of cells (plus a one-cell halo) is read from HBM in
-// 16-byte chunks, consecutive threads taking consecutive chunks (coalesced),
-// and kept in LDS as fp32 in four channel-quad planes, so that the 16 lanes
-// of a quad read 16 consecutive 16-byte words (no bank conflicts).  The plane
-// stride is 2 mod 8 (in 16-byte words) so the four planes of one cell sit in
-// different bank groups.  Loads go through registers: the next tile's loads
-// are issued before the current tile is computed and written to LDS after it
-// (software pipelining), so HBM latency overlaps the compute.
+// Halo tiles: HY rows of 34 cells (a 32-cell-wide interior plus one halo cell
+// on each side) of one z plane.  In LDS they are kept as fp32 in four
+// channel-quad planes, so that the 16 lanes of a quad read 16 consecutive
+// 16-byte words (no bank conflicts); the plane stride is 2 mod 8 (16-byte
+// words, see plane_stride).
+// Loads are whole 16-byte chunks: a "body" load moves the 64 chunks of a row
+// segment (16 cells in fp32, 32 in fp16) from one wave-uniform address, a
+// "side" load moves the left and right halo cells of several rows.  The loads are spread over the 4 waves
+// and go through registers: the next tile's loads are issued before the
+// current tile is computed and written to LDS after it (software
+// pipelining), so HBM latency overlaps the compute.
 // ---------------------------------------------------------------------------
 template <typename T> struct CellChunks;
 template <> struct CellChunks<float> { static constexpr int N = 4; };    // 16 B = 4 channels
 template <> struct CellChunks<__half> { static constexpr int N = 2; };   // 16 B = 8 channels
 
-constexpr int plane_stride(int cells) { return (cells + 7) / 8 * 8 + 2; }
+// Plane stride rounded up to 16 words (256 B): measured on gfx950, strides of
+// 2, 4 and 12 words mod 16 left the 16-lane plane reads with ~20x more LDS
+// bank-conflict cycles than this choice.
+constexpr int plane_stride(int cells) { return (cells + 15) / 16 * 16; }
+constexpr int kTileW = 32;
+constexpr int kHaloW = kTileW + 2;
 
-template <typename T, int HY, int HX>
-struct HaloLoader {
-    static constexpr int kCells = HY * HX;
+// Buffer resources: every global access of the step kernel goes through a
+// raw buffer descriptor whose range covers only the rows a tile may touch;
+// an out-of-range offset (0xffffffff is used for cells outside the grid)
+// reads 0 and drops a store.  So no load or store sits behind a branch, the
+// compiler sees a fixed sequence of vector-memory operations per tile, and
+// waits for the prefetched loads without draining the stores (loads and
+// stores share one completion counter).
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
+constexpr uint32_t kOut = 0xffffffffu;      // offset that is always out of range
+constexpr int kRsrcWord3 = 0x00020000;      // raw buffer, 32-bit data format
+
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, kRsrcWord3);
+}
+
+template <typename T, int HY>
+struct RowLoader {
     static constexpr int NQ = CellChunks<T>::N;
-    static constexpr int kChunks = kCells * NQ;
-    static constexpr int NCH = (kChunks + kThreads - 1) / kThreads;
-    static constexpr int PS = plane_stride(kCells);
-    uint4 v[NCH];
+    static constexpr int kCellBytes = kC * (int)sizeof(T);
+    static constexpr int kCellsPerBody = 64 / NQ;            // cells per body load
+    static constexpr int kBodyPerRow = kTileW / kCellsPerBody;
+    static constexpr int kRowsPerSide = 64 / (2 * NQ);       // rows per side load
+    static constexpr int kBody = HY * kBodyPerRow;
+    static constexpr int kSide = (HY + kRowsPerSide - 1) / kRowsPerSide;
+    static constexpr int kBodySlots = (kBody + 3) / 4;       // body loads per wave (max)
+    static_assert(kSide <= 4, "one side load per wave at most");
+    static constexpr int PS = plane_stride(HY * kHaloW);
+    // Body load J (0 <= J < kBody) is slot J / 4 of wave J % 4: every wave
+    // runs the same instruction sequence.  Side load s is done by wave 3 - s,
+    // in one extra slot.
+    uint4 v[kBodySlots + 1];
 
-    // Halo plane z (ignored for 2D: pass z = 0, dd = 1) of the tile whose
-    // interior starts at (y0, x0); cells outside the grid read as zero.
+    // A body load moves the kCellsPerBody cells x NQ chunks of a row segment.
+    // Lane i takes chunk i / kCellsPerBody of cell i % kCellsPerBody: the
+    // wave still reads one contiguous 1 KB, and each group of consecutive
+    // lanes writes consecutive 16-byte words of one LDS plane (no bank
+    // conflicts on the commit).
+    __device__ static __forceinline__ int body_cell(int lane) { return lane % kCellsPerBody; }
+    __device__ static __forceinline__ int body_chunk(int lane) { return lane / kCellsPerBody; }
+
+    // Tile whose interior starts at (y0, x0) in plane z; cells outside the
+    // grid (or z outside [0, dd)) read as zero.  The grid must satisfy
+    // HY * dw * kCellBytes < 2^32 (checked by the launcher).
+    // With active = false nothing is read (every offset is out of range) and
+    // the registers are zero: the next-tile prefetch is issued unconditionally.
     __device__ __forceinline__ void issue(const T *__restrict__ src, int z, int dd, int dh, int dw,
-                                          int y0, int x0) {
-        const bool zin = z >= 0 && z < dd;
+                                          int y0, int x0, bool active = true) {
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int gy0 = y0 - 1;
+        const int base_row = gy0 > 0 ? gy0 : 0;
+        const int rows =
+            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
+        const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
+        const Rsrc r = make_rsrc(src + ((int64_t)max(z, 0) * dh + base_row) * dw * kC,
+                                 (uint32_t)rows * row_bytes);
+        const int cell = body_cell(lane);
+        const uint32_t lane_off = (uint32_t)(cell * kCellBytes + body_chunk(lane) * 16);
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int i = (int)threadIdx.x + c * kThreads;
-            const int q = i % NQ;
-            const int cell = i / NQ;
-            const int ly = cell / HX, lx = cell - (cell / HX) * HX;
-            const int gy = y0 + ly - 1, gx = x0 + lx - 1;
-            const bool valid = i < kChunks && zin && gy >= 0 && gy < dh && gx >= 0 && gx < dw;
-            v[c] = make_uint4(0u, 0u, 0u, 0u);
-            if (valid) {
-                const int64_t gcell = ((int64_t)z * dh + gy) * dw + gx;
-                v[c] = reinterpret_cast<const uint4 *>(src + gcell * kC)[q];
-            }
+        for (int k = 0; k < kBodySlots; ++k) {
+            const int J = wave + 4 * k;                       // wave-uniform
+            const int gy = gy0 + J / kBodyPerRow;
+            const int cx0 = x0 + (J % kBodyPerRow) * kCellsPerBody;
+            const bool ok = J < kBody && gy >= 0 && cx0 + cell < dw;
+            const uint32_t off = (uint32_t)(gy - base_row) * row_bytes +
+                                 (uint32_t)cx0 * kCellBytes + lane_off;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const int s = 3 - wave;
+        const int row = s * kRowsPerSide + lane / (2 * NQ);
+        const int gy = gy0 + row;
+        const int gx = ((lane / NQ) & 1) ? x0 + kTileW : x0 - 1;
+        const bool ok = s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw;
+        const uint32_t off = (uint32_t)(gy - base_row) * row_bytes + (uint32_t)gx * kCellBytes +
+                             (uint32_t)(lane % NQ) * 16;
+        const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
+        v[kBodySlots] = make_uint4(x[0], x[1], x[2], x[3]);
+    }
+
+__device__ __forceinline__ static void put(float4 *planes, int q, int cell, const uint4 &c) {
+        if constexpr (NQ == 4) {
+            planes[q * PS + cell] = make_float4(__uint_as_float(c.x), __uint_as_float(c.y),
+                                                __uint_as_float(c.z), __uint_as_float(c.w));
+        } else {
+            float f[8];
+            Storage<__half>::unpack(c, f);
+            planes[(2 * q) * PS + cell] = make_float4(f[0], f[1], f[2], f[3]);
+            planes[(2 * q + 1) * PS + cell] = make_float4(f[4], f[5], f[6], f[7]);
         }
     }
 
+    // LDS slot that is never read (plane padding): target of the writes of
+    // unused load slots, so the commit has no branches either.
+    static constexpr int kDummyCell = HY * kHaloW;
+    static_assert(kDummyCell < PS, "plane padding holds the dummy slot");
+
     __device__ __forceinline__ void commit(float4 *planes) const {
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int cell = body_cell(lane), chunk = body_chunk(lane);
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int i = (int)threadIdx.x + c * kThreads;
-            if (i < kChunks) {
-                const int q = i % NQ;
-                const int cell = i / NQ;
-                if constexpr (NQ == 4) {
-                    planes[q * PS + cell] = make_float4(__uint_as_float(v[c].x),
-                                                        __uint_as_float(v[c].y),
-                                                        __uint_as_float(v[c].z),
-                                                        __uint_as_float(v[c].w));
-                } else {
-                    float f[8];
-                    Storage<__half>::unpack(v[c], f);
-                    planes[(2 * q) * PS + cell] = make_float4(f[0], f[1], f[2], f[3]);
-                    planes[(2 * q + 1) * PS + cell] = make_float4(f[4], f[5], f[6], f[7]);
-                }
-            }
+        for (int k = 0; k < kBodySlots; ++k) {
+            const int J = wave + 4 * k;
+            const int slot =
+                (J / kBodyPerRow) * kHaloW + 1 + (J % kBodyPerRow) * kCellsPerBody + cell;
+            put(planes, chunk, J < kBody ? slot : kDummyCell, v[k]);
         }
+        const int s = 3 - wave;
+        const int row = s * kRowsPerSide + lane / (2 * NQ);
+        const int slot = row * kHaloW + (((lane / NQ) & 1) ? kHaloW - 1 : 0);
+        put(planes, lane % NQ, (s < kSide && row < HY) ? slot : kDummyCell, v[kBodySlots]);
     }
 };
 
 // Residual update and store of the lane's 4 channels (fp32 values, stored in
-// the storage type).  upd[k] is 0 for input channels, 1 otherwise; with
-// m * upd = 0 the fma returns the state bit for bit (u is finite).
-__device__ __forceinline__ void store_quad(float *dst, int64_t cell, int g, v4f v) {
-    *reinterpret_cast<float4 *>(dst + cell * kC + 4 * g) = make_float4(v[0], v[1], v[2], v[3]);
+// the storage type) through the tile's store descriptor; `off` is the byte
+// offset of the cell in it, or kOut for a cell outside the grid.  upd[k] is
+// 0 for input channels, 1 otherwise; with m * upd = 0 the fma returns the
+// state bit for bit (u is finite).
+__device__ __forceinline__ void store_quad(float *, Rsrc w, uint32_t off, int g, const v4f &v) {
+    const v4u x = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                   __float_as_uint(v[3])};
+    __builtin_amdgcn_raw_buffer_store_b128(x, w, off == kOut ? kOut : off + 16u * g, 0, 0);
 }
-__device__ __forceinline__ void store_quad(__half *dst, int64_t cell, int g, v4f v) {
-    const uint32_t lo = Storage<__half>::pack_pair(v[0], v[1]);
-    const uint32_t hi = Storage<__half>::pack_pair(v[2], v[3]);
-    *reinterpret_cast<uint2 *>(dst + cell * kC + 4 * g) = make_uint2(lo, hi);
+__device__ __forceinline__ void store_quad(__half *, Rsrc w, uint32_t off, int g, const v4f &v) {
+    const v2u x = {Storage<__half>::pack_pair(v[0], v[1]), Storage<__half>::pack_pair(v[2], v[3])};
+    __builtin_amdgcn_raw_buffer_store_b64(x, w, off == kOut ? kOut : off + 8u * g, 0, 0);
 }
 
 template <typename T>
-__device__ __forceinline__ void update_store(T *dst, int64_t idx, int g, const float f[8],
+__device__ __forceinline__ void update_store(T *tag, Rsrc w, uint32_t off, int g, const float f[8],
                                              const v4f &u, const float upd[4], bool fire) {
     const float m = fire ? 1.f : 0.f;
     v4f out;
@@ -375,105 +511,197 @@ __device__ __forceinline__ void update_store(T *dst, int64_t idx, int g, const f
     out[1] = fmaf(m * upd[1], u[1], f[1]);
     out[2] = fmaf(m * upd[2], u[2], f[2]);
     out[3] = fmaf(m * upd[3], u[3], f[3]);
-    store_quad(dst, idx, g, out);
+    store_quad(tag, w, off, g, out);
+}
+
+// Perception of channels 4g..4g+3 of the cell at LDS slot `centre`: the
+// cell's own state in f[0..4), bias + taps in f[4..8).  `pl` points at the
+// lane's channel-quad plane(s); tapw holds the conv weights as [tap][quad].
+__device__ __forceinline__ void perceive_2d(const float4 *pl, const float4 (*tapw)[4], int g,
+                                            int centre, const float cb[4], float f[8]) {
+    const float4 sv = pl[centre];
+    f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
+    float p[4] = {cb[0], cb[1], cb[2], cb[3]};
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+        const float4 v = pl[centre + (t / 3 - 1) * kHaloW + (t % 3 - 1)];
+        const float4 w = tapw[t][g];
+        p[0] = fmaf(w.x, v.x, p[0]);
+        p[1] = fmaf(w.y, v.y, p[1]);
+        p[2] = fmaf(w.z, v.z, p[2]);
+        p[3] = fmaf(w.w, v.w, p[3]);
+    }
+    f[4] = p[0]; f[5] = p[1]; f[6] = p[2]; f[7] = p[3];
+}
+
+// 3D: planes z-1, z, z+1 of the ring; taps in order (dz, dy, dx), one plane
+// at a time (bounds the LDS values in flight and the registers).
+__device__ __forceinline__ void perceive_3d(const float4 *pm, const float4 *pc, const float4 *pp,
+                                            const float4 (*tapw)[4], int g, int centre,
+                                            const float cb[4], float f[8]) {
+    const float4 sv = pc[centre];
+    f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
+    float p[4] = {cb[0], cb[1], cb[2], cb[3]};
+#pragma unroll 1
+    for (int pz = 0; pz < 3; ++pz) {
+        const float4 *pl = pz == 0 ? pm : pz == 1 ? pc : pp;
+#pragma unroll
+        for (int tt = 0; tt < 9; ++tt) {
+            const float4 v = pl[centre + (tt / 3 - 1) * kHaloW + (tt % 3 - 1)];
+            const float4 w = tapw[pz * 9 + tt][g];
+            p[0] = fmaf(w.x, v.x, p[0]);
+            p[1] = fmaf(w.y, v.y, p[1]);
+            p[2] = fmaf(w.z, v.z, p[2]);
+            p[3] = fmaf(w.w, v.w, p[3]);
+        }
+    }
+    f[4] = p[0]; f[5] = p[1]; f[6] = p[2]; f[7] = p[3];
 }
 
 // ---------------------------------------------------------------------------
-// 2D: persistent blocks loop over 16 x 32 tiles (tile index row-major).
+// 2D: persistent blocks loop over 16 x 32 tiles (tile index row-major); wave
+// w computes rows 4w .. 4w+3 of the tile, 8 groups of 16 cells.
 // ---------------------------------------------------------------------------
-constexpr int k2TY = 16, k2TX = 32;
-constexpr int k2HY = k2TY + 2, k2HX = k2TX + 2;
+constexpr int k2TY = 16;
+constexpr int k2BlocksPerCu = 2;   // 2 waves per SIMD: <= 256 VGPRs
 
 template <typename T, int NIN, class Mlp>
-__global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_2d(
+__global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int tiles_x, int tiles,
     const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
-    using Loader = HaloLoader<T, k2HY, k2HX>;
+    using Loader = RowLoader<T, k2TY + 2>;
     __shared__ float4 planes[4 * Loader::PS];
+    __shared__ float4 tapw[9][4];       // [tap][quad] conv weights of channels 4q..4q+3
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
     const int g = lane >> 4;
 
+    {
+        const int i = min((int)threadIdx.x, 9 * 4 - 1);
+        const int t = i / 4, q = i % 4;
+        const float4 tw = make_float4(conv_w[(4 * q + 0) * 9 + t], conv_w[(4 * q + 1) * 9 + t],
+                                      conv_w[(4 * q + 2) * 9 + t], conv_w[(4 * q + 3) * 9 + t]);
+        if (threadIdx.x < 9 * 4) tapw[t][q] = tw;
+    }
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g);
-    float cw[9][4];
     float cb[4];
     float upd[4];   // channels < NIN are copied, never updated
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         cb[k] = conv_b[4 * g + k];
         upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
-#pragma unroll
-        for (int t = 0; t < 9; ++t) cw[t][k] = conv_w[(4 * g + k) * 9 + t];
     }
+    // all weight loads done before the tile loop (keeps the compiler's
+    // vector-memory counting exact inside it)
+    mlp.pin_all();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        pin(cb[k]);
+        pin(upd[k]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // rows start on a quad boundary: one fire evaluation serves two tiles
+    const bool aligned = (dw & 3) == 0;
+    const int qpr = aligned ? 8 : 16;
+    const int stride = (int)gridDim.x;
+    constexpr int kCellBytes = Loader::kCellBytes;
+    const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
 
+    // The tile's halo is in LDS when an iteration starts: the first tile is
+    // staged here, each later one is loaded during the previous iteration's
+    // compute and written to LDS at its end (so every wait for those loads
+    // sees the same history of memory operations).
     Loader ld;
     int tile = blockIdx.x;
     if (tile < tiles) {
         const int ty = tile / tiles_x;
-        ld.issue(src, 0, 1, dh, dw, ty * k2TY, (tile - ty * tiles_x) * k2TX);
-    }
-    for (; tile < tiles; tile += gridDim.x) {
-        const int ty = tile / tiles_x;
-        const int y0 = ty * k2TY, x0 = (tile - ty * tiles_x) * k2TX;
+        ld.issue(src, 0, 1, dh, dw, ty * k2TY, (tile - ty * tiles_x) * kTileW);
         ld.commit(planes);
-        // fire bits of the wave's 4 rows (rows 4*wave .. 4*wave+3 of the tile)
-        const uint64_t brow_idx = (uint64_t)(y0 + 4 * wave + (lane >> 4)) * dw + x0;
-        const FireBallots fb =
-            fire_ballots((brow_idx >> 2) + (lane & 15), step, level, seed, threshold);
+    }
+    FireBallots fb;
+    for (int iter = 0; tile < tiles; tile += stride, ++iter) {
+        const int ty = tile / tiles_x;
+        const int y0 = ty * k2TY, x0 = (tile - ty * tiles_x) * kTileW;
+        int slot0 = 0;
+        if (aligned) {
+            // lanes 0-31: this tile, lanes 32-63: this block's next tile
+            if ((iter & 1) == 0) {
+                int t2 = tile + (lane >> 5) * stride;
+                t2 = t2 < tiles ? t2 : tile;
+                const int ty2 = t2 / tiles_x;
+                const uint64_t row = (uint64_t)(ty2 * k2TY + 4 * wave + ((lane >> 3) & 3));
+                const uint64_t q0 = (row * dw + (uint64_t)(t2 - ty2 * tiles_x) * kTileW) >> 2;
+                fb = fire_ballots(q0 + (lane & 7), step, level, seed, threshold);
+            } else {
+                slot0 = 4;
+            }
+        } else {
+            const uint64_t row = (uint64_t)(y0 + 4 * wave + (lane >> 4));
+            fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 15), step, level, seed, threshold);
+        }
         __syncthreads();
-        const int next = tile + (int)gridDim.x;
-        if (next < tiles) {
-            const int nty = next / tiles_x;
-            ld.issue(src, 0, 1, dh, dw, nty * k2TY, (next - nty * tiles_x) * k2TX);
+        {
+            const int next = tile + stride;
+            const bool more = next < tiles;
+            const int nt = more ? next : tile;
+            const int nty = nt / tiles_x;
+            ld.issue(src, 0, 1, dh, dw, nty * k2TY, (nt - nty * tiles_x) * kTileW, more);
         }
 
+        // stores of this tile: rows y0 .. y0 + k2TY - 1 (clipped to the grid)
+        const Rsrc wr = make_rsrc(dst + (int64_t)y0 * dw * kC,
+                                  (uint32_t)min(k2TY, dh - y0) * row_bytes);
+        // groups are software-pipelined: group grp + 1's perception is issued
+        // while group grp's first-layer MFMAs run
         const float4 *pl = planes + g * Loader::PS;
-#pragma unroll 1
-        for (int grp = 0; grp < 8; ++grp) {
-            const int r = grp >> 1;                 // row slot within the wave
-            const int cx = (grp & 1) * 16 + n;      // column within the tile
-            const int ly = 4 * wave + r;
-            const int centre = (ly + 1) * k2HX + cx + 1;
-
-            float f[8];
-            const float4 sv = pl[centre];
-            f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
-            float p[4] = {cb[0], cb[1], cb[2], cb[3]};
+        auto centre_of = [&](int grp) {
+            return (4 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
+        };
+        float f[8];
+        perceive_2d(pl, tapw, g, centre_of(0), cb, f);
+        // fully unrolled: with a counted sequence of stores the compiler can
+        // wait for the prefetched loads alone (stores share the vector-memory
+        // counter), instead of draining every store of the tile
 #pragma unroll
-            for (int t = 0; t < 9; ++t) {
-                const float4 v = pl[centre + (t / 3 - 1) * k2HX + (t % 3 - 1)];
-                p[0] = fmaf(cw[t][0], v.x, p[0]);
-                p[1] = fmaf(cw[t][1], v.y, p[1]);
-                p[2] = fmaf(cw[t][2], v.z, p[2]);
-                p[3] = fmaf(cw[t][3], v.w, p[3]);
-            }
-            f[4] = p[0]; f[5] = p[1]; f[6] = p[2]; f[7] = p[3];
+        for (int grp = 0; grp < 8; ++grp) {
+            v4f acc[4];
+            mlp.layer1(f, acc);
+            float fn[8];
+            if (grp < 7) perceive_2d(pl, tapw, g, centre_of(grp + 1), cb, fn);
+            const v4f u = mlp.layer2(acc);
 
-            const v4f u = mlp.update(f);
-
-            const int y = y0 + ly, x = x0 + cx;
-            if (y < dh && x < dw) {
-                const uint64_t idx = (uint64_t)y * dw + x;
-                const uint64_t row_q0 = ((uint64_t)y * dw + x0) >> 2;
-                update_store(dst, (int64_t)idx, g, f, u, upd, fire_bit(fb, r, idx, row_q0));
-            }
+            const int r = grp >> 1;                 // row slot within the wave
+            const int ly = 4 * wave + r;
+            const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
+            const uint64_t idx = (uint64_t)y * dw + x;
+            const uint64_t row_q0 = ((uint64_t)y * dw + x0) >> 2;
+            const uint32_t off = x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
+            update_store(dst, wr, off, g, f, u, upd, fire_bit(fb, slot0 + r, qpr, idx, row_q0));
+#pragma unroll
+            for (int k = 0; k < 8; ++k) f[k] = fn[k];
+            // keep the scheduler from interleaving whole groups (register pressure)
+            __builtin_amdgcn_sched_barrier(0);
         }
         __syncthreads();
+        ld.commit(planes);   // the next tile (zeros when there is none)
     }
 }
 
 // ---------------------------------------------------------------------------
 // 3D: a work item is an 8 x 32 (y, x) column and a run of z planes; planes
 // stream through a ring of three halo planes in LDS, the plane after next
-// being loaded while the current one is computed.
+// being loaded while the current one is computed.  Wave w computes rows
+// 2w, 2w+1 of each plane (4 groups of 16 cells).
 // ---------------------------------------------------------------------------
-constexpr int k3TY = 8, k3TX = 32;
-constexpr int k3HY = k3TY + 2, k3HX = k3TX + 2;
+constexpr int k3TY = 8;
 constexpr int k3ZRun = 16;    // z planes per work item
 
 template <typename T, int NIN, class Mlp>
@@ -482,19 +710,21 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     int tiles_y, int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
-    using Loader = HaloLoader<T, k3HY, k3HX>;
+    using Loader = RowLoader<T, k3TY + 2>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 15;
     const int g = lane >> 4;
 
-    for (int i = threadIdx.x; i < 27 * 4; i += kThreads) {
+    {
+        const int i = min((int)threadIdx.x, 27 * 4 - 1);
         const int t = i / 4, q = i % 4;
-        tapw[t][q] = make_float4(conv_w[(4 * q + 0) * 27 + t], conv_w[(4 * q + 1) * 27 + t],
-                                 conv_w[(4 * q + 2) * 27 + t], conv_w[(4 * q + 3) * 27 + t]);
+        const float4 tw = make_float4(conv_w[(4 * q + 0) * 27 + t], conv_w[(4 * q + 1) * 27 + t],
+                                      conv_w[(4 * q + 2) * 27 + t], conv_w[(4 * q + 3) * 27 + t]);
+        if (threadIdx.x < 27 * 4) tapw[t][q] = tw;
     }
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g);
@@ -505,8 +735,24 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         cb[k] = conv_b[4 * g + k];
         upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
     }
+    mlp.pin_all();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        pin(cb[k]);
+        pin(upd[k]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // rows start on a quad boundary: one fire evaluation serves four planes
+    const bool aligned = (dw & 3) == 0;
+    const int qpr = aligned ? 8 : 16;
+    constexpr int kCellBytes = Loader::kCellBytes;
+    const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
     Loader ld;
+    FireBallots fb;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         int rest = item;
@@ -514,67 +760,76 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         rest /= zruns;
         const int tx = rest % tiles_x;
         const int ty = rest / tiles_x;
-        const int y0 = ty * k3TY, x0 = tx * k3TX;
+        const int y0 = ty * k3TY, x0 = tx * kTileW;
         const int z_begin = zr * k3ZRun;
         const int z_end = min(dd, z_begin + k3ZRun);
 
+        // planes z_begin - 1 .. z_begin + 1 are staged here; each later plane
+        // is loaded while the plane two before it is computed and written to
+        // the ring at the end of that iteration
         __syncthreads();   // the previous item's readers are done with the ring
         ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
         ld.commit(ring[(z_begin + 2) % 3]);
         ld.issue(src, z_begin, dd, dh, dw, y0, x0);
         ld.commit(ring[z_begin % 3]);
         ld.issue(src, z_begin + 1, dd, dh, dw, y0, x0);
+        ld.commit(ring[(z_begin + 1) % 3]);
 
         for (int z = z_begin; z < z_end; ++z) {
-            ld.commit(ring[(z + 1) % 3]);
-            // fire bits of the wave's 2 rows of this plane
-            const uint64_t brow_idx =
-                ((uint64_t)z * dh + (y0 + 2 * wave + ((lane >> 4) & 1))) * dw + x0;
-            const FireBallots fb =
-                fire_ballots((brow_idx >> 2) + (lane & 15), step, level, seed, threshold);
+            int slot0 = 0;
+            if (aligned) {
+                // lane group pz = lane / 16 evaluates plane z + pz (pz < 4)
+                if (((z - z_begin) & 3) == 0) {
+                    const int zz = min(z + (lane >> 4), dd - 1);
+                    const uint64_t row =
+                        (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> 3) & 1));
+                    fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 7), step, level, seed,
+                                      threshold);
+                }
+                slot0 = 2 * ((z - z_begin) & 3);
+            } else {
+                const uint64_t row = (uint64_t)z * dh + (uint64_t)(y0 + 2 * wave + ((lane >> 4) & 1));
+                fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 15), step, level, seed,
+                                  threshold);
+            }
             __syncthreads();
-            if (z + 2 <= z_end) ld.issue(src, z + 2, dd, dh, dw, y0, x0);
+            // plane z + 2 (needed by the next plane; after the run's last
+            // plane nothing is read)
+            ld.issue(src, z + 2, dd, dh, dw, y0, x0, z + 1 < z_end);
 
+            // stores of this plane: rows y0 .. y0 + k3TY - 1 (clipped to the grid)
+            const Rsrc wr = make_rsrc(dst + ((int64_t)z * dh + y0) * dw * kC,
+                                      (uint32_t)min(k3TY, dh - y0) * row_bytes);
             const float4 *pm = ring[(z + 2) % 3] + g * Loader::PS;   // plane z - 1
             const float4 *pc = ring[z % 3] + g * Loader::PS;         // plane z
             const float4 *pp = ring[(z + 1) % 3] + g * Loader::PS;   // plane z + 1
-#pragma unroll 1
-            for (int grp = 0; grp < 4; ++grp) {
-                const int r = grp >> 1;
-                const int cx = (grp & 1) * 16 + n;
-                const int ly = 2 * wave + r;
-                const int centre = (ly + 1) * k3HX + cx + 1;
-                float f[8];
-                const float4 sv = pc[centre];
-                f[0] = sv.x; f[1] = sv.y; f[2] = sv.z; f[3] = sv.w;
-                float p[4] = {cb[0], cb[1], cb[2], cb[3]};
-                // taps in order (dz, dy, dx); one plane at a time keeps the
-                // number of LDS values in flight (and registers) bounded
-#pragma unroll 1
-                for (int pz = 0; pz < 3; ++pz) {
-                    const float4 *pl = pz == 0 ? pm : pz == 1 ? pc : pp;
+            auto centre_of = [&](int grp) {
+                return (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
+            };
+            float f[8];
+            perceive_3d(pm, pc, pp, tapw, g, centre_of(0), cb, f);
 #pragma unroll
-                    for (int tt = 0; tt < 9; ++tt) {
-                        const float4 v = pl[centre + (tt / 3 - 1) * k3HX + (tt % 3 - 1)];
-                        const float4 w = tapw[pz * 9 + tt][g];
-                        p[0] = fmaf(w.x, v.x, p[0]);
-                        p[1] = fmaf(w.y, v.y, p[1]);
-                        p[2] = fmaf(w.z, v.z, p[2]);
-                        p[3] = fmaf(w.w, v.w, p[3]);
-                    }
-                }
-                f[4] = p[0]; f[5] = p[1]; f[6] = p[2]; f[7] = p[3];
+            for (int grp = 0; grp < 4; ++grp) {
+                v4f acc[4];
+                mlp.layer1(f, acc);
+                float fn[8];
+                if (grp < 3) perceive_3d(pm, pc, pp, tapw, g, centre_of(grp + 1), cb, fn);
+                const v4f u = mlp.layer2(acc);
 
-                const v4f u = mlp.update(f);
-
-                const int y = y0 + ly, x = x0 + cx;
-                if (y < dh && x < dw) {
-                    const uint64_t idx = ((uint64_t)z * dh + y) * dw + x;
-                    const uint64_t row_q0 = (((uint64_t)z * dh + y) * dw + x0) >> 2;
-                    update_store(dst, (int64_t)idx, g, f, u, upd, fire_bit(fb, r, idx, row_q0));
-                }
+                const int r = grp >> 1;
+                const int ly = 2 * wave + r;
+                const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
+                const uint64_t idx = ((uint64_t)z * dh + y) * dw + x;
+                const uint64_t row_q0 = (((uint64_t)z * dh + y) * dw + x0) >> 2;
+                const uint32_t off =
+                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
+                update_store(dst, wr, off, g, f, u, upd, fire_bit(fb, slot0 + r, qpr, idx, row_q0));
+#pragma unroll
+                for (int k = 0; k < 8; ++k) f[k] = fn[k];
+                __builtin_amdgcn_sched_barrier(0);
             }
-            __syncthreads();   // plane z - 1's slot is refilled next
+            __syncthreads();                    // plane z - 1's slot is free
+            ld.commit(ring[(z + 2) % 3]);       // plane z + 2 into it
         }
     }
 }
@@ -597,12 +852,12 @@ constexpr int kBlocksPerCu = 2;
 
 template <typename T, int NIN, class Mlp>
 hipError_t launch_2d(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
-    const int tiles_x = (int)((a.ext.w + k2TX - 1) / k2TX);
+    const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k2TY - 1) / k2TY);
     const int64_t tiles = (int64_t)tiles_x * tiles_y;
     if (tiles == 0) return hipSuccess;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
-    const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * kBlocksPerCu);
+    const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
     nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
         (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles, a.w.conv_w,
         a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed, a.threshold);
@@ -611,7 +866,7 @@ hipError_t launch_2d(const StepArgs &a, const void *src, void *dst, hipStream_t 
 
 template <typename T, int NIN, class Mlp>
 hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
-    const int tiles_x = (int)((a.ext.w + k3TX - 1) / k3TX);
+    const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t zruns = (a.ext.d + k3ZRun - 1) / k3ZRun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
@@ -641,6 +896,11 @@ hipError_t dispatch(const StepArgs &a, const void *src, void *dst, hipStream_t s
 
 hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, const void *src, void *dst,
                             hipStream_t stream) {
+    // Buffer descriptors address a tile's rows with 32-bit offsets: rows of
+    // more than (2^32 / 18 rows) bytes go to the vector kernel instead.
+    const int64_t cell_bytes = (int64_t)kC * (a.dtype == Dtype::F32 ? 4 : 2);
+    if ((int64_t)(k2TY + 2) * a.ext.w * cell_bytes >= (int64_t(1) << 32))
+        return launch_step_valu(a, src, dst, stream);
     if (mlp == MfmaMlp::Default)
         mlp = a.dtype == Dtype::F32 ? MfmaMlp::Bf16x3 : MfmaMlp::F16;
     if (a.dtype == Dtype::F32) {
