@@ -31,9 +31,10 @@
  *   - Fire mask (the paper draws it with PyTorch's generator; this library
  *     uses a counter-based generator so any implementation can reproduce
  *     it): Philox4x64-10 (Salmon et al., SC 2011) with counter
- *     (idx >> 2, step, level, 0) and key (seed, 0); the cell takes output
- *     word (idx & 3) and fires iff (word >> 32) < T, where
- *     T = min(2^32, floor(fire_rate * 2^32)), fire_rate in [0, 1].
+ *     (idx >> 3, step, level, 0) and key (seed, 0), one call per block of 8
+ *     cells; cell idx takes output word (idx >> 1) & 3, its upper 32 bits if
+ *     idx is odd and its lower 32 bits if even, and fires iff that draw < T,
+ *     where T = min(2^32, floor(fire_rate * 2^32)), fire_rate in [0, 1].
  *   - Weights are fp32, per level, in device memory, in the layout of
  *     octnca_level_weights.
  *   - All pointers to arrays are DEVICE pointers unless marked "host".

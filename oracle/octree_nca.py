@@ -38,7 +38,8 @@ Readings taken where the paper is silent or ambiguous (each is listed with its
 reason in the design notes): average pooling for the image pyramid, zero
 padding, cross-correlation tap order, feature order [state, perception],
 biases placed as the printed parameter counts require, one fire bit per cell
-drawn from Philox4x64-10, argmax ties resolved to the lower channel.
+drawn from Philox4x64-10 (one 32-bit half of an output word per cell), argmax
+ties resolved to the lower channel.
 """
 from __future__ import annotations
 
@@ -129,14 +130,16 @@ def fire_threshold(fire_rate: float) -> int:
 def fire_bits(seed: int, level: int, step: int, idx: np.ndarray, fire_rate: float) -> np.ndarray:
     """Fire bit of each cell with canonical linear index ``idx``
     (idx = (z*H + y)*W + x at its level).  Philox4x64-10 with counter
-    (idx >> 2, step, level, 0) and key (seed, 0); the cell uses output word
-    idx & 3, and its draw is that word's upper 32 bits."""
+    (idx >> 3, step, level, 0) and key (seed, 0) gives four 64-bit words for
+    a block of 8 consecutive cells; cell idx takes word (idx >> 1) & 3 and,
+    within it, the upper 32 bits when idx is odd, the lower 32 bits when even."""
     idx = np.asarray(idx, dtype=np.uint64)
-    quads, where = np.unique(idx >> np.uint64(2), return_inverse=True)
-    words = np.stack(philox4x64((quads, np.uint64(step), np.uint64(level), np.uint64(0)),
-                                (np.uint64(seed), np.uint64(0))), axis=-1)   # [quads][4]
-    w = words[where.reshape(idx.shape), (idx & np.uint64(3)).astype(np.intp)]
-    draw = w >> np.uint64(32)
+    octs, where = np.unique(idx >> np.uint64(3), return_inverse=True)
+    words = np.stack(philox4x64((octs, np.uint64(step), np.uint64(level), np.uint64(0)),
+                                (np.uint64(seed), np.uint64(0))), axis=-1)   # [octs][4]
+    w = words[where.reshape(idx.shape), ((idx >> np.uint64(1)) & np.uint64(3)).astype(np.intp)]
+    odd = (idx & np.uint64(1)) == np.uint64(1)
+    draw = np.where(odd, w >> np.uint64(32), w & np.uint64(0xFFFFFFFF))
     return draw < np.uint64(fire_threshold(fire_rate))
 
 

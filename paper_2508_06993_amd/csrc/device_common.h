@@ -16,9 +16,10 @@ constexpr int kH = 64;   // hidden units of the per-cell MLP
 // Numbers: As Easy as 1, 2, 3", SC 2011).  The paper only asks for a 50%
 // Bernoulli gate per cell and step (Sec. 3.1); a counter-based generator makes
 // the gate a pure function of (seed, level, step, cell), independent of launch
-// shape.  Counter (idx >> 2, step, level, 0), key (seed, 0); the cell uses
-// output word idx & 3, and fires iff the upper 32 bits of that word are below
-// the threshold T = min(2^32, floor(rate * 2^32)).
+// shape.  Counter (idx >> 3, step, level, 0), key (seed, 0): one call covers
+// 8 consecutive cells, cell idx takes the upper (odd idx) or lower (even idx)
+// 32 bits of output word (idx >> 1) & 3 and fires iff that draw is below the
+// threshold T = min(2^32, floor(rate * 2^32)).
 // ---------------------------------------------------------------------------
 struct Philox4x64Out {
     uint64_t w[4];
@@ -54,13 +55,20 @@ __device__ __forceinline__ Philox4x64Out philox4x64_10(uint64_t c0, uint64_t c1,
     return Philox4x64Out{{c0, c1, c2, c3}};
 }
 
-// Fire bit of the cell with canonical index `idx` = (z*h + y)*w + x.
+// Fire bit of the cell with canonical index `idx` = (z*h + y)*w + x: block
+// (idx >> 3), word (idx >> 1) & 3, upper 32 bits for odd idx, lower for even.
+__device__ __forceinline__ uint32_t draw_of(const Philox4x64Out &r, uint32_t cell_in_block) {
+    const uint32_t k = (cell_in_block >> 1) & 3u;
+    const uint64_t lo = (k & 1u) ? r.w[1] : r.w[0];
+    const uint64_t hi = (k & 1u) ? r.w[3] : r.w[2];
+    const uint64_t w = (k & 2u) ? hi : lo;
+    return (cell_in_block & 1u) ? (uint32_t)(w >> 32) : (uint32_t)w;
+}
+
 __device__ __forceinline__ bool cell_fires(uint64_t seed, uint32_t level, uint32_t step,
                                            uint64_t idx, uint64_t threshold) {
-    const Philox4x64Out r = philox4x64_10(idx >> 2, step, level, 0, seed, 0);
-    const int word = (int)(idx & 3);
-    const uint64_t w = word == 0 ? r.w[0] : word == 1 ? r.w[1] : word == 2 ? r.w[2] : r.w[3];
-    return (w >> 32) < threshold;
+    const Philox4x64Out r = philox4x64_10(idx >> 3, step, level, 0, seed, 0);
+    return (uint64_t)draw_of(r, (uint32_t)idx & 7u) < threshold;
 }
 
 // ---------------------------------------------------------------------------

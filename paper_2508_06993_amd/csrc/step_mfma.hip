@@ -24,9 +24,9 @@
 //   * layer 2's accumulator holds channels 4g .. 4g+3 of cell n in lane l:
 //     the channels whose state the lane already holds, so the residual
 //     update and the 16-byte store need no data exchange.
-// Fire bits: each wave evaluates Philox4x64-10 once per lane for up to 64
-// quads of cells (the rows it owns), spreads the bits with four ballots and
-// every lane picks its cell's bit.
+// Fire bits: each lane evaluates Philox4x64-10 for one block of 8 cells of
+// the rows its wave owns (covering several tiles or planes ahead), the bits
+// are spread with eight ballots and every lane picks its cell's bit.
 //
 // 2D: a persistent grid loops over 16 x 32 tiles; the 18 x 34 halo tile is
 // staged in LDS as fp32 in four channel-quad planes (conflict-free 16-byte
@@ -312,39 +312,56 @@ struct MlpF16 {
     }
 };
 
-// Fire bits.  One Philox4x64-10 evaluation gives the bits of a quad of 4
-// consecutive cells, so a wave evaluates one quad per lane and spreads the
-// bits with four ballots (one per output word).  Lanes are assigned to row
-// slots of `qpr` quads each: bit (slot, quad offset o) of ballot k holds the
-// bit of cell 4 (q0(slot) + o) + k, q0(slot) = (canonical index of the slot's
-// first cell) >> 2.  When rows start on a quad boundary (w % 4 == 0) a row of
-// 32 cells is exactly 8 quads and one evaluation covers 8 row slots (2 tiles
-// in 2D, 4 planes in 3D); otherwise rows use 16 quads and 4 slots.
+// Fire bits.  One Philox4x64-10 evaluation gives the draws of a block of 8
+// consecutive cells, so a wave evaluates one block per lane and spreads the
+// bits with eight ballots (ballot b holds the bit of cell b of each lane's
+// block).  Lanes are assigned to row slots of `opr` blocks each: bit
+// (slot * opr + o) of ballot b is the bit of cell 8 * (b0(slot) + o) + b,
+// where b0(slot) = (canonical index of the slot's first cell) >> 3.
+// When rows start on an 8-cell boundary (w % 8 == 0) a 32-cell tile row is
+// exactly 4 blocks (opr = 4) and a lane's cells always take the same ballot
+// (cell n of a 16-cell group has b = n % 8), so each lane selects its ballot
+// once per evaluation; otherwise a row uses opr = 8 and the ballot is
+// selected per cell.
 struct FireBallots {
-    uint64_t w[4];
+    uint64_t w[8];
 };
 
-__device__ __forceinline__ FireBallots fire_ballots(uint64_t quad, uint32_t step, uint32_t level,
+__device__ __forceinline__ FireBallots fire_ballots(uint64_t block, uint32_t step, uint32_t level,
                                                     uint64_t seed, uint64_t threshold) {
-    const Philox4x64Out r = philox4x64_10(quad, step, level, 0, seed, 0);
-    FireBallots b;
-    b.w[0] = __ballot((r.w[0] >> 32) < threshold);
-    b.w[1] = __ballot((r.w[1] >> 32) < threshold);
-    b.w[2] = __ballot((r.w[2] >> 32) < threshold);
-    b.w[3] = __ballot((r.w[3] >> 32) < threshold);
-    return b;
+    const Philox4x64Out r = philox4x64_10(block, step, level, 0, seed, 0);
+    FireBallots f;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) f.w[b] = __ballot((uint64_t)draw_of(r, (uint32_t)b) < threshold);
+    return f;
 }
 
-__device__ __forceinline__ bool fire_bit(const FireBallots &b, int slot, int qpr, uint64_t idx,
-                                         uint64_t row_quad0) {
-    const int o = (int)((idx >> 2) - row_quad0);
-    const uint32_t k = (uint32_t)idx & 3u;
-    // word k of the quad, selected without branches
-    const uint64_t lo = (k & 1u) ? b.w[1] : b.w[0];
-    const uint64_t hi = (k & 1u) ? b.w[3] : b.w[2];
-    const uint64_t w = (k & 2u) ? hi : lo;
-    return (w >> (slot * qpr + o)) & 1;
+// Ballot b of the set, selected without branches.
+__device__ __forceinline__ uint64_t select_ballot(const FireBallots &f, uint32_t b) {
+    const uint64_t w01 = (b & 1u) ? f.w[1] : f.w[0];
+    const uint64_t w23 = (b & 1u) ? f.w[3] : f.w[2];
+    const uint64_t w45 = (b & 1u) ? f.w[5] : f.w[4];
+    const uint64_t w67 = (b & 1u) ? f.w[7] : f.w[6];
+    const uint64_t w03 = (b & 2u) ? w23 : w01;
+    const uint64_t w47 = (b & 2u) ? w67 : w45;
+    return (b & 4u) ? w47 : w03;
 }
+
+// Per-lane view of one evaluation: `mine` is the ballot of the lane's cells
+// when rows are 8-aligned.
+struct FireBits {
+    FireBallots f;
+    uint64_t mine;
+    bool aligned;
+    int opr;
+
+    // Bit of cell idx in row slot `slot` whose first block is row_b0.
+    __device__ __forceinline__ bool bit(int slot, uint64_t idx, uint64_t row_b0) const {
+        const int o = (int)((idx >> 3) - row_b0);
+        const uint64_t w = aligned ? mine : select_ballot(f, (uint32_t)idx & 7u);
+        return (w >> (slot * opr + o)) & 1;
+    }
+};
 
 // ---------------------------------------------------------------------------
 // Halo tiles: HY rows of 34 cells (a 32-cell-wide interior plus one halo cell
@@ -608,9 +625,14 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    // rows start on a quad boundary: one fire evaluation serves two tiles
-    const bool aligned = (dw & 3) == 0;
-    const int qpr = aligned ? 8 : 16;
+    // Fire evaluations: a tile's 4 rows per wave take 4 * opr lanes, so one
+    // evaluation serves 64 / (4 opr) consecutive tiles of this block (4 when
+    // rows are 8-aligned, else 2).
+    FireBits fire;
+    fire.aligned = (dw & 7) == 0;
+    fire.opr = fire.aligned ? 4 : 8;
+    const int lg_opr = fire.aligned ? 2 : 3;
+    const int tiles_per_eval = 64 / (4 * fire.opr);
     const int stride = (int)gridDim.x;
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
@@ -626,27 +648,22 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
         ld.issue(src, 0, 1, dh, dw, ty * k2TY, (tile - ty * tiles_x) * kTileW);
         ld.commit(planes);
     }
-    FireBallots fb;
     for (int iter = 0; tile < tiles; tile += stride, ++iter) {
         const int ty = tile / tiles_x;
         const int y0 = ty * k2TY, x0 = (tile - ty * tiles_x) * kTileW;
-        int slot0 = 0;
-        if (aligned) {
-            // lanes 0-31: this tile, lanes 32-63: this block's next tile
-            if ((iter & 1) == 0) {
-                int t2 = tile + (lane >> 5) * stride;
-                t2 = t2 < tiles ? t2 : tile;
-                const int ty2 = t2 / tiles_x;
-                const uint64_t row = (uint64_t)(ty2 * k2TY + 4 * wave + ((lane >> 3) & 3));
-                const uint64_t q0 = (row * dw + (uint64_t)(t2 - ty2 * tiles_x) * kTileW) >> 2;
-                fb = fire_ballots(q0 + (lane & 7), step, level, seed, threshold);
-            } else {
-                slot0 = 4;
-            }
-        } else {
-            const uint64_t row = (uint64_t)(y0 + 4 * wave + (lane >> 4));
-            fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 15), step, level, seed, threshold);
+        const int phase = iter & (tiles_per_eval - 1);
+        if (phase == 0) {
+            // lane -> (tile offset, row r of the wave's 4, block o of the row)
+            const int tt = lane >> (lg_opr + 2);
+            int t2 = tile + tt * stride;
+            t2 = t2 < tiles ? t2 : tile;
+            const int ty2 = t2 / tiles_x;
+            const uint64_t row = (uint64_t)(ty2 * k2TY + 4 * wave + ((lane >> lg_opr) & 3));
+            const uint64_t b0 = (row * dw + (uint64_t)(t2 - ty2 * tiles_x) * kTileW) >> 3;
+            fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, seed, threshold);
+            fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
         }
+        const int slot0 = phase * 4;
         __syncthreads();
         {
             const int next = tile + stride;
@@ -682,9 +699,9 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
             const int ly = 4 * wave + r;
             const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
             const uint64_t idx = (uint64_t)y * dw + x;
-            const uint64_t row_q0 = ((uint64_t)y * dw + x0) >> 2;
+            const uint64_t row_b0 = ((uint64_t)y * dw + x0) >> 3;
             const uint32_t off = x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-            update_store(dst, wr, off, g, f, u, upd, fire_bit(fb, slot0 + r, qpr, idx, row_q0));
+            update_store(dst, wr, off, g, f, u, upd, fire.bit(slot0 + r, idx, row_b0));
 #pragma unroll
             for (int k = 0; k < 8; ++k) f[k] = fn[k];
             // keep the scheduler from interleaving whole groups (register pressure)
@@ -745,14 +762,18 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    // rows start on a quad boundary: one fire evaluation serves four planes
-    const bool aligned = (dw & 3) == 0;
-    const int qpr = aligned ? 8 : 16;
+    // Fire evaluations: a plane's 2 rows per wave take 2 * opr lanes, so one
+    // evaluation serves 64 / (2 opr) consecutive planes (8 when rows are
+    // 8-aligned, else 4).
+    FireBits fire;
+    fire.aligned = (dw & 7) == 0;
+    fire.opr = fire.aligned ? 4 : 8;
+    const int lg_opr = fire.aligned ? 2 : 3;
+    const int planes_per_eval = 64 / (2 * fire.opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
     Loader ld;
-    FireBallots fb;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         int rest = item;
@@ -776,22 +797,17 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         ld.commit(ring[(z_begin + 1) % 3]);
 
         for (int z = z_begin; z < z_end; ++z) {
-            int slot0 = 0;
-            if (aligned) {
-                // lane group pz = lane / 16 evaluates plane z + pz (pz < 4)
-                if (((z - z_begin) & 3) == 0) {
-                    const int zz = min(z + (lane >> 4), dd - 1);
-                    const uint64_t row =
-                        (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> 3) & 1));
-                    fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 7), step, level, seed,
-                                      threshold);
-                }
-                slot0 = 2 * ((z - z_begin) & 3);
-            } else {
-                const uint64_t row = (uint64_t)z * dh + (uint64_t)(y0 + 2 * wave + ((lane >> 4) & 1));
-                fb = fire_ballots(((row * dw + x0) >> 2) + (lane & 15), step, level, seed,
-                                  threshold);
+            const int phase = (z - z_begin) & (planes_per_eval - 1);
+            if (phase == 0) {
+                // lane -> (plane offset, row r of the wave's 2, block o of the row)
+                const int zz = min(z + (lane >> (lg_opr + 1)), dd - 1);
+                const uint64_t row =
+                    (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
+                fire.f = fire_ballots(((row * dw + x0) >> 3) + (lane & (fire.opr - 1)), step,
+                                      level, seed, threshold);
+                fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
             }
+            const int slot0 = 2 * phase;
             __syncthreads();
             // plane z + 2 (needed by the next plane; after the run's last
             // plane nothing is read)
@@ -820,10 +836,10 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 const int ly = 2 * wave + r;
                 const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
                 const uint64_t idx = ((uint64_t)z * dh + y) * dw + x;
-                const uint64_t row_q0 = (((uint64_t)z * dh + y) * dw + x0) >> 2;
+                const uint64_t row_b0 = (((uint64_t)z * dh + y) * dw + x0) >> 3;
                 const uint32_t off =
                     x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-                update_store(dst, wr, off, g, f, u, upd, fire_bit(fb, slot0 + r, qpr, idx, row_q0));
+                update_store(dst, wr, off, g, f, u, upd, fire.bit(slot0 + r, idx, row_b0));
 #pragma unroll
                 for (int k = 0; k < 8; ++k) f[k] = fn[k];
                 __builtin_amdgcn_sched_barrier(0);

@@ -30,7 +30,7 @@ CASES = [
     ((0, 3, 2, 0), (0, 0)),                 # borrow across words in numpy's form
     ((0, 0, 0, 0), (MASK64, MASK64)),
     ((MASK64, MASK64, MASK64, MASK64), (0xDEADBEEF, 42)),
-    ((46117, 19, 5, 0), (2024, 0)),          # a typical (cell quad, step, level, 0)
+    ((46117, 19, 5, 0), (2024, 0)),          # a typical (cell block, step, level, 0)
 ]
 
 
@@ -77,14 +77,30 @@ def test_fire_extremes():
     assert fire_mask(0, 0, 0, (2, 17, 33), 1.0).all()
 
 
-def test_fire_bits_are_the_upper_halves_of_the_quad_block():
-    """Cell idx uses word idx & 3 of the block at counter (idx >> 2, t, l, 0)."""
+def test_fire_bits_are_the_32_bit_halves_of_the_block():
+    """Cell idx uses block (idx >> 3, t, l, 0), word (idx >> 1) & 3, upper half
+    for odd idx and lower half for even idx: the 8 cells of a block use all
+    256 bits of one Philox call."""
     seed, lvl, t = 11, 2, 5
-    m = fire_mask(seed, lvl, t, (1, 4, 8), 0.5).reshape(-1)
-    for idx in range(32):
-        block = numpy_block((idx >> 2, t, lvl, 0), (seed, 0))
-        draw = block[idx & 3] >> 32
+    m = fire_mask(seed, lvl, t, (1, 4, 16), 0.5).reshape(-1)
+    for idx in range(64):
+        block = numpy_block((idx >> 3, t, lvl, 0), (seed, 0))
+        word = block[(idx >> 1) & 3]
+        draw = (word >> 32) if idx & 1 else (word & 0xFFFFFFFF)
         assert m[idx] == (draw < (1 << 31))
+
+
+def test_fire_bits_of_one_block_use_distinct_bits():
+    """The 8 draws of one block are the 8 distinct 32-bit halves (no draw is
+    reused for two cells)."""
+    seed, lvl, t = 3, 0, 1
+    block = numpy_block((5, t, lvl, 0), (seed, 0))
+    halves = sorted([w & 0xFFFFFFFF for w in block] + [w >> 32 for w in block])
+    for p in (0.2, 0.5, 0.8):
+        thr = fire_threshold(p)
+        idx = np.arange(40, 48, dtype=np.uint64)
+        got = fire_bits(seed, lvl, t, idx, p)
+        assert int(got.sum()) == sum(h < thr for h in halves)
 
 
 def test_fire_rate_is_binomial():
