@@ -361,6 +361,7 @@ struct FireBits {
         const uint64_t w = aligned ? mine : select_ballot(f, (uint32_t)idx & 7u);
         return (w >> (slot * opr + o)) & 1;
     }
+
 };
 
 // ---------------------------------------------------------------------------
@@ -713,13 +714,18 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
 }
 
 // ---------------------------------------------------------------------------
-// 3D: a work item is an 8 x 32 (y, x) column and a run of z planes; planes
-// stream through a ring of three halo planes in LDS, the plane after next
-// being loaded while the current one is computed.  Wave w computes rows
-// 2w, 2w+1 of each plane (4 groups of 16 cells).
+// 3D: a work item is an 8 x 32 (y, x) column and a run of k3ZRun output
+// planes.  Input planes stream through a ring of three LDS plane slots
+// (planes p - 1 and p are in use while p + 1 is written).  Each input plane p
+// is read once: its 9 in-plane taps feed three rolling perception sums, for
+// outputs p + 1 (the dz = -1 weights), p (dz = 0) and p - 1 (dz = +1).  After
+// plane p the sum of output p - 1 is complete and that plane's MLP, fire gate
+// and store run, with the cell's own state re-read from the ring.  Wave w
+// owns rows 2w, 2w+1 (4 groups of 16 cells); the conv weights of a tap are
+// read once per wave and applied to all 4 groups.
 // ---------------------------------------------------------------------------
 constexpr int k3TY = 8;
-constexpr int k3ZRun = 16;    // z planes per work item
+constexpr int k3ZRun = 32;    // output planes per work item
 
 template <typename T, int NIN, class Mlp>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
@@ -730,6 +736,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     using Loader = RowLoader<T, k3TY + 2>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
+    __shared__ uint64_t fire_words[4][8];   // [wave][b]: ballot b of the last evaluation
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -763,17 +770,24 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
     // Fire evaluations: a plane's 2 rows per wave take 2 * opr lanes, so one
-    // evaluation serves 64 / (2 opr) consecutive planes (8 when rows are
-    // 8-aligned, else 4).
-    FireBits fire;
-    fire.aligned = (dw & 7) == 0;
-    fire.opr = fire.aligned ? 4 : 8;
-    const int lg_opr = fire.aligned ? 2 : 3;
-    const int planes_per_eval = 64 / (2 * fire.opr);
+    // evaluation serves 64 / (2 opr) consecutive output planes (8 when rows
+    // are 8-aligned, else 4).  The 8 ballots go to a per-wave LDS array and a
+    // cell reads the one it needs by address: selecting among them by a
+    // per-lane value in registers makes the compiler build a private
+    // (scratch) array, whose loads would be waited for with the stores.
+    const int opr = (dw & 7) == 0 ? 4 : 8;
+    const int lg_opr = opr == 4 ? 2 : 3;
+    const int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
     Loader ld;
+    // LDS word of group grp's cell (row 2 wave + grp / 2, column 16 (grp % 2) + n)
+    // in the quad plane of this lane, relative to a plane slot.
+    int centre[4];
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp)
+        centre[grp] = g * Loader::PS + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         int rest = item;
@@ -785,67 +799,129 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         const int z_begin = zr * k3ZRun;
         const int z_end = min(dd, z_begin + k3ZRun);
 
-        // planes z_begin - 1 .. z_begin + 1 are staged here; each later plane
-        // is loaded while the plane two before it is computed and written to
-        // the ring at the end of that iteration
+        // rolling perception sums (bias included) of outputs p - 1, p, p + 1
+        float acc_p[4][4], acc_c[4][4], acc_n[4][4];
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                acc_p[grp][k] = cb[k];
+                acc_c[grp][k] = cb[k];
+                acc_n[grp][k] = cb[k];
+            }
+
         __syncthreads();   // the previous item's readers are done with the ring
         ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
-        ld.commit(ring[(z_begin + 2) % 3]);
+        ld.commit(ring[0]);
         ld.issue(src, z_begin, dd, dh, dw, y0, x0);
-        ld.commit(ring[z_begin % 3]);
-        ld.issue(src, z_begin + 1, dd, dh, dw, y0, x0);
-        ld.commit(ring[(z_begin + 1) % 3]);
+        __syncthreads();
 
-        for (int z = z_begin; z < z_end; ++z) {
-            const int phase = (z - z_begin) & (planes_per_eval - 1);
-            if (phase == 0) {
-                // lane -> (plane offset, row r of the wave's 2, block o of the row)
-                const int zz = min(z + (lane >> (lg_opr + 1)), dd - 1);
+        int slot = 0;        // ring slot of plane p
+        int slot_prev = 2;   // ring slot of plane p - 1
+        for (int p = z_begin - 1; p <= z_end; ++p) {
+            const float4 *pl = ring[slot];
+            // Taps are software-pipelined: the LDS reads of tap t + 1 are issued
+            // before the FMAs of tap t, and pinning the sums after each tap keeps
+            // the compiler from hoisting every read of the plane at once.
+            int gq = g;
+            pin(gq);   // re-read the tap weights every plane rather than keep 27 in registers
+            float4 sv[2][4], wv[2][3];
+            auto read_tap = [&](int t, float4 (&s4)[4], float4 (&w3)[3]) {
+                const int off = (t / 3 - 1) * kHaloW + (t % 3 - 1);
+                w3[0] = tapw[t][gq];        // dz = -1: output p + 1
+                w3[1] = tapw[9 + t][gq];    // dz =  0: output p
+                w3[2] = tapw[18 + t][gq];   // dz = +1: output p - 1
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) s4[grp] = pl[centre[grp] + off];
+            };
+            read_tap(0, sv[0], wv[0]);
+#pragma unroll
+            for (int t = 0; t < 9; ++t) {
+                if (t + 1 < 9) read_tap(t + 1, sv[(t + 1) & 1], wv[(t + 1) & 1]);
+                const float4 *w3 = wv[t & 1];
+                const float a_m[4] = {w3[0].x, w3[0].y, w3[0].z, w3[0].w};
+                const float a_0[4] = {w3[1].x, w3[1].y, w3[1].z, w3[1].w};
+                const float a_p[4] = {w3[2].x, w3[2].y, w3[2].z, w3[2].w};
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) {
+                    const float4 v = sv[t & 1][grp];
+                    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        acc_n[grp][k] = fmaf(a_m[k], vv[k], acc_n[grp][k]);
+                        acc_c[grp][k] = fmaf(a_0[k], vv[k], acc_c[grp][k]);
+                        acc_p[grp][k] = fmaf(a_p[k], vv[k], acc_p[grp][k]);
+                    }
+                }
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        pin(acc_n[grp][k]);
+                        pin(acc_c[grp][k]);
+                        pin(acc_p[grp][k]);
+                    }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+
+            // output plane zo = p - 1: MLP, fire gate, store (stores of planes
+            // outside [z_begin, z_end) are dropped by an empty descriptor)
+            const int zo = p - 1;
+            const bool out_ok = zo >= z_begin && zo < z_end;
+            const int phase = (zo - z_begin) & (planes_per_eval - 1);
+            if (out_ok && phase == 0) {
+                const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
                 const uint64_t row =
                     (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
-                fire.f = fire_ballots(((row * dw + x0) >> 3) + (lane & (fire.opr - 1)), step,
-                                      level, seed, threshold);
-                fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
+                const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
+                                                    step, level, seed, threshold);
+                uint64_t word = fb.w[0];
+#pragma unroll
+                for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
+                fire_words[wave][lane & 7] = word;   // 8 lanes per address, same value
             }
             const int slot0 = 2 * phase;
-            __syncthreads();
-            // plane z + 2 (needed by the next plane; after the run's last
-            // plane nothing is read)
-            ld.issue(src, z + 2, dd, dh, dw, y0, x0, z + 1 < z_end);
-
-            // stores of this plane: rows y0 .. y0 + k3TY - 1 (clipped to the grid)
-            const Rsrc wr = make_rsrc(dst + ((int64_t)z * dh + y0) * dw * kC,
-                                      (uint32_t)min(k3TY, dh - y0) * row_bytes);
-            const float4 *pm = ring[(z + 2) % 3] + g * Loader::PS;   // plane z - 1
-            const float4 *pc = ring[z % 3] + g * Loader::PS;         // plane z
-            const float4 *pp = ring[(z + 1) % 3] + g * Loader::PS;   // plane z + 1
-            auto centre_of = [&](int grp) {
-                return (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
-            };
-            float f[8];
-            perceive_3d(pm, pc, pp, tapw, g, centre_of(0), cb, f);
+            const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
+                                      out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
+            const float4 *own = ring[slot_prev];
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
+                const float4 sp = own[centre[grp]];
+                float f[8] = {sp.x, sp.y, sp.z, sp.w};
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[4 + k] = acc_p[grp][k];
                 v4f acc[4];
                 mlp.layer1(f, acc);
-                float fn[8];
-                if (grp < 3) perceive_3d(pm, pc, pp, tapw, g, centre_of(grp + 1), cb, fn);
                 const v4f u = mlp.layer2(acc);
-
                 const int r = grp >> 1;
                 const int ly = 2 * wave + r;
                 const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
-                const uint64_t idx = ((uint64_t)z * dh + y) * dw + x;
-                const uint64_t row_b0 = (((uint64_t)z * dh + y) * dw + x0) >> 3;
+                const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
+                const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
                 const uint32_t off =
                     x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-                update_store(dst, wr, off, g, f, u, upd, fire.bit(slot0 + r, idx, row_b0));
-#pragma unroll
-                for (int k = 0; k < 8; ++k) f[k] = fn[k];
+                const uint64_t fw = fire_words[wave][idx & 7];
+                const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
+                update_store(dst, wr, off, g, f, u, upd, fires);
                 __builtin_amdgcn_sched_barrier(0);
             }
-            __syncthreads();                    // plane z - 1's slot is free
-            ld.commit(ring[(z + 2) % 3]);       // plane z + 2 into it
+
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    acc_p[grp][k] = acc_c[grp][k];
+                    acc_c[grp][k] = acc_n[grp][k];
+                    acc_n[grp][k] = cb[k];
+                }
+
+            // plane p + 1 into the free slot, then start loading p + 2
+            const int slot_next = 3 - slot - slot_prev;
+            ld.commit(ring[slot_next]);
+            ld.issue(src, p + 2, dd, dh, dw, y0, x0, p + 2 <= z_end);
+            __syncthreads();
+            slot_prev = slot;
+            slot = slot_next;
         }
     }
 }
