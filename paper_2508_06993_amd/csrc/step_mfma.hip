@@ -34,6 +34,7 @@
 // of z planes, keeping three halo planes in an LDS ring (each plane is read
 // from HBM once per run).
 #include <algorithm>
+#include <type_traits>
 
 #include "launch.h"
 
@@ -292,7 +293,11 @@ struct MlpF16 {
         v8f fx;
 #pragma unroll
         for (int s = 0; s < 8; ++s) fx[s] = f[s];
-        const v8h fh = __builtin_convertvector(fx, v8h);
+        layer1_h(__builtin_convertvector(fx, v8h), acc);
+    }
+
+    // features already in fp16 (slot s = feature_of(s, g))
+    __device__ __forceinline__ void layer1_h(const v8h &fh, v4f acc[4]) const {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1[jt], fh, b1[jt], 0, 0, 0);
@@ -322,7 +327,10 @@ struct MlpF16 {
 // exactly 4 blocks (opr = 4) and a lane's cells always take the same ballot
 // (cell n of a 16-cell group has b = n % 8), so each lane selects its ballot
 // once per evaluation; otherwise a row uses opr = 8 and the ballot is
-// selected per cell.
+// selected per cell.  The 2D step selects in registers (FireBits below); the
+// 3D steps keep the 8 ballots in a small per-wave LDS array and read ballot
+// (idx & 7) by address, because there the register select was lowered to a
+// private array whose loads the stores then had to wait for.
 struct FireBallots {
     uint64_t w[8];
 };
@@ -502,6 +510,32 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
         const int row = s * kRowsPerSide + lane / (2 * NQ);
         const int slot = row * kHaloW + (((lane / NQ) & 1) ? kHaloW - 1 : 0);
         put(planes, lane % NQ, (s < kSide && row < HY) ? slot : kDummyCell, v[kBodySlots]);
+    }
+
+    // fp16 rows kept as fp16 in LDS: four channel-quad planes of 8-byte words
+    // (channels 4q..4q+3 of a cell); a 16-byte chunk c (channels 8c..8c+7)
+    // is split between quad planes 2c and 2c+1.  Same slots as commit().
+    __device__ static __forceinline__ void put_raw(uint2 *planes, int c, int cell, const uint4 &x) {
+        planes[(2 * c) * PS + cell] = make_uint2(x.x, x.y);
+        planes[(2 * c + 1) * PS + cell] = make_uint2(x.z, x.w);
+    }
+
+    __device__ __forceinline__ void commit_raw(uint2 *planes) const {
+        static_assert(NQ == 2, "raw fp16 planes");
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int cell = body_cell(lane), chunk = body_chunk(lane);
+#pragma unroll
+        for (int k = 0; k < kBodySlots; ++k) {
+            const int J = wave + 4 * k;
+            const int slot =
+                (J / kBodyPerRow) * kHaloW + 1 + (J % kBodyPerRow) * kCellsPerBody + cell;
+            put_raw(planes, chunk, J < kBody ? slot : kDummyCell, v[k]);
+        }
+        const int s = 3 - wave;
+        const int row = s * kRowsPerSide + lane / (2 * NQ);
+        const int slot = row * kHaloW + (((lane / NQ) & 1) ? kHaloW - 1 : 0);
+        put_raw(planes, lane % NQ, (s < kSide && row < HY) ? slot : kDummyCell, v[kBodySlots]);
     }
 };
 
@@ -926,6 +960,208 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     }
 }
 
+// ---------------------------------------------------------------------------
+// 3D step for fp16 states with the fp16 MLP: the same z streaming as
+// nca_step_mfma_3d, but the ring holds the planes as fp16 (8-byte channel
+// quads, half the LDS) and the perception sums are packed fp16 FMAs
+// (v_pk_fma_f16: two channels per instruction, half the VALU work of fp32
+// sums).  The features go to the fp16 MFMAs without conversion.  The sums
+// are rounded to fp16 after every tap; with fp16 storage this changes the
+// result by far less than the fp16 rounding of the stored state itself.
+// ---------------------------------------------------------------------------
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+__device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
+
+constexpr int k3hBlocksPerCu = 3;
+
+template <int NIN>
+__global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16(
+    const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
+    int tiles_x, int tiles_y, int items, const float *__restrict__ conv_w,
+    const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
+    const float *__restrict__ w2, uint32_t level, uint32_t step, uint64_t seed,
+    uint64_t threshold) {
+    using Loader = RowLoader<__half, k3TY + 2>;
+    __shared__ uint2 ring[3][4 * Loader::PS];
+    __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
+    __shared__ uint64_t fire_words[4][8];   // [wave][b]: ballot b of the last evaluation
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n = lane & 15;
+    const int g = lane >> 4;
+
+    {
+        const int i = min((int)threadIdx.x, 27 * 4 - 1);
+        const int t = i / 4, q = i % 4;
+        const h2 lo = {(_Float16)conv_w[(4 * q + 0) * 27 + t], (_Float16)conv_w[(4 * q + 1) * 27 + t]};
+        const h2 hi = {(_Float16)conv_w[(4 * q + 2) * 27 + t], (_Float16)conv_w[(4 * q + 3) * 27 + t]};
+        if (threadIdx.x < 27 * 4) tapw[t][q] = make_uint2(as_u32(lo), as_u32(hi));
+    }
+    MlpF16 mlp;
+    mlp.load(w1, b1, w2, n, g);
+    h2 cb[2];
+    float upd[4];
+    cb[0] = h2{(_Float16)conv_b[4 * g + 0], (_Float16)conv_b[4 * g + 1]};
+    cb[1] = h2{(_Float16)conv_b[4 * g + 2], (_Float16)conv_b[4 * g + 3]};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
+    mlp.pin_all();
+    pin(cb[0]);
+    pin(cb[1]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pin(upd[k]);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // fire evaluations as in nca_step_mfma_3d
+    const int opr = (dw & 7) == 0 ? 4 : 8;
+    const int lg_opr = opr == 4 ? 2 : 3;
+    const int planes_per_eval = 64 / (2 * opr);
+    constexpr int kCellBytes = Loader::kCellBytes;
+    const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
+    const int zruns = (dd + k3ZRun - 1) / k3ZRun;
+    Loader ld;
+    int centre[4];
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp)
+        centre[grp] = g * Loader::PS + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
+
+    for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        int rest = item;
+        const int zr = rest % zruns;
+        rest /= zruns;
+        const int tx = rest % tiles_x;
+        const int ty = rest / tiles_x;
+        const int y0 = ty * k3TY, x0 = tx * kTileW;
+        const int z_begin = zr * k3ZRun;
+        const int z_end = min(dd, z_begin + k3ZRun);
+
+        // rolling perception sums (bias included) of outputs p - 1, p, p + 1,
+        // channels (4g, 4g+1) in [.][0] and (4g+2, 4g+3) in [.][1]
+        h2 acc_p[4][2], acc_c[4][2], acc_n[4][2];
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                acc_p[grp][k] = cb[k];
+                acc_c[grp][k] = cb[k];
+                acc_n[grp][k] = cb[k];
+            }
+
+        __syncthreads();
+        ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
+        ld.commit_raw(ring[0]);
+        ld.issue(src, z_begin, dd, dh, dw, y0, x0);
+        __syncthreads();
+
+        int slot = 0, slot_prev = 2;
+        for (int p = z_begin - 1; p <= z_end; ++p) {
+            const uint2 *pl = ring[slot];
+            int gq = g;
+            pin(gq);
+            uint2 sv[2][4], wv[2][3];
+            auto read_tap = [&](int t, uint2 (&s4)[4], uint2 (&w3)[3]) {
+                const int off = (t / 3 - 1) * kHaloW + (t % 3 - 1);
+                w3[0] = tapw[t][gq];
+                w3[1] = tapw[9 + t][gq];
+                w3[2] = tapw[18 + t][gq];
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) s4[grp] = pl[centre[grp] + off];
+            };
+            read_tap(0, sv[0], wv[0]);
+#pragma unroll
+            for (int t = 0; t < 9; ++t) {
+                if (t + 1 < 9) read_tap(t + 1, sv[(t + 1) & 1], wv[(t + 1) & 1]);
+                const uint2 *w3 = wv[t & 1];
+                const h2 a_m[2] = {as_h2(w3[0].x), as_h2(w3[0].y)};
+                const h2 a_0[2] = {as_h2(w3[1].x), as_h2(w3[1].y)};
+                const h2 a_p[2] = {as_h2(w3[2].x), as_h2(w3[2].y)};
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp) {
+                    const h2 v[2] = {as_h2(sv[t & 1][grp].x), as_h2(sv[t & 1][grp].y)};
+#pragma unroll
+                    for (int k = 0; k < 2; ++k) {
+                        acc_n[grp][k] = __builtin_elementwise_fma(a_m[k], v[k], acc_n[grp][k]);
+                        acc_c[grp][k] = __builtin_elementwise_fma(a_0[k], v[k], acc_c[grp][k]);
+                        acc_p[grp][k] = __builtin_elementwise_fma(a_p[k], v[k], acc_p[grp][k]);
+                    }
+                }
+#pragma unroll
+                for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                    for (int k = 0; k < 2; ++k) {
+                        pin(acc_n[grp][k]);
+                        pin(acc_c[grp][k]);
+                        pin(acc_p[grp][k]);
+                    }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+
+            const int zo = p - 1;
+            const bool out_ok = zo >= z_begin && zo < z_end;
+            const int phase = (zo - z_begin) & (planes_per_eval - 1);
+            if (out_ok && phase == 0) {
+                const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
+                const uint64_t row =
+                    (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
+                const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
+                                                    step, level, seed, threshold);
+                uint64_t word = fb.w[0];
+#pragma unroll
+                for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
+                fire_words[wave][lane & 7] = word;
+            }
+            const int slot0 = 2 * phase;
+            const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
+                                      out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
+            const uint2 *own = ring[slot_prev];
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp) {
+                const uint2 sp = own[centre[grp]];
+                const h2 s01 = as_h2(sp.x), s23 = as_h2(sp.y);
+                const v8h fh = {s01[0], s01[1], s23[0], s23[1], acc_p[grp][0][0], acc_p[grp][0][1],
+                                acc_p[grp][1][0], acc_p[grp][1][1]};
+                v4f acc[4];
+                mlp.layer1_h(fh, acc);
+                const v4f u = mlp.layer2(acc);
+                const float f[8] = {(float)s01[0], (float)s01[1], (float)s23[0], (float)s23[1],
+                                    0.f, 0.f, 0.f, 0.f};
+                const int r = grp >> 1;
+                const int ly = 2 * wave + r;
+                const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
+                const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
+                const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
+                const uint32_t off =
+                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
+                const uint64_t fw = fire_words[wave][idx & 7];
+                const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
+                update_store(dst, wr, off, g, f, u, upd, fires);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+
+#pragma unroll
+            for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    acc_p[grp][k] = acc_c[grp][k];
+                    acc_c[grp][k] = acc_n[grp][k];
+                    acc_n[grp][k] = cb[k];
+                }
+
+            const int slot_next = 3 - slot - slot_prev;
+            ld.commit_raw(ring[slot_next]);
+            ld.issue(src, p + 2, dd, dh, dw, y0, x0, p + 2 <= z_end);
+            __syncthreads();
+            slot_prev = slot;
+            slot = slot_next;
+        }
+    }
+}
+
 int device_cus() {
     static int cached[64] = {0};
     int dev = 0;
@@ -964,11 +1200,19 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
     if (items > INT32_MAX) return hipErrorInvalidValue;
-    const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * kBlocksPerCu);
-    nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
-        (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
-        (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
-        a.threshold);
+    if constexpr (std::is_same_v<T, __half> && std::is_same_v<Mlp, MlpF16>) {
+        const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * k3hBlocksPerCu);
+        nca_step_mfma_3d_f16<NIN><<<grid, kThreads, 0, stream>>>(
+            (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
+            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
+            a.seed, a.threshold);
+    } else {
+        const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * kBlocksPerCu);
+        nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
+            (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
+            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            a.threshold);
+    }
     return hipGetLastError();
 }
 
