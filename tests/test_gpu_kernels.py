@@ -165,6 +165,9 @@ STEP_CASES = [
     ("f32", 2, 3, (1, 1, 70)), ("f32", 3, 1, (7, 19, 13)), ("f32", 3, 3, (5, 9, 17)),
     ("f32", 3, 1, (1, 1, 1)), ("f16", 2, 3, (1, 21, 45)), ("f16", 3, 3, (6, 11, 10)),
     ("f16", 3, 1, (3, 8, 8)),
+    # several 32-plane z runs with a ragged last run, ragged y tiles, 8-aligned
+    # and unaligned rows
+    ("f32", 3, 1, (70, 12, 40)), ("f16", 3, 3, (70, 10, 36)), ("f16", 3, 3, (33, 16, 64)),
 ]
 
 
@@ -172,7 +175,8 @@ STEP_CASES = [
 # nine steps of one level, per storage type and step kernel.  fp32 operands
 # (vector FMAs or fp32 MFMA) differ from the fp64 oracle by fp32 rounding only;
 # split-bf16 operands keep products to about 2^-16 relative; with fp16 states
-# the storage rounding (2^-11) dominates, plus fp16 MLP operands on "mfma".
+# the storage rounding (2^-11) dominates, plus fp16 MLP operands and (3D)
+# fp16 perception sums on "mfma".
 STEP_TOL = {
     ("f32", "valu"): (2e-6, 1e-4), ("f32", "mfma_f32"): (2e-6, 1e-4),
     ("f32", "mfma"): (5e-5, 5e-4),
@@ -209,7 +213,9 @@ def test_one_step_matches_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
 
 @pytest.mark.parametrize("dt,ndim,n_in,shape", [("f32", 2, 3, (1, 40, 70)),
                                                 ("f32", 3, 1, (6, 20, 18)),
-                                                ("f16", 3, 3, (8, 12, 20))])
+                                                ("f16", 3, 3, (8, 12, 20)),
+                                                ("f32", 3, 1, (40, 12, 40)),
+                                                ("f16", 3, 3, (40, 10, 36))])
 def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     rng = np.random.default_rng(12)
     w = rand_weights(rng, ndim)
