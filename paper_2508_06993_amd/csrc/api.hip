@@ -341,16 +341,25 @@ namespace octnca {
 //   "mfma_f32"      matrix-core kernel with fp32 MLP operands;
 //   "mfma_bf16x3"   matrix-core kernel with split bf16 operands (any storage);
 //   "mfma_f16"      matrix-core kernel with fp16 operands (fp16 states only);
+//   "mfma_rows", "mfma_tiles"  the default kernel with the 2D work layout
+//                   forced to row streaming or to 16 x 32 tiles;
 //   "valu"          one thread per cell, fp32 FMAs on the vector ALUs.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
     const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
+    const Layout2d automatic = Layout2d::Auto;
     if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0)
-        return launch_step_mfma(a, MfmaMlp::Default, src, dst, stream);
+        return launch_step_mfma(a, MfmaMlp::Default, automatic, src, dst, stream);
     if (strcmp(sel, "valu") == 0) return launch_step_valu(a, src, dst, stream);
-    if (strcmp(sel, "mfma_f32") == 0) return launch_step_mfma(a, MfmaMlp::F32, src, dst, stream);
+    if (strcmp(sel, "mfma_f32") == 0)
+        return launch_step_mfma(a, MfmaMlp::F32, automatic, src, dst, stream);
     if (strcmp(sel, "mfma_bf16x3") == 0)
-        return launch_step_mfma(a, MfmaMlp::Bf16x3, src, dst, stream);
-    if (strcmp(sel, "mfma_f16") == 0) return launch_step_mfma(a, MfmaMlp::F16, src, dst, stream);
+        return launch_step_mfma(a, MfmaMlp::Bf16x3, automatic, src, dst, stream);
+    if (strcmp(sel, "mfma_f16") == 0)
+        return launch_step_mfma(a, MfmaMlp::F16, automatic, src, dst, stream);
+    if (strcmp(sel, "mfma_rows") == 0)
+        return launch_step_mfma(a, MfmaMlp::Default, Layout2d::Rows, src, dst, stream);
+    if (strcmp(sel, "mfma_tiles") == 0)
+        return launch_step_mfma(a, MfmaMlp::Default, Layout2d::Tiles, src, dst, stream);
     return hipErrorInvalidValue;
 }
 }  // namespace octnca

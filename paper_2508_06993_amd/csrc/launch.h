@@ -48,7 +48,10 @@ hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipSt
 // MLP operand precision of the MFMA step kernel.  Default: split bf16 (x3)
 // for fp32 states, fp16 for fp16 states.
 enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3 };
-hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, const void *src, void *dst,
-                            hipStream_t stream);
+// Work layout of the 2D MFMA step.  Auto: row streaming on large levels,
+// 16 x 32 tiles on small ones; Rows / Tiles force one (3D steps ignore it).
+enum class Layout2d : int { Auto = 0, Rows = 1, Tiles = 2 };
+hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
+                            void *dst, hipStream_t stream);
 
 }  // namespace octnca

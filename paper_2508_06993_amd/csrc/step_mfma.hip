@@ -748,6 +748,246 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
 }
 
 // ---------------------------------------------------------------------------
+// 2D, row streaming: a block is one wave, and a work item is a 32-cell-wide
+// strip of a run of rows.  The wave streams the strip's halo rows (34 cells)
+// through a private ring of four LDS row slots, so no block barrier is
+// needed (LDS accesses of one wave complete in order).  Each input row q is
+// read once: its 3 taps along x feed three rolling perception sums per
+// 16-cell group, for outputs q + 1 (the dy = -1 weights), q (dy = 0) and
+// q - 1 (dy = +1).  After row q the sum of output q - 1 is complete and that
+// row's MLP, fire gate and store run, with the cell's own state re-read from
+// the ring.  An iteration takes two input rows; the loads of the next two are
+// issued at its start and written to LDS at its end.
+// ---------------------------------------------------------------------------
+constexpr int k2RunRows = 64;       // output rows per work item (largest)
+constexpr int k2WavesPerSimd = 2;   // 255 VGPRs with the split-bf16 MLP
+
+// One halo row of a strip: kBody body loads (16 cells x 4 chunks in fp32,
+// 32 cells x 2 chunks in fp16, lane i -> cell i % cells-per-load, chunk
+// i / cells-per-load) and one side load whose first 2 NQ lanes take the left
+// and right halo cells.  Cells outside the grid and rows outside [0, h) read
+// as zero through an out-of-range offset or an empty descriptor.
+template <typename T>
+struct RowStream {
+    static constexpr int NQ = CellChunks<T>::N;
+    static constexpr int kCellBytes = kC * (int)sizeof(T);
+    static constexpr int kCellsPerBody = 64 / NQ;
+    static constexpr int kBody = kTileW / kCellsPerBody;
+    static constexpr int kDummy = kHaloW;                 // never-read slot
+    static constexpr int PS = plane_stride(kHaloW + 1);   // quad plane stride (16-byte words)
+    static constexpr int kSlotWords = 4 * PS;             // one ring slot
+    uint4 v[kBody + 1];
+
+    __device__ __forceinline__ void issue(const T *__restrict__ src, int y, int dh, int dw, int x0) {
+        const int lane = threadIdx.x & 63;
+        const bool row_ok = y >= 0 && y < dh;
+        const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? y : 0) * dw * kC,
+                                 row_ok ? (uint32_t)dw * kCellBytes : 0u);
+        const int cell = lane % kCellsPerBody, chunk = lane / kCellsPerBody;
+#pragma unroll
+        for (int k = 0; k < kBody; ++k) {
+            const int cx = x0 + k * kCellsPerBody + cell;
+            const uint32_t off = cx < dw ? (uint32_t)cx * kCellBytes + (uint32_t)chunk * 16 : kOut;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const int cx = lane < NQ ? x0 - 1 : x0 + kTileW;
+        const bool ok = lane < 2 * NQ && cx >= 0 && cx < dw;
+        const uint32_t off = ok ? (uint32_t)cx * kCellBytes + (uint32_t)(lane % NQ) * 16 : kOut;
+        const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+        v[kBody] = make_uint4(x[0], x[1], x[2], x[3]);
+    }
+
+    // LDS: four channel-quad planes of PS 16-byte words, fp32; slot 0 is the
+    // left halo cell, 1..32 the strip, 33 the right halo cell.
+    __device__ static __forceinline__ void put(float4 *planes, int q, int slot, const uint4 &c) {
+        if constexpr (NQ == 4) {
+            planes[q * PS + slot] = make_float4(__uint_as_float(c.x), __uint_as_float(c.y),
+                                                __uint_as_float(c.z), __uint_as_float(c.w));
+        } else {
+            float f[8];
+            Storage<__half>::unpack(c, f);
+            planes[(2 * q) * PS + slot] = make_float4(f[0], f[1], f[2], f[3]);
+            planes[(2 * q + 1) * PS + slot] = make_float4(f[4], f[5], f[6], f[7]);
+        }
+    }
+
+    __device__ __forceinline__ void commit(float4 *planes) const {
+        const int lane = threadIdx.x & 63;
+        const int cell = lane % kCellsPerBody, chunk = lane / kCellsPerBody;
+#pragma unroll
+        for (int k = 0; k < kBody; ++k) put(planes, chunk, 1 + k * kCellsPerBody + cell, v[k]);
+        const int slot = lane < NQ ? 0 : (lane < 2 * NQ ? kHaloW - 1 : kDummy);
+        put(planes, lane % NQ, slot, v[kBody]);
+    }
+};
+
+template <typename T, int NIN, class Mlp>
+__global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
+    const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int runs,
+    int run_rows, int items, const float *__restrict__ conv_w,
+    const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
+    const float *__restrict__ w2, uint32_t level, uint32_t step, uint64_t seed,
+    uint64_t threshold) {
+    using RS = RowStream<T>;
+    __shared__ float4 ring[4][RS::kSlotWords];   // row y in slot y & 3
+    __shared__ float4 tapw[9][4];                // [tap][quad] conv weights of channels 4q..4q+3
+
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 15;
+    const int g = lane >> 4;
+
+    {
+        const int i = min(lane, 9 * 4 - 1);
+        const int t = i / 4, q = i % 4;
+        const float4 tw = make_float4(conv_w[(4 * q + 0) * 9 + t], conv_w[(4 * q + 1) * 9 + t],
+                                      conv_w[(4 * q + 2) * 9 + t], conv_w[(4 * q + 3) * 9 + t]);
+        if (lane < 9 * 4) tapw[t][q] = tw;
+    }
+    Mlp mlp;
+    mlp.load(w1, b1, w2, n, g);
+    float cb[4];
+    float upd[4];   // channels < NIN are copied, never updated
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        cb[k] = conv_b[4 * g + k];
+        upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
+    }
+    mlp.pin_all();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        pin(cb[k]);
+        pin(upd[k]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // Fire evaluations: a row takes opr lanes, so one evaluation serves
+    // 64 / opr consecutive output rows (16 when rows are 8-aligned, else 8).
+    FireBits fire;
+    fire.aligned = (dw & 7) == 0;
+    fire.opr = fire.aligned ? 4 : 8;
+    const int lg_opr = fire.aligned ? 2 : 3;
+    const int rows_per_eval = 64 / fire.opr;
+    constexpr int kCellBytes = RS::kCellBytes;
+    const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
+    int gq = g;
+    RS ra, rb;
+
+    for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        const int sx = item % strips;
+        const int ry = item / strips;
+        const int x0 = sx * kTileW;
+        const int y_begin = ry * run_rows;
+        const int y_end = min(dh, y_begin + run_rows);
+
+        // rolling perception sums (bias included) of outputs q - 1, q, q + 1
+        float acc_p[2][4], acc_c[2][4], acc_n[2][4];
+#pragma unroll
+        for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                acc_p[grp][k] = cb[k];
+                acc_c[grp][k] = cb[k];
+                acc_n[grp][k] = cb[k];
+            }
+
+        // rows y_begin - 1 and y_begin into the ring
+        ra.issue(src, y_begin - 1, dh, dw, x0);
+        rb.issue(src, y_begin, dh, dw, x0);
+        ra.commit(ring[(y_begin - 1) & 3]);
+        rb.commit(ring[y_begin & 3]);
+
+        // Input row q with its x taps: output q + 1 takes the dy = -1 weights,
+        // q the dy = 0 ones and q - 1 the dy = +1 ones.
+        auto fold_row = [&](int q) {
+            const float4 *pl = ring[q & 3] + g * RS::PS;
+            pin(gq);   // re-read the tap weights every row instead of keeping 36 registers
+#pragma unroll
+            for (int dx = 0; dx < 3; ++dx) {
+                const float4 wm = tapw[dx][gq];
+                const float4 w0 = tapw[3 + dx][gq];
+                const float4 wp = tapw[6 + dx][gq];
+                const float a_m[4] = {wm.x, wm.y, wm.z, wm.w};
+                const float a_0[4] = {w0.x, w0.y, w0.z, w0.w};
+                const float a_p[4] = {wp.x, wp.y, wp.z, wp.w};
+#pragma unroll
+                for (int grp = 0; grp < 2; ++grp) {
+                    const float4 v = pl[grp * 16 + n + dx];
+                    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        acc_n[grp][k] = fmaf(a_m[k], vv[k], acc_n[grp][k]);
+                        acc_c[grp][k] = fmaf(a_0[k], vv[k], acc_c[grp][k]);
+                        acc_p[grp][k] = fmaf(a_p[k], vv[k], acc_p[grp][k]);
+                    }
+                }
+            }
+        };
+
+        // Output row yo (complete in acc_p): MLP, fire gate and store of its
+        // two groups; stores of rows outside [y_begin, y_end) are dropped by an
+        // empty descriptor.  Then the sums shift by one row.
+        auto finish_row = [&](int yo) {
+            const bool out_ok = yo >= y_begin && yo < y_end;
+            const int phase = (yo - y_begin) & (rows_per_eval - 1);
+            if (out_ok && phase == 0) {
+                const int yy = min(yo + (lane >> lg_opr), dh - 1);
+                const uint64_t b0 = ((uint64_t)yy * dw + x0) >> 3;
+                fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, seed, threshold);
+                fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
+            }
+            const int yc = max(yo, 0);
+            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
+            const float4 *own = ring[yo & 3] + g * RS::PS;
+            const uint64_t row_b0 = ((uint64_t)yc * dw + x0) >> 3;
+            v4f acc[2][4];
+            float f[2][8];
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const float4 sp = own[1 + grp * 16 + n];
+                f[grp][0] = sp.x; f[grp][1] = sp.y; f[grp][2] = sp.z; f[grp][3] = sp.w;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[grp][4 + k] = acc_p[grp][k];
+                mlp.layer1(f[grp], acc[grp]);
+            }
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const v4f u = mlp.layer2(acc[grp]);
+                const int x = x0 + grp * 16 + n;
+                const uint64_t idx = (uint64_t)yc * dw + x;
+                const uint32_t off = x < dw ? (uint32_t)x * kCellBytes : kOut;
+                update_store(dst, wr, off, g, f[grp], u, upd, fire.bit(phase, idx, row_b0));
+            }
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    acc_p[grp][k] = acc_c[grp][k];
+                    acc_c[grp][k] = acc_n[grp][k];
+                    acc_n[grp][k] = cb[k];
+                }
+        };
+
+        // input rows q, q + 1 per iteration, from y_begin - 1 through y_end
+        // (plus one padding row when the count is odd)
+        for (int q = y_begin - 1; q <= y_end; q += 2) {
+            ra.issue(src, q + 2, dh, dw, x0);
+            rb.issue(src, q + 3, dh, dw, x0);
+            fold_row(q);
+            finish_row(q - 1);
+            __builtin_amdgcn_sched_barrier(0);
+            fold_row(q + 1);
+            finish_row(q);
+            __builtin_amdgcn_sched_barrier(0);
+            ra.commit(ring[(q + 2) & 3]);
+            rb.commit(ring[(q + 3) & 3]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // 3D: a work item is an 8 x 32 (y, x) column and a run of k3ZRun output
 // planes.  Input planes stream through a ring of three LDS plane slots
 // (planes p - 1 and p are in use while p + 1 is written).  Each input plane p
@@ -1179,16 +1419,35 @@ int device_cus() {
 constexpr int kBlocksPerCu = 2;
 
 template <typename T, int NIN, class Mlp>
-hipError_t launch_2d(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *dst,
+                     hipStream_t stream) {
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k2TY - 1) / k2TY);
     const int64_t tiles = (int64_t)tiles_x * tiles_y;
     if (tiles == 0) return hipSuccess;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
-    const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
-    nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
-        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles, a.w.conv_w,
-        a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed, a.threshold);
+    // Large levels: row streaming over strips of 32 cells and runs of
+    // k2RunRows rows, once there are at least two runs per wave slot.  Small
+    // levels: 16 x 32 tiles, where the per-run start-up of the row kernel
+    // (two rows loaded and waited for) would not be amortised.
+    const int64_t slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
+    const int64_t runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
+    const int64_t items = (int64_t)tiles_x * runs;
+    const bool rows = layout == Layout2d::Rows || (layout == Layout2d::Auto && items >= 2 * slots);
+    if (rows) {
+        if (items > INT32_MAX) return hipErrorInvalidValue;
+        const int grid = (int)std::min<int64_t>(items, slots);
+        nca_step_mfma_2d_rows<T, NIN, Mlp><<<grid, 64, 0, stream>>>(
+            (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)runs, k2RunRows,
+            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            a.threshold);
+    } else {
+        const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
+        nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
+            (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles,
+            a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            a.threshold);
+    }
     return hipGetLastError();
 }
 
@@ -1217,10 +1476,11 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
 }
 
 template <typename T, class Mlp>
-hipError_t dispatch(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+hipError_t dispatch(const StepArgs &a, Layout2d layout, const void *src, void *dst,
+                    hipStream_t stream) {
     if (a.ndim == 2) {
-        if (a.n_in == 1) return launch_2d<T, 1, Mlp>(a, src, dst, stream);
-        if (a.n_in == 3) return launch_2d<T, 3, Mlp>(a, src, dst, stream);
+        if (a.n_in == 1) return launch_2d<T, 1, Mlp>(a, layout, src, dst, stream);
+        if (a.n_in == 3) return launch_2d<T, 3, Mlp>(a, layout, src, dst, stream);
     } else {
         if (a.n_in == 1) return launch_3d<T, 1, Mlp>(a, src, dst, stream);
         if (a.n_in == 3) return launch_3d<T, 3, Mlp>(a, src, dst, stream);
@@ -1230,8 +1490,8 @@ hipError_t dispatch(const StepArgs &a, const void *src, void *dst, hipStream_t s
 
 }  // namespace
 
-hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, const void *src, void *dst,
-                            hipStream_t stream) {
+hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
+                            void *dst, hipStream_t stream) {
     // Buffer descriptors address a tile's rows with 32-bit offsets: rows of
     // more than (2^32 / 18 rows) bytes go to the vector kernel instead.
     const int64_t cell_bytes = (int64_t)kC * (a.dtype == Dtype::F32 ? 4 : 2);
@@ -1241,15 +1501,15 @@ hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, const void *src, voi
         mlp = a.dtype == Dtype::F32 ? MfmaMlp::Bf16x3 : MfmaMlp::F16;
     if (a.dtype == Dtype::F32) {
         switch (mlp) {
-            case MfmaMlp::F32: return dispatch<float, MlpF32>(a, src, dst, stream);
-            case MfmaMlp::Bf16x3: return dispatch<float, MlpBf16x3>(a, src, dst, stream);
+            case MfmaMlp::F32: return dispatch<float, MlpF32>(a, layout, src, dst, stream);
+            case MfmaMlp::Bf16x3: return dispatch<float, MlpBf16x3>(a, layout, src, dst, stream);
             default: return hipErrorInvalidValue;   // fp16 operands are too coarse for fp32 states
         }
     }
     switch (mlp) {
-        case MfmaMlp::F32: return dispatch<__half, MlpF32>(a, src, dst, stream);
-        case MfmaMlp::Bf16x3: return dispatch<__half, MlpBf16x3>(a, src, dst, stream);
-        case MfmaMlp::F16: return dispatch<__half, MlpF16>(a, src, dst, stream);
+        case MfmaMlp::F32: return dispatch<__half, MlpF32>(a, layout, src, dst, stream);
+        case MfmaMlp::Bf16x3: return dispatch<__half, MlpBf16x3>(a, layout, src, dst, stream);
+        case MfmaMlp::F16: return dispatch<__half, MlpF16>(a, layout, src, dst, stream);
         default: return hipErrorInvalidValue;
     }
 }

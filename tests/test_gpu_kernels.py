@@ -168,6 +168,8 @@ STEP_CASES = [
     # several 32-plane z runs with a ragged last run, ragged y tiles, 8-aligned
     # and unaligned rows
     ("f32", 3, 1, (70, 12, 40)), ("f16", 3, 3, (70, 10, 36)), ("f16", 3, 3, (33, 16, 64)),
+    # several 64-row runs of the 2D row layout with ragged last runs and strips
+    ("f32", 2, 3, (1, 150, 70)), ("f16", 2, 3, (1, 131, 40)),
 ]
 
 
@@ -179,9 +181,11 @@ STEP_CASES = [
 # fp16 perception sums on "mfma".
 STEP_TOL = {
     ("f32", "valu"): (2e-6, 1e-4), ("f32", "mfma_f32"): (2e-6, 1e-4),
-    ("f32", "mfma"): (5e-5, 5e-4),
+    ("f32", "mfma"): (5e-5, 5e-4), ("f32", "mfma_rows"): (5e-5, 5e-4),
+    ("f32", "mfma_tiles"): (5e-5, 5e-4),
     ("f16", "valu"): (1e-3, 1e-2), ("f16", "mfma_f32"): (1e-3, 1e-2),
-    ("f16", "mfma"): (3e-3, 1e-2),
+    ("f16", "mfma"): (3e-3, 1e-2), ("f16", "mfma_rows"): (3e-3, 1e-2),
+    ("f16", "mfma_tiles"): (3e-3, 1e-2),
 }
 
 
@@ -215,6 +219,7 @@ def test_one_step_matches_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
                                                 ("f32", 3, 1, (6, 20, 18)),
                                                 ("f16", 3, 3, (8, 12, 20)),
                                                 ("f32", 3, 1, (40, 12, 40)),
+                                                ("f32", 2, 3, (1, 140, 50)),
                                                 ("f16", 3, 3, (40, 10, 36))])
 def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     rng = np.random.default_rng(12)
