@@ -303,15 +303,19 @@ struct MlpF16 {
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1[jt], fh, b1[jt], 0, 0, 0);
     }
 
+    // ReLU after the rounding to fp16, as packed fp16 max (half the
+    // instructions of an fp32 max; rounding is monotonic and keeps 0, so the
+    // operand is the same fp16 value).
     __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
         v4f u = {0.f, 0.f, 0.f, 0.f};
+        const v8h zero = {};
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = relu(acc[2 * p + s / 4][s % 4]);
-            u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2[p], __builtin_convertvector(x, v8h), u,
-                                                       0, 0, 0);
+            for (int s = 0; s < 8; ++s) x[s] = acc[2 * p + s / 4][s % 4];
+            const v8h h = __builtin_elementwise_max(__builtin_convertvector(x, v8h), zero);
+            u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2[p], h, u, 0, 0, 0);
         }
         return u;
     }
@@ -515,9 +519,15 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
     // fp16 rows kept as fp16 in LDS: four channel-quad planes of 8-byte words
     // (channels 4q..4q+3 of a cell); a 16-byte chunk c (channels 8c..8c+7)
     // is split between quad planes 2c and 2c+1.  Same slots as commit().
+    // Quad plane stride of the fp16 planes (8-byte words): 16 mod 32, so the
+    // planes of lane groups g and g + 1 start 128 bytes apart modulo 256 (the
+    // 8-byte reads of one wave then hit disjoint banks; measured 8.8x fewer
+    // bank-conflict cycles than a multiple of 32).
+    static constexpr int PS16 = (HY * kHaloW + 1 + 15) / 32 * 32 + 16;
+    static_assert(PS16 > kDummyCell, "fp16 plane padding holds the dummy slot");
     __device__ static __forceinline__ void put_raw(uint2 *planes, int c, int cell, const uint4 &x) {
-        planes[(2 * c) * PS + cell] = make_uint2(x.x, x.y);
-        planes[(2 * c + 1) * PS + cell] = make_uint2(x.z, x.w);
+        planes[(2 * c) * PS16 + cell] = make_uint2(x.x, x.y);
+        planes[(2 * c + 1) * PS16 + cell] = make_uint2(x.z, x.w);
     }
 
     __device__ __forceinline__ void commit_raw(uint2 *planes) const {
@@ -1224,7 +1234,7 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint64_t seed,
     uint64_t threshold) {
     using Loader = RowLoader<__half, k3TY + 2>;
-    __shared__ uint2 ring[3][4 * Loader::PS];
+    __shared__ uint2 ring[3][4 * Loader::PS16];
     __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
     __shared__ uint64_t fire_words[4][8];   // [wave][b]: ballot b of the last evaluation
 
@@ -1268,7 +1278,7 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
     int centre[4];
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp)
-        centre[grp] = g * Loader::PS + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
+        centre[grp] = g * Loader::PS16 + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         int rest = item;
@@ -1368,18 +1378,24 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
                 v4f acc[4];
                 mlp.layer1_h(fh, acc);
                 const v4f u = mlp.layer2(acc);
-                const float f[8] = {(float)s01[0], (float)s01[1], (float)s23[0], (float)s23[1],
-                                    0.f, 0.f, 0.f, 0.f};
                 const int r = grp >> 1;
                 const int ly = 2 * wave + r;
                 const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
                 const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
                 const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
                 const uint32_t off =
-                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
+                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes + 8u * g : kOut;
                 const uint64_t fw = fire_words[wave][idx & 7];
                 const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
-                update_store(dst, wr, off, g, f, u, upd, fires);
+                // state + update in fp32, rounded once to fp16 (upd[k] = 0 keeps an
+                // input channel exactly); a cell that does not fire keeps its
+                // stored bits
+                const h2 n01 = {(_Float16)fmaf(upd[0], u[0], (float)s01[0]),
+                                (_Float16)fmaf(upd[1], u[1], (float)s01[1])};
+                const h2 n23 = {(_Float16)fmaf(upd[2], u[2], (float)s23[0]),
+                                (_Float16)fmaf(upd[3], u[3], (float)s23[1])};
+                const v2u out = {fires ? as_u32(n01) : sp.x, fires ? as_u32(n23) : sp.y};
+                __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
