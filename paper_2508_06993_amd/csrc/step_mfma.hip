@@ -1226,7 +1226,7 @@ __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uin
 
 constexpr int k3hBlocksPerCu = 3;
 
-template <int NIN>
+template <int NIN, bool ALIGNED>
 __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16(
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
     int tiles_x, int tiles_y, int items, const float *__restrict__ conv_w,
@@ -1267,10 +1267,11 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    // fire evaluations as in nca_step_mfma_3d
-    const int opr = (dw & 7) == 0 ? 4 : 8;
-    const int lg_opr = opr == 4 ? 2 : 3;
-    const int planes_per_eval = 64 / (2 * opr);
+    // fire evaluations as in nca_step_mfma_3d; ALIGNED (w % 8 == 0) makes the
+    // ballot and bit offsets of a lane's cells lane constants
+    constexpr int opr = ALIGNED ? 4 : 8;
+    constexpr int lg_opr = ALIGNED ? 2 : 3;
+    constexpr int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
@@ -1289,6 +1290,15 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
         const int y0 = ty * k3TY, x0 = tx * kTileW;
         const int z_begin = zr * k3ZRun;
         const int z_end = min(dd, z_begin + k3ZRun);
+        // store offsets of the lane's 4 cells within an output plane's tile rows
+        uint32_t offs[4];
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+            const int x = x0 + (grp & 1) * 16 + n;
+            offs[grp] = x < dw ? (uint32_t)(2 * wave + (grp >> 1)) * row_bytes +
+                                     (uint32_t)x * kCellBytes + 8u * g
+                               : kOut;
+        }
 
         // rolling perception sums (bias included) of outputs p - 1, p, p + 1,
         // channels (4g, 4g+1) in [.][0] and (4g+2, 4g+3) in [.][1]
@@ -1369,6 +1379,8 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
             const uint2 *own = ring[slot_prev];
+            uint64_t fw_lane = 0;
+            if constexpr (ALIGNED) fw_lane = fire_words[wave][n & 7];
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const uint2 sp = own[centre[grp]];
@@ -1379,14 +1391,18 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
                 mlp.layer1_h(fh, acc);
                 const v4f u = mlp.layer2(acc);
                 const int r = grp >> 1;
-                const int ly = 2 * wave + r;
-                const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
-                const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
-                const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
-                const uint32_t off =
-                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes + 8u * g : kOut;
-                const uint64_t fw = fire_words[wave][idx & 7];
-                const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
+                bool fires;
+                if constexpr (ALIGNED) {
+                    // cell n of the group is cell n % 8 of block (grp & 1) * 2 + n / 8 of its row
+                    fires = (fw_lane >> ((slot0 + r) * opr + (grp & 1) * 2 + (n >> 3))) & 1;
+                } else {
+                    const int y = y0 + 2 * wave + r, x = x0 + (grp & 1) * 16 + n;
+                    const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
+                    const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
+                    const uint64_t fw = fire_words[wave][idx & 7];
+                    fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
+                }
+                const uint32_t off = offs[grp];
                 // state + update in fp32, rounded once to fp16 (upd[k] = 0 keeps an
                 // input channel exactly); a cell that does not fire keeps its
                 // stored bits
@@ -1396,7 +1412,6 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
                                 (_Float16)fmaf(upd[3], u[3], (float)s23[1])};
                 const v2u out = {fires ? as_u32(n01) : sp.x, fires ? as_u32(n23) : sp.y};
                 __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
             }
 
 #pragma unroll
@@ -1477,7 +1492,9 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     if (items > INT32_MAX) return hipErrorInvalidValue;
     if constexpr (std::is_same_v<T, __half> && std::is_same_v<Mlp, MlpF16>) {
         const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * k3hBlocksPerCu);
-        nca_step_mfma_3d_f16<NIN><<<grid, kThreads, 0, stream>>>(
+        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true>
+                                     : nca_step_mfma_3d_f16<NIN, false>;
+        kern<<<grid, kThreads, 0, stream>>>(
             (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
             tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
             a.seed, a.threshold);

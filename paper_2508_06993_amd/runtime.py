@@ -4,6 +4,7 @@ only; the computation is the library's.
 """
 from __future__ import annotations
 
+import warnings
 from typing import List, Optional, Sequence
 
 import numpy as np
@@ -28,7 +29,10 @@ def upload_weights(levels, device="cuda") -> List[dict]:
 def to_device_image(image: np.ndarray, model: Model, device="cuda") -> torch.Tensor:
     """[D][H][W][n_in] numpy image -> contiguous device tensor of the model's storage type."""
     assert image.ndim == 4 and image.shape[-1] == model.n_in
-    t = torch.from_numpy(np.ascontiguousarray(image))
+    with warnings.catch_warnings():
+        # a read-only (memory-mapped) array is only read by the copy below
+        warnings.filterwarnings("ignore", message="The given NumPy array is not writable")
+        t = torch.from_numpy(np.ascontiguousarray(image))
     return t.to(device=device, dtype=model.torch_dtype)
 
 
