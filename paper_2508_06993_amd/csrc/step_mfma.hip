@@ -832,7 +832,7 @@ struct RowStream {
     }
 };
 
-template <typename T, int NIN, class Mlp>
+template <typename T, int NIN, class Mlp, bool ALIGNED>
 __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int runs,
     int run_rows, int items, const float *__restrict__ conv_w,
@@ -875,11 +875,13 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     __syncthreads();
     // Fire evaluations: a row takes opr lanes, so one evaluation serves
     // 64 / opr consecutive output rows (16 when rows are 8-aligned, else 8).
+    // ALIGNED (w % 8 == 0): a lane's cells always take ballot n % 8 at bit
+    // offset 2 grp + n / 8 within their row's slot.
     FireBits fire;
-    fire.aligned = (dw & 7) == 0;
-    fire.opr = fire.aligned ? 4 : 8;
-    const int lg_opr = fire.aligned ? 2 : 3;
-    const int rows_per_eval = 64 / fire.opr;
+    fire.aligned = ALIGNED;
+    fire.opr = ALIGNED ? 4 : 8;
+    constexpr int lg_opr = ALIGNED ? 2 : 3;
+    constexpr int rows_per_eval = ALIGNED ? 16 : 8;
     constexpr int kCellBytes = RS::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     int gq = g;
@@ -966,9 +968,15 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             for (int grp = 0; grp < 2; ++grp) {
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
-                const uint64_t idx = (uint64_t)yc * dw + x;
                 const uint32_t off = x < dw ? (uint32_t)x * kCellBytes : kOut;
-                update_store(dst, wr, off, g, f[grp], u, upd, fire.bit(phase, idx, row_b0));
+                bool fires;
+                if constexpr (ALIGNED) {
+                    fires = (fire.mine >> (phase * 4 + 2 * grp + (n >> 3))) & 1;
+                } else {
+                    const uint64_t idx = (uint64_t)yc * dw + x;
+                    fires = fire.bit(phase, idx, row_b0);
+                }
+                update_store(dst, wr, off, g, f[grp], u, upd, fires);
             }
 #pragma unroll
             for (int grp = 0; grp < 2; ++grp)
@@ -1468,7 +1476,9 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     if (rows) {
         if (items > INT32_MAX) return hipErrorInvalidValue;
         const int grid = (int)std::min<int64_t>(items, slots);
-        nca_step_mfma_2d_rows<T, NIN, Mlp><<<grid, 64, 0, stream>>>(
+        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_2d_rows<T, NIN, Mlp, true>
+                                     : nca_step_mfma_2d_rows<T, NIN, Mlp, false>;
+        kern<<<grid, 64, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)runs, k2RunRows,
             (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
             a.threshold);
