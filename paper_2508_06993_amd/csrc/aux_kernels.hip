@@ -2,6 +2,8 @@
 // upsample + image injection between levels, two-class readout, fire-mask
 // export.  All are single passes over HBM with coalesced 16-byte accesses
 // where the layout allows it.
+#include <algorithm>
+
 #include "launch.h"
 
 namespace octnca {
@@ -12,67 +14,88 @@ constexpr int kBlock = 256;
 
 inline unsigned grid_for(int64_t n) { return (unsigned)((n + kBlock - 1) / kBlock); }
 
+// Grids of the pyramid and upsample kernels: x covers the elements of one
+// row, y the rows and z the planes (each clamped to the hardware limit of
+// those grid dimensions, with the kernels looping over the rest).  The row
+// and plane come from the block index, so a thread's index arithmetic is a
+// few 32-bit operations (64-bit division per element made these kernels
+// instruction-bound).
+constexpr int64_t kMaxGridYZ = 65535;
+
+inline dim3 row_grid(int64_t row_elems, int64_t rows, int64_t planes) {
+    return dim3((unsigned)((row_elems + kBlock - 1) / kBlock),
+                (unsigned)std::min<int64_t>(rows, kMaxGridYZ),
+                (unsigned)std::min<int64_t>(planes, kMaxGridYZ));
+}
+
 // ---------------------------------------------------------------------------
-// Pyramid (Sec. 3.2; supplement S7): one thread per output element (cell, c).
+// Pyramid (Sec. 3.2; supplement S7): one thread per output element (cell, c)
+// of a row; the fz*fy*fx inputs are summed in fp32 in (dz, dy, dx) order and
+// the sum is divided by their count.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kBlock) void pool_kernel(const T *__restrict__ src,
-                                                      T *__restrict__ dst, int64_t dd, int64_t dh,
-                                                      int64_t dw, int fz, int fy, int fx,
-                                                      int n_in) {
-    const int64_t total = dd * dh * dw * n_in;
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= total) return;
-    const int c = (int)(i % n_in);
-    const int64_t cell = i / n_in;
-    const int64_t x = cell % dw;
-    const int64_t y = (cell / dw) % dh;
-    const int64_t z = cell / (dw * dh);
-    const int64_t sh = dh * fy, sw = dw * fx;
-    float acc = 0.f;
-    for (int a = 0; a < fz; ++a)
-        for (int b = 0; b < fy; ++b)
-            for (int e = 0; e < fx; ++e) {
-                const int64_t s = ((z * fz + a) * sh + (y * fy + b)) * sw + (x * fx + e);
-                acc += Storage<T>::to_float(src[s * n_in + c]);
-            }
-    dst[i] = Storage<T>::from_float(acc / (float)(fz * fy * fx));
+                                                      T *__restrict__ dst, int dd, int dh, int dw,
+                                                      int fz, int fy, int fx, int n_in) {
+    const uint32_t i = blockIdx.x * (uint32_t)kBlock + threadIdx.x;   // element in the row
+    if ((uint64_t)i >= (uint64_t)dw * n_in) return;
+    const uint32_t x = i / (uint32_t)n_in;
+    const uint32_t c = i - x * (uint32_t)n_in;
+    const int64_t sh = (int64_t)dh * fy, sw = (int64_t)dw * fx;
+    const float inv = (float)(fz * fy * fx);
+    for (int z = blockIdx.z; z < dd; z += gridDim.z) {
+        for (int y = blockIdx.y; y < dh; y += gridDim.y) {
+            float acc = 0.f;
+            for (int a = 0; a < fz; ++a)
+                for (int b = 0; b < fy; ++b) {
+                    const int64_t srow = (((int64_t)z * fz + a) * sh + ((int64_t)y * fy + b)) * sw;
+                    for (int e = 0; e < fx; ++e) {
+                        const int64_t s = srow + (int64_t)x * fx + e;
+                        acc += Storage<T>::to_float(src[s * n_in + c]);
+                    }
+                }
+            dst[((int64_t)z * dh + y) * dw * n_in + i] = Storage<T>::from_float(acc / inv);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
 // Upsample + inject (Sec. 3.2; supplement S6, Listings 2 and 3): one thread
-// per 16-byte chunk of a fine cell.
+// per 16-byte chunk of a fine cell of a row (consecutive threads write
+// consecutive chunks).
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ coarse,
-                                                          int64_t fd, int64_t fh, int64_t fw,
-                                                          int fz, int fy, int fx,
+__global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ coarse, int fd,
+                                                          int fh, int fw, int fz, int fy, int fx,
                                                           const T *__restrict__ img,
                                                           T *__restrict__ fine, int n_in) {
     constexpr int K = Storage<T>::kPerChunk;
     constexpr int NQ = kC / K;
-    const int64_t total = fd * fh * fw * NQ;
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= total) return;
-    const int q = (int)(i % NQ);
-    const int64_t cell = i / NQ;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (coarse != nullptr) {
-        const int64_t x = cell % fw;
-        const int64_t y = (cell / fw) % fh;
-        const int64_t z = cell / (fw * fh);
-        const int64_t ch = fh / fy, cw = fw / fx;
-        const int64_t parent = ((z / fz) * ch + (y / fy)) * cw + (x / fx);
-        v = reinterpret_cast<const uint4 *>(coarse + parent * kC)[q];
+    constexpr int kLgNQ = NQ == 4 ? 2 : 1;
+    const uint32_t i = blockIdx.x * (uint32_t)kBlock + threadIdx.x;   // chunk in the row
+    if ((uint64_t)i >= (uint64_t)fw * NQ) return;
+    const int q = (int)(i & (NQ - 1));
+    const uint32_t x = i >> kLgNQ;
+    const int64_t ch = fh / fy, cw = fw / fx;
+    const uint32_t px = x / (uint32_t)fx;
+    for (int z = blockIdx.z; z < fd; z += gridDim.z) {
+        for (int y = blockIdx.y; y < fh; y += gridDim.y) {
+            const int64_t cell = ((int64_t)z * fh + y) * fw + x;
+            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            if (coarse != nullptr) {
+                const int64_t parent = ((int64_t)(z / fz) * ch + y / fy) * cw + px;
+                v = reinterpret_cast<const uint4 *>(coarse + parent * kC)[q];
+            }
+            if (q * K < n_in) {
+                // this chunk holds input channels: overwrite them with the level's image
+                T vals[K];
+                __builtin_memcpy(vals, &v, sizeof(v));
+                for (int k = 0; k < K && q * K + k < n_in; ++k) vals[k] = img[cell * n_in + q * K + k];
+                __builtin_memcpy(&v, vals, sizeof(v));
+            }
+            reinterpret_cast<uint4 *>(fine + cell * kC)[q] = v;
+        }
     }
-    if (q * K < n_in) {
-        // this chunk holds input channels: overwrite them with the level's image
-        T vals[K];
-        __builtin_memcpy(vals, &v, sizeof(v));
-        for (int k = 0; k < K && q * K + k < n_in; ++k) vals[k] = img[cell * n_in + q * K + k];
-        __builtin_memcpy(&v, vals, sizeof(v));
-    }
-    reinterpret_cast<uint4 *>(fine + cell * kC)[q] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -102,30 +125,32 @@ __global__ __launch_bounds__(kBlock) void fire_mask_kernel(uint64_t seed, uint32
 
 hipError_t launch_pool(Dtype dt, const void *src, Extent3 e, void *dst, int fz, int fy, int fx,
                        int n_in, hipStream_t stream) {
-    const int64_t n = e.cells() * n_in;
-    if (n == 0) return hipSuccess;
+    if (e.cells() == 0) return hipSuccess;
+    const dim3 grid = row_grid(e.w * n_in, e.h, e.d);
     if (dt == Dtype::F32)
-        pool_kernel<float><<<grid_for(n), kBlock, 0, stream>>>(
-            (const float *)src, (float *)dst, e.d, e.h, e.w, fz, fy, fx, n_in);
+        pool_kernel<float><<<grid, kBlock, 0, stream>>>((const float *)src, (float *)dst,
+                                                         (int)e.d, (int)e.h, (int)e.w, fz, fy, fx,
+                                                         n_in);
     else
-        pool_kernel<__half><<<grid_for(n), kBlock, 0, stream>>>(
-            (const __half *)src, (__half *)dst, e.d, e.h, e.w, fz, fy, fx, n_in);
+        pool_kernel<__half><<<grid, kBlock, 0, stream>>>((const __half *)src, (__half *)dst,
+                                                          (int)e.d, (int)e.h, (int)e.w, fz, fy,
+                                                          fx, n_in);
     return hipGetLastError();
 }
 
 hipError_t launch_upsample(Dtype dt, const void *coarse, Extent3 e, int fz, int fy, int fx,
                            const void *img, void *fine, int n_in, hipStream_t stream) {
     const int nq = dt == Dtype::F32 ? kC / 4 : kC / 8;
-    const int64_t n = e.cells() * nq;
-    if (n == 0) return hipSuccess;
+    if (e.cells() == 0) return hipSuccess;
+    const dim3 grid = row_grid(e.w * nq, e.h, e.d);
     if (dt == Dtype::F32)
-        upsample_kernel<float><<<grid_for(n), kBlock, 0, stream>>>(
-            (const float *)coarse, e.d, e.h, e.w, fz, fy, fx, (const float *)img, (float *)fine,
-            n_in);
+        upsample_kernel<float><<<grid, kBlock, 0, stream>>>(
+            (const float *)coarse, (int)e.d, (int)e.h, (int)e.w, fz, fy, fx, (const float *)img,
+            (float *)fine, n_in);
     else
-        upsample_kernel<__half><<<grid_for(n), kBlock, 0, stream>>>(
-            (const __half *)coarse, e.d, e.h, e.w, fz, fy, fx, (const __half *)img,
-            (__half *)fine, n_in);
+        upsample_kernel<__half><<<grid, kBlock, 0, stream>>>(
+            (const __half *)coarse, (int)e.d, (int)e.h, (int)e.w, fz, fy, fx,
+            (const __half *)img, (__half *)fine, n_in);
     return hipGetLastError();
 }
 
