@@ -31,10 +31,12 @@
  *   - Fire mask (the paper draws it with PyTorch's generator; this library
  *     uses a counter-based generator so any implementation can reproduce
  *     it): Philox4x64-10 (Salmon et al., SC 2011) with counter
- *     (idx >> 3, step, level, 0) and key (seed, 0), one call per block of 8
+ *     (idx >> 3, step, level, b) and key (seed, 0), one call per block of 8
  *     cells; cell idx takes output word (idx >> 1) & 3, its upper 32 bits if
  *     idx is odd and its lower 32 bits if even, and fires iff that draw < T,
  *     where T = min(2^32, floor(fire_rate * 2^32)), fire_rate in [0, 1].
+ *     b is the image's index in a batch (octree_nca_infer_batch); every other
+ *     entry point uses b = 0.
  *   - Weights are fp32, per level, in device memory, in the layout of
  *     octnca_level_weights.
  *   - All pointers to arrays are DEVICE pointers unless marked "host".
@@ -60,7 +62,7 @@
 extern "C" {
 #endif
 
-#define OCTNCA_ABI_VERSION 1
+#define OCTNCA_ABI_VERSION 2
 
 typedef enum {
     OCTNCA_OK = 0,
@@ -155,6 +157,18 @@ int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1,
 int octree_nca_readout(const octnca_model *model, const void *state, octnca_extent extent,
                        uint8_t *seg, void *stream);
 
+/* K-class readout on the finest level, for models whose last K hidden
+ * channels score K classes (the paper's surgery data has several classes,
+ * Sec. 4): seg[p] = the index k in [0, K) of the largest of
+ * state[p, C-K+k], found by scanning k upwards and moving only on a strictly
+ * greater value, so ties go to the lower class and a NaN never replaces an
+ * earlier channel.  K = 2 gives the same result as octree_nca_readout.
+ *   state [extent][C];  classes K in [2, C - n_in];  seg [extent] uint8, written.
+ * Errors: EINVAL (null pointer, K out of range), ESHAPE, EUNSUPPORTED, EHIP. */
+int octree_nca_readout_classes(const octnca_model *model, const void *state,
+                               octnca_extent extent, int32_t classes, uint8_t *seg,
+                               void *stream);
+
 /* Bytes of device workspace octree_nca_infer needs for this model, finest
  * extent and pyramid: the images of levels 1..L-1, plus one finest-size state
  * buffer when final_state is given (two when it is NULL), each 256-byte
@@ -185,6 +199,26 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
                      const octnca_level_weights *weights, const int32_t *steps,
                      float fire_rate, uint64_t seed, void *workspace, size_t workspace_bytes,
                      void *final_state, uint8_t *seg, void *const *level_events, void *stream);
+
+/* Inference of a batch of images of the same extent (the paper's kernel
+ * works on one image and notes that a batch is an extra dimension to iterate
+ * over, supplement S3): image b runs exactly as octree_nca_infer, with the
+ * fire-mask counter word 3 set to b, so the images draw independent masks and
+ * image 0 reproduces octree_nca_infer.  The images run one after another on
+ * `stream` and share one workspace.
+ *   images       [batch][finest][n_in], storage type;  batch >= 1.
+ *   workspace    device, >= octree_nca_workspace_bytes(..., final_states != NULL).
+ *   final_states [batch][finest][C] written, or NULL.
+ *   segs         [batch][finest] uint8 written with the two-class readout, or NULL.
+ * Outputs must not overlap the images or the workspace (EINVAL).  All images'
+ * arguments are checked before anything is enqueued.
+ * Errors: EINVAL, ESHAPE, EUNSUPPORTED, ESPACE, EHIP. */
+int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_t batch,
+                           octnca_extent finest, int32_t levels, const int32_t *factors,
+                           const octnca_level_weights *weights, const int32_t *steps,
+                           float fire_rate, uint64_t seed, void *workspace,
+                           size_t workspace_bytes, void *final_states, uint8_t *segs,
+                           void *stream);
 
 /* Export the fire mask of one step of one level (test hook for the
  * generator described above): mask[idx] = 1 if cell idx fires, else 0.

@@ -127,15 +127,17 @@ def fire_threshold(fire_rate: float) -> int:
     return min(1 << 32, int(np.floor(p * 4294967296.0)))
 
 
-def fire_bits(seed: int, level: int, step: int, idx: np.ndarray, fire_rate: float) -> np.ndarray:
+def fire_bits(seed: int, level: int, step: int, idx: np.ndarray, fire_rate: float,
+              batch: int = 0) -> np.ndarray:
     """Fire bit of each cell with canonical linear index ``idx``
     (idx = (z*H + y)*W + x at its level).  Philox4x64-10 with counter
-    (idx >> 3, step, level, 0) and key (seed, 0) gives four 64-bit words for
-    a block of 8 consecutive cells; cell idx takes word (idx >> 1) & 3 and,
-    within it, the upper 32 bits when idx is odd, the lower 32 bits when even."""
+    (idx >> 3, step, level, batch) and key (seed, 0) gives four 64-bit words
+    for a block of 8 consecutive cells; cell idx takes word (idx >> 1) & 3 and,
+    within it, the upper 32 bits when idx is odd, the lower 32 bits when even.
+    ``batch`` is the image's index in a batch (0 for a single image)."""
     idx = np.asarray(idx, dtype=np.uint64)
     octs, where = np.unique(idx >> np.uint64(3), return_inverse=True)
-    words = np.stack(philox4x64((octs, np.uint64(step), np.uint64(level), np.uint64(0)),
+    words = np.stack(philox4x64((octs, np.uint64(step), np.uint64(level), np.uint64(batch)),
                                 (np.uint64(seed), np.uint64(0))), axis=-1)   # [octs][4]
     w = words[where.reshape(idx.shape), ((idx >> np.uint64(1)) & np.uint64(3)).astype(np.intp)]
     odd = (idx & np.uint64(1)) == np.uint64(1)
@@ -143,11 +145,12 @@ def fire_bits(seed: int, level: int, step: int, idx: np.ndarray, fire_rate: floa
     return draw < np.uint64(fire_threshold(fire_rate))
 
 
-def fire_mask(seed: int, level: int, step: int, extent: Sequence[int], fire_rate: float) -> np.ndarray:
+def fire_mask(seed: int, level: int, step: int, extent: Sequence[int], fire_rate: float,
+              batch: int = 0) -> np.ndarray:
     """Fire bits of a whole level, shape [D][H][W] (bool)."""
     d, h, w = extent
     idx = np.arange(d * h * w, dtype=np.uint64)
-    return fire_bits(seed, level, step, idx, fire_rate).reshape(d, h, w)
+    return fire_bits(seed, level, step, idx, fire_rate, batch).reshape(d, h, w)
 
 
 # --------------------------------------------------------------------------
@@ -199,7 +202,8 @@ def linear_index(origin: Sequence[int], shape: Sequence[int], grid: Sequence[int
 
 
 def nca_step(state: np.ndarray, weights, n_in: int, ndim: int, level: int, step: int,
-             seed: int, fire_rate: float, dtype, origin=(0, 0, 0), grid=None) -> np.ndarray:
+             seed: int, fire_rate: float, dtype, origin=(0, 0, 0), grid=None,
+             batch: int = 0) -> np.ndarray:
     """One synchronous NCA step of every cell of ``state`` (out of place).
 
     ``state`` covers the window [origin, origin + shape) of a level of extent
@@ -212,17 +216,18 @@ def nca_step(state: np.ndarray, weights, n_in: int, ndim: int, level: int, step:
     p = perceive(s, weights.conv_w, weights.conv_b, ndim)
     u = update(s, p, weights.w1, weights.b1, weights.w2)
     idx = linear_index(origin, state.shape[:3], grid)
-    m = fire_bits(seed, level, step, idx, fire_rate).astype(np.float64)
+    m = fire_bits(seed, level, step, idx, fire_rate, batch).astype(np.float64)
     new = s.copy()
     new[..., n_in:] = s[..., n_in:] + m[..., None] * u[..., n_in:]
     return to_storage(new, dtype)
 
 
 def run_level(state: np.ndarray, weights, n_in: int, ndim: int, level: int, steps: int,
-              seed: int, fire_rate: float, dtype) -> np.ndarray:
+              seed: int, fire_rate: float, dtype, batch: int = 0) -> np.ndarray:
     """``steps`` consecutive steps t = 0 .. steps-1 of one level."""
     for t in range(steps):
-        state = nca_step(state, weights, n_in, ndim, level, t, seed, fire_rate, dtype)
+        state = nca_step(state, weights, n_in, ndim, level, t, seed, fire_rate, dtype,
+                         batch=batch)
     return state
 
 
@@ -236,6 +241,24 @@ def readout(state: np.ndarray) -> np.ndarray:
     return (state[..., -1] > state[..., -2]).astype(np.uint8)
 
 
+def readout_classes(state: np.ndarray, classes: int) -> np.ndarray:
+    """K-class segmentation from the last K channels (the paper's surgery data
+    has several classes, Sec. 4): the index k in [0, K) of the largest of
+    state[..., C-K+k], scanning k upwards and moving only on a strictly greater
+    value, so ties go to the lower index and a NaN is never chosen over an
+    earlier channel.  K = 2 is ``readout``."""
+    c = state.shape[-1]
+    assert 2 <= classes <= c
+    s = state[..., c - classes:]
+    best = np.zeros(state.shape[:-1], dtype=np.intp)
+    best_val = s[..., 0]
+    for k in range(1, classes):
+        up = s[..., k] > best_val
+        best = np.where(up, k, best)
+        best_val = np.where(up, s[..., k], best_val)
+    return best.astype(np.uint8)
+
+
 @dataclass
 class InferLog:
     max_abs_per_level: List[float]
@@ -243,11 +266,12 @@ class InferLog:
 
 def infer(image: np.ndarray, weights: Sequence, *, ndim: int, n_in: int, channels: int,
           factors: Sequence[Sequence[int]], steps: Sequence[int], fire_rate: float,
-          seed: int, dtype, log: Optional[InferLog] = None):
+          seed: int, dtype, log: Optional[InferLog] = None, batch: int = 0):
     """Full OctreeNCA inference: pyramid, coarsest seed, then for every level
     from coarsest to finest an upsample+inject (except the coarsest) followed
     by that level's steps with that level's weights.  Returns (state, seg) of
-    the finest level."""
+    the finest level.  ``batch`` is the image's index in a batch: it only
+    enters the fire-mask counter."""
     levels = len(steps)
     assert len(weights) == levels and len(factors) == levels - 1
     pyr = build_pyramid(image, factors, dtype)
@@ -255,7 +279,8 @@ def infer(image: np.ndarray, weights: Sequence, *, ndim: int, n_in: int, channel
     for lvl in range(levels - 1, -1, -1):
         if lvl < levels - 1:
             state = upsample_inject(state, factors[lvl], pyr[lvl], dtype)
-        state = run_level(state, weights[lvl], n_in, ndim, lvl, steps[lvl], seed, fire_rate, dtype)
+        state = run_level(state, weights[lvl], n_in, ndim, lvl, steps[lvl], seed, fire_rate, dtype,
+                          batch=batch)
         if log is not None:
             log.max_abs_per_level.append(float(np.max(np.abs(state.astype(np.float64)))))
     return state, readout(state)

@@ -21,9 +21,9 @@ from .build import LIB_PATH
 __all__ = [
     "OctreeNCAError", "Model", "lib", "library_path", "level_weights_struct",
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
-    "octree_nca_readout", "octree_nca_workspace_bytes", "octree_nca_infer",
-    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
-    "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL", "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
+    "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_fire_mask", "octree_nca_strerror",
+    "octree_nca_abi_version", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL", "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
     "OCTNCA_EHIP", "OCTNCA_ESPACE", "OCTNCA_F32", "OCTNCA_F16",
 ]
 
@@ -33,8 +33,9 @@ OCTNCA_F32, OCTNCA_F16 = 0, 1
 
 EXPORTED_SYMBOLS = (
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
-    "octree_nca_readout", "octree_nca_workspace_bytes", "octree_nca_infer",
-    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
+    "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_fire_mask", "octree_nca_strerror",
+    "octree_nca_abi_version",
 )
 
 
@@ -70,12 +71,17 @@ _SIGS = {
                                     ctypes.POINTER(_LevelWeights), _I32, _I32, ctypes.c_float,
                                     ctypes.c_uint64, ctypes.POINTER(_I32), _P]),
     "octree_nca_readout": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _P, _P]),
+    "octree_nca_readout_classes": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32, _P, _P]),
     "octree_nca_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(_Model), _Extent, _I32,
                                                      ctypes.POINTER(_I32), _I32]),
     "octree_nca_infer": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32, ctypes.POINTER(_I32),
                                 ctypes.POINTER(_LevelWeights), ctypes.POINTER(_I32),
                                 ctypes.c_float, ctypes.c_uint64, _P, ctypes.c_size_t, _P, _P,
                                 ctypes.POINTER(_P), _P]),
+    "octree_nca_infer_batch": (_I32, [ctypes.POINTER(_Model), _P, _I32, _Extent, _I32,
+                                      ctypes.POINTER(_I32), ctypes.POINTER(_LevelWeights),
+                                      ctypes.POINTER(_I32), ctypes.c_float, ctypes.c_uint64, _P,
+                                      ctypes.c_size_t, _P, _P, _P]),
     "octree_nca_fire_mask": (_I32, [ctypes.c_uint64, _I32, _I32, _Extent, ctypes.c_float, _P,
                                     _P]),
     "octree_nca_strerror": (ctypes.c_char_p, [ctypes.c_int]),
@@ -235,6 +241,15 @@ def octree_nca_readout(model: Model, state, seg, stream=None) -> None:
     _check(st, "octree_nca_readout")
 
 
+def octree_nca_readout_classes(model: Model, state, classes: int, seg, stream=None) -> None:
+    d, h, w = state.shape[:3]
+    st = lib().octree_nca_readout_classes(ctypes.byref(model.struct()),
+                                          _ptr(state, model.torch_dtype, "state"),
+                                          _extent((d, h, w)), int(classes),
+                                          _ptr(seg, torch.uint8, "seg"), _stream(stream))
+    _check(st, "octree_nca_readout_classes")
+
+
 def octree_nca_workspace_bytes(model: Model, finest, factors, with_final_state=True) -> int:
     levels = len(factors) + 1
     n = lib().octree_nca_workspace_bytes(ctypes.byref(model.struct()), _extent(finest), levels,
@@ -263,6 +278,26 @@ def octree_nca_infer(model: Model, image, factors, weights, steps, fire_rate: fl
                                 _ptr(final_state, model.torch_dtype, "final_state"),
                                 _ptr(seg, torch.uint8, "seg"), ev, _stream(stream))
     _check(st, "octree_nca_infer")
+
+
+def octree_nca_infer_batch(model: Model, images, factors, weights, steps, fire_rate: float,
+                           seed: int, workspace, final_states=None, segs=None,
+                           stream=None) -> None:
+    """images: [batch][d][h][w][n_in]; final_states [batch][d][h][w][C] or None;
+    segs [batch][d][h][w] uint8 or None."""
+    levels = len(steps)
+    batch, d, h, w = images.shape[:4]
+    ws = (_LevelWeights * levels)(*[level_weights_struct(x) for x in weights])
+    st = lib().octree_nca_infer_batch(ctypes.byref(model.struct()),
+                                      _ptr(images, model.torch_dtype, "images"), int(batch),
+                                      _extent((d, h, w)), levels, _factors(factors), ws,
+                                      (_I32 * levels)(*[int(s) for s in steps]),
+                                      float(fire_rate), int(seed),
+                                      _ptr(workspace, torch.uint8, "workspace"),
+                                      workspace.numel(),
+                                      _ptr(final_states, model.torch_dtype, "final_states"),
+                                      _ptr(segs, torch.uint8, "segs"), _stream(stream))
+    _check(st, "octree_nca_infer_batch")
 
 
 def octree_nca_fire_mask(seed: int, level: int, step: int, extent, fire_rate: float, mask,

@@ -95,8 +95,9 @@ Dtype dtype_of(const octnca_model *m) { return m->state_dtype == OCTNCA_F16 ? Dt
 // Enqueue `steps` steps; bufs[t % 2] -> bufs[(t + 1) % 2].
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
               const octnca_level_weights *w, int32_t level, int32_t steps, uint64_t seed,
-              uint64_t threshold, hipStream_t stream) {
+              uint64_t threshold, hipStream_t stream, uint32_t batch = 0) {
     StepArgs a;
+    a.batch = batch;
     a.dtype = dtype_of(m);
     a.ndim = m->ndim;
     a.n_in = m->n_in;
@@ -234,6 +235,18 @@ int octree_nca_readout(const octnca_model *model, const void *state, octnca_exte
                                      (hipStream_t)stream));
 }
 
+int octree_nca_readout_classes(const octnca_model *model, const void *state, octnca_extent extent,
+                               int32_t classes, uint8_t *seg, void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if ((st = check_extent(model, extent))) return st;
+    if (state == nullptr || seg == nullptr || classes < 2 || classes > kC - model->n_in)
+        return OCTNCA_EINVAL;
+    return hip_status(launch_readout_classes(dtype_of(model), state,
+                                             extent.d * extent.h * extent.w, classes, seg,
+                                             (hipStream_t)stream));
+}
+
 int octree_nca_fire_mask(uint64_t seed, int32_t level, int32_t step, octnca_extent extent,
                          float fire_rate, uint8_t *mask, void *stream) {
     uint64_t threshold;
@@ -255,11 +268,15 @@ size_t octree_nca_workspace_bytes(const octnca_model *model, octnca_extent fines
     return p.bytes;
 }
 
-int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent finest,
-                     int32_t levels, const int32_t *factors, const octnca_level_weights *weights,
-                     const int32_t *steps, float fire_rate, uint64_t seed, void *workspace,
-                     size_t workspace_bytes, void *final_state, uint8_t *seg,
-                     void *const *level_events, void *stream) {
+}  // extern "C"
+
+namespace {
+
+int infer_impl(const octnca_model *model, const void *image, octnca_extent finest,
+               int32_t levels, const int32_t *factors, const octnca_level_weights *weights,
+               const int32_t *steps, float fire_rate, uint64_t seed, void *workspace,
+               size_t workspace_bytes, void *final_state, uint8_t *seg,
+               void *const *level_events, void *stream, uint32_t batch, bool check_only) {
     Plan p;
     int st = make_plan(model, finest, levels, factors, final_state != nullptr, &p);
     if (st) return st;
@@ -284,6 +301,7 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
     if (overlap(workspace, p.bytes, image,
                 (size_t)(finest.d * finest.h * finest.w) * model->n_in * eb))
         return OCTNCA_EINVAL;
+    if (check_only) return OCTNCA_OK;
 
     // bufs[0] ends up holding the final state: the coarsest seed goes to the
     // buffer that makes the parity of (upsamples + steps) land there.
@@ -318,7 +336,7 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
             hipEventRecord((hipEvent_t)level_events[2 * l], s) != hipSuccess)
             return OCTNCA_EHIP;
         st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, steps[l], seed,
-                       threshold, s);
+                       threshold, s, batch);
         if (st) return st;
         cur ^= steps[l] & 1;
         if (level_events && level_events[2 * l + 1] &&
@@ -329,6 +347,68 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
     if (seg != nullptr &&
         launch_readout(dt, bufs[cur], finest.d * finest.h * finest.w, seg, s) != hipSuccess)
         return OCTNCA_EHIP;
+    return OCTNCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent finest,
+                     int32_t levels, const int32_t *factors, const octnca_level_weights *weights,
+                     const int32_t *steps, float fire_rate, uint64_t seed, void *workspace,
+                     size_t workspace_bytes, void *final_state, uint8_t *seg,
+                     void *const *level_events, void *stream) {
+    return infer_impl(model, image, finest, levels, factors, weights, steps, fire_rate, seed,
+                      workspace, workspace_bytes, final_state, seg, level_events, stream, 0,
+                      false);
+}
+
+int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_t batch,
+                           octnca_extent finest, int32_t levels, const int32_t *factors,
+                           const octnca_level_weights *weights, const int32_t *steps,
+                           float fire_rate, uint64_t seed, void *workspace,
+                           size_t workspace_bytes, void *final_states, uint8_t *segs,
+                           void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if (images == nullptr || batch < 1) return OCTNCA_EINVAL;
+    if ((st = check_extent(model, finest))) return st;
+    const size_t cells = (size_t)(finest.d * finest.h * finest.w);
+    const size_t eb = elem_bytes(model);
+    const size_t image_bytes = cells * model->n_in * eb, state_bytes = cells * kC * eb;
+    // the batch's outputs must not overlap its inputs or the workspace
+    if (final_states != nullptr &&
+        (overlap(final_states, state_bytes * batch, images, image_bytes * batch) ||
+         (workspace != nullptr &&
+          overlap(final_states, state_bytes * batch, workspace, workspace_bytes))))
+        return OCTNCA_EINVAL;
+    if (segs != nullptr &&
+        (overlap(segs, cells * batch, images, image_bytes * batch) ||
+         (final_states != nullptr && overlap(segs, cells * batch, final_states,
+                                             state_bytes * batch)) ||
+         (workspace != nullptr && overlap(segs, cells * batch, workspace, workspace_bytes))))
+        return OCTNCA_EINVAL;
+    if (workspace != nullptr && overlap(workspace, workspace_bytes, images, image_bytes * batch))
+        return OCTNCA_EINVAL;
+    auto image_of = [&](int32_t b) { return (const char *)images + image_bytes * b; };
+    auto state_of = [&](int32_t b) {
+        return final_states ? (void *)((char *)final_states + state_bytes * b) : nullptr;
+    };
+    auto seg_of = [&](int32_t b) { return segs ? segs + cells * b : nullptr; };
+    // every image's arguments are checked before anything is enqueued
+    for (int32_t b = 0; b < batch; ++b) {
+        st = infer_impl(model, image_of(b), finest, levels, factors, weights, steps, fire_rate,
+                        seed, workspace, workspace_bytes, state_of(b), seg_of(b), nullptr, stream,
+                        (uint32_t)b, true);
+        if (st) return st;
+    }
+    for (int32_t b = 0; b < batch; ++b) {
+        st = infer_impl(model, image_of(b), finest, levels, factors, weights, steps, fire_rate,
+                        seed, workspace, workspace_bytes, state_of(b), seg_of(b), nullptr, stream,
+                        (uint32_t)b, false);
+        if (st) return st;
+    }
     return OCTNCA_OK;
 }
 

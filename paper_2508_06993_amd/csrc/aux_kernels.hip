@@ -99,6 +99,31 @@ __global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ 
 }
 
 // ---------------------------------------------------------------------------
+// K-class readout (several classes, as in the paper's surgery data, Sec. 4):
+// seg = index k in [0, K) of the largest of state[C-K+k], scanning k upwards
+// and moving only on a strictly greater value (ties to the lower class; a NaN
+// never replaces an earlier channel).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kBlock) void readout_classes_kernel(const T *__restrict__ state,
+                                                                 int64_t cells, int classes,
+                                                                 uint8_t *__restrict__ seg) {
+    const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (p >= cells) return;
+    const T *s = state + p * kC + (kC - classes);
+    float best = Storage<T>::to_float(s[0]);
+    int best_k = 0;
+    for (int k = 1; k < classes; ++k) {
+        const float v = Storage<T>::to_float(s[k]);
+        if (v > best) {
+            best = v;
+            best_k = k;
+        }
+    }
+    seg[p] = (uint8_t)best_k;
+}
+
+// ---------------------------------------------------------------------------
 // Readout (Sec. 3.2): seg = state[C-1] > state[C-2].
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -118,7 +143,7 @@ __global__ __launch_bounds__(kBlock) void fire_mask_kernel(uint64_t seed, uint32
                                                            uint8_t *__restrict__ mask) {
     const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (p >= cells) return;
-    mask[p] = cell_fires(seed, level, step, (uint64_t)p, threshold) ? 1 : 0;
+    mask[p] = cell_fires(seed, level, step, 0, (uint64_t)p, threshold) ? 1 : 0;
 }
 
 }  // namespace
@@ -163,6 +188,18 @@ hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, uint8_t *s
     else
         readout_kernel<__half><<<grid_for(cells), kBlock, 0, stream>>>((const __half *)state,
                                                                        cells, seg);
+    return hipGetLastError();
+}
+
+hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int classes,
+                                  uint8_t *seg, hipStream_t stream) {
+    if (cells == 0) return hipSuccess;
+    if (dt == Dtype::F32)
+        readout_classes_kernel<float><<<grid_for(cells), kBlock, 0, stream>>>(
+            (const float *)state, cells, classes, seg);
+    else
+        readout_classes_kernel<__half><<<grid_for(cells), kBlock, 0, stream>>>(
+            (const __half *)state, cells, classes, seg);
     return hipGetLastError();
 }
 

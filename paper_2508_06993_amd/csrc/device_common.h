@@ -16,10 +16,11 @@ constexpr int kH = 64;   // hidden units of the per-cell MLP
 // Numbers: As Easy as 1, 2, 3", SC 2011).  The paper only asks for a 50%
 // Bernoulli gate per cell and step (Sec. 3.1); a counter-based generator makes
 // the gate a pure function of (seed, level, step, cell), independent of launch
-// shape.  Counter (idx >> 3, step, level, 0), key (seed, 0): one call covers
-// 8 consecutive cells, cell idx takes the upper (odd idx) or lower (even idx)
-// 32 bits of output word (idx >> 1) & 3 and fires iff that draw is below the
-// threshold T = min(2^32, floor(rate * 2^32)).
+// shape.  Counter (idx >> 3, step, level, batch), key (seed, 0): one call
+// covers 8 consecutive cells, cell idx takes the upper (odd idx) or lower
+// (even idx) 32 bits of output word (idx >> 1) & 3 and fires iff that draw is
+// below the threshold T = min(2^32, floor(rate * 2^32)).  batch is the image's
+// index in a batch (0 for a single image).
 // ---------------------------------------------------------------------------
 struct Philox4x64Out {
     uint64_t w[4];
@@ -66,8 +67,8 @@ __device__ __forceinline__ uint32_t draw_of(const Philox4x64Out &r, uint32_t cel
 }
 
 __device__ __forceinline__ bool cell_fires(uint64_t seed, uint32_t level, uint32_t step,
-                                           uint64_t idx, uint64_t threshold) {
-    const Philox4x64Out r = philox4x64_10(idx >> 3, step, level, 0, seed, 0);
+                                           uint32_t batch, uint64_t idx, uint64_t threshold) {
+    const Philox4x64Out r = philox4x64_10(idx >> 3, step, level, batch, seed, 0);
     return (uint64_t)draw_of(r, (uint32_t)idx & 7u) < threshold;
 }
 

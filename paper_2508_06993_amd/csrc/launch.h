@@ -27,6 +27,8 @@ hipError_t launch_upsample(Dtype dt, const void *coarse, Extent3 fine_ext, int f
 
 hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, uint8_t *seg,
                           hipStream_t stream);
+hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int classes,
+                                  uint8_t *seg, hipStream_t stream);
 
 hipError_t launch_fire_mask(uint64_t seed, uint32_t level, uint32_t step, int64_t cells,
                             uint64_t threshold, uint8_t *mask, hipStream_t stream);
@@ -40,6 +42,7 @@ struct StepArgs {
     LevelWeightsDev w;
     uint32_t level;
     uint32_t step;
+    uint32_t batch = 0;   // image index in a batch (fire-mask counter word 3)
     uint64_t seed;
     uint64_t threshold;
 };

@@ -340,8 +340,9 @@ struct FireBallots {
 };
 
 __device__ __forceinline__ FireBallots fire_ballots(uint64_t block, uint32_t step, uint32_t level,
-                                                    uint64_t seed, uint64_t threshold) {
-    const Philox4x64Out r = philox4x64_10(block, step, level, 0, seed, 0);
+                                                    uint32_t batch, uint64_t seed,
+                                                    uint64_t threshold) {
+    const Philox4x64Out r = philox4x64_10(block, step, level, batch, seed, 0);
     FireBallots f;
 #pragma unroll
     for (int b = 0; b < 8; ++b) f.w[b] = __ballot((uint64_t)draw_of(r, (uint32_t)b) < threshold);
@@ -632,7 +633,7 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int tiles_x, int tiles,
     const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
-    uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
     using Loader = RowLoader<T, k2TY + 2>;
     __shared__ float4 planes[4 * Loader::PS];
     __shared__ float4 tapw[9][4];       // [tap][quad] conv weights of channels 4q..4q+3
@@ -705,7 +706,7 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
             const int ty2 = t2 / tiles_x;
             const uint64_t row = (uint64_t)(ty2 * k2TY + 4 * wave + ((lane >> lg_opr) & 3));
             const uint64_t b0 = (row * dw + (uint64_t)(t2 - ty2 * tiles_x) * kTileW) >> 3;
-            fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, seed, threshold);
+            fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, batch, seed, threshold);
             fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
         }
         const int slot0 = phase * 4;
@@ -837,7 +838,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int runs,
     int run_rows, int items, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
-    const float *__restrict__ w2, uint32_t level, uint32_t step, uint64_t seed,
+    const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
     uint64_t threshold) {
     using RS = RowStream<T>;
     __shared__ float4 ring[4][RS::kSlotWords];   // row y in slot y & 3
@@ -947,7 +948,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             if (out_ok && phase == 0) {
                 const int yy = min(yo + (lane >> lg_opr), dh - 1);
                 const uint64_t b0 = ((uint64_t)yy * dw + x0) >> 3;
-                fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, seed, threshold);
+                fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, batch, seed, threshold);
                 fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
             }
             const int yc = max(yo, 0);
@@ -1024,7 +1025,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const T *__restrict__ src, T *__restrict__ dst, int dd, int dh, int dw, int tiles_x,
     int tiles_y, int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
-    uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
     using Loader = RowLoader<T, k3TY + 2>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
@@ -1166,7 +1167,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 const uint64_t row =
                     (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
                 const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
-                                                    step, level, seed, threshold);
+                                                    step, level, batch, seed, threshold);
                 uint64_t word = fb.w[0];
 #pragma unroll
                 for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
@@ -1239,7 +1240,7 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
     int tiles_x, int tiles_y, int items, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
-    const float *__restrict__ w2, uint32_t level, uint32_t step, uint64_t seed,
+    const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
     uint64_t threshold) {
     using Loader = RowLoader<__half, k3TY + 2>;
     __shared__ uint2 ring[3][4 * Loader::PS16];
@@ -1377,7 +1378,7 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
                 const uint64_t row =
                     (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
                 const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
-                                                    step, level, seed, threshold);
+                                                    step, level, batch, seed, threshold);
                 uint64_t word = fb.w[0];
 #pragma unroll
                 for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
@@ -1480,13 +1481,13 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
                                      : nca_step_mfma_2d_rows<T, NIN, Mlp, false>;
         kern<<<grid, 64, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)runs, k2RunRows,
-            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
             a.threshold);
     } else {
         const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
         nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles,
-            a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
             a.threshold);
     }
     return hipGetLastError();
@@ -1506,13 +1507,13 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
                                      : nca_step_mfma_3d_f16<NIN, false>;
         kern<<<grid, kThreads, 0, stream>>>(
             (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
-            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
+            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
             a.seed, a.threshold);
     } else {
         const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * kBlocksPerCu);
         nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
-            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed,
+            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
             a.threshold);
     }
     return hipGetLastError();

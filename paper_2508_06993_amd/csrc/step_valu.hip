@@ -23,7 +23,7 @@ __global__ __launch_bounds__(kValuThreads) void nca_step_valu(
     const T *__restrict__ src, T *__restrict__ dst, int dd, int dh, int dw, int tiles_x,
     int tiles_y, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
-    uint32_t level, uint32_t step, uint64_t seed, uint64_t threshold) {
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
     using S = Storage<T>;
     constexpr int K = S::kPerChunk;                 // channels per 16-byte chunk
     constexpr int NQ = kC / K;                      // chunks per cell
@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kValuThreads) void nca_step_valu(
     }
 
     const int64_t idx = ((int64_t)z * dh + y) * dw + x;
-    const bool fire = cell_fires(seed, level, step, (uint64_t)idx, threshold);
+    const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
     float out[kC];
 #pragma unroll
     for (int c = 0; c < kC; ++c) out[c] = (c >= NIN && fire) ? f[c] + u[c] : f[c];
@@ -127,7 +127,7 @@ hipError_t launch_valu(const StepArgs &a, const void *src, void *dst, hipStream_
     if (blocks == 0) return hipSuccess;
     nca_step_valu<T, NDIM, NIN><<<(unsigned)blocks, kValuThreads, 0, stream>>>(
         (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
-        a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.seed, a.threshold);
+        a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold);
     return hipGetLastError();
 }
 

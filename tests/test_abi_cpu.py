@@ -54,7 +54,8 @@ def test_library_exports_every_declared_symbol(lib, library_path):
 
 
 def test_version_and_strerror(lib):
-    assert lib.octree_nca_abi_version() == 1
+    declared = int(re.search(r"#define OCTNCA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert lib.octree_nca_abi_version() == declared == 2
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.octree_nca_strerror(st).decode() not in ("", "unknown status")
     assert lib.octree_nca_strerror(17).decode() == "unknown status"
@@ -158,6 +159,57 @@ def test_infer_rejects_small_workspace_and_bad_steps(lib):
     # final state inside the workspace
     assert lib.octree_nca_infer(model(), image, ext, L, f, ws, steps, 0.5, 0, wsp, need,
                                 ctypes.c_void_p(wsp.value + 256), None, None, None) == EINVAL
+
+
+@pytest.mark.parametrize("classes,n_in,expect", [(1, 3, EINVAL), (0, 3, EINVAL),
+                                                  (14, 3, EINVAL), (16, 1, EINVAL),
+                                                  (-2, 3, EINVAL)])
+def test_readout_classes_range(lib, classes, n_in, expect):
+    st = lib.octree_nca_readout_classes(model(n_in=n_in), FAKE, _Extent(1, 8, 8), classes, FAKE2,
+                                        None)
+    assert st == expect
+
+
+def test_readout_classes_other_checks(lib):
+    assert lib.octree_nca_readout_classes(model(), None, _Extent(1, 8, 8), 2, FAKE2,
+                                          None) == EINVAL
+    assert lib.octree_nca_readout_classes(model(), FAKE, _Extent(1, 8, 8), 2, None,
+                                          None) == EINVAL
+    assert lib.octree_nca_readout_classes(model(), FAKE, _Extent(2, 8, 8), 2, FAKE2,
+                                          None) == ESHAPE
+    assert lib.octree_nca_readout_classes(model(c=12), FAKE, _Extent(1, 8, 8), 2, FAKE2,
+                                          None) == EUNSUP
+
+
+def test_infer_batch_argument_checks(lib):
+    L = 3
+    f = (ctypes.c_int32 * 6)(1, 2, 2, 1, 2, 2)
+    ws = (_LevelWeights * L)(*[_LevelWeights(FAKE, FAKE, FAKE, FAKE, FAKE)] * L)
+    steps = (ctypes.c_int32 * L)(10, 10, 10)
+    ext = _Extent(1, 64, 64)
+    need = lib.octree_nca_workspace_bytes(model(), ext, L, f, 1)
+    images = ctypes.c_void_p(0x7f2000000000)
+    finals = ctypes.c_void_p(0x7f1000000000)
+    wsp = ctypes.c_void_p(0x7f3000000000)
+    image_bytes, state_bytes = 64 * 64 * 3 * 4, 64 * 64 * 16 * 4
+
+    def call(batch=2, finals=finals, segs=None, wsp=wsp, n=need, steps=steps, images=images):
+        return lib.octree_nca_infer_batch(model(), images, batch, ext, L, f, ws, steps, 0.5, 0,
+                                          wsp, n, finals, segs, None)
+    assert call(batch=0) == EINVAL
+    assert call(batch=-3) == EINVAL
+    assert call(images=None) == EINVAL
+    assert call(n=need - 1) == ESPACE
+    assert call(steps=(ctypes.c_int32 * L)(10, -1, 10)) == EINVAL
+    # the second image's final state overlaps the first image
+    assert call(finals=ctypes.c_void_p(images.value + image_bytes - state_bytes)) == EINVAL
+    # segmentation of image 1 inside the workspace
+    assert call(segs=ctypes.c_void_p(wsp.value + 64)) == EINVAL
+    # images inside the workspace
+    assert call(images=ctypes.c_void_p(wsp.value + 512)) == EINVAL
+    # an unsupported model is reported before anything else
+    assert lib.octree_nca_infer_batch(model(c=12), images, 2, ext, L, f, ws, steps, 0.5, 0, wsp,
+                                      need, finals, None, None) == EUNSUP
 
 
 def test_python_binding_refuses_host_tensors(lib):

@@ -71,6 +71,55 @@ def test_infer_matches_oracle(gpu, step_kernel, wl):
     assert_seg_close(to_np(seg), want_seg, want_state, wl.dtype)
 
 
+BATCH_CASES = [scaled(TINY_2D, (1, 48, 80), steps=(3, 2, 5)),
+               scaled(VIDEO_2DT, (8, 16, 32), steps=(2, 3, 2, 2, 1), image_kind="uniform")]
+
+
+@pytest.mark.parametrize("wl", BATCH_CASES, ids=lambda w: w.name)
+def test_infer_batch_matches_oracle(gpu, step_kernel, wl):
+    """Image b of a batch runs with fire-mask counter word 3 = b: each image
+    against the oracle with that batch index; image 0 bit for bit equal to a
+    single-image inference."""
+    batch = 3
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    rng = np.random.default_rng(21)
+    images = np.stack([make_image(wl)] + [rng.uniform(0, 1, make_image(wl).shape)
+                                          .astype(storage_dtype(wl)) for _ in range(batch - 1)])
+    weights = make_weights(wl)
+    dev_images = torch.from_numpy(images).to(gpu)
+    ws = torch.empty(octnca.octree_nca_workspace_bytes(model, wl.extent, wl.factors, True),
+                     dtype=torch.uint8, device=gpu)
+    finals = torch.empty((batch,) + tuple(wl.extent) + (wl.channels,), dtype=model.torch_dtype,
+                         device=gpu)
+    segs = torch.empty((batch,) + tuple(wl.extent), dtype=torch.uint8, device=gpu)
+    octnca.octree_nca_infer_batch(model, dev_images, wl.factors, upload_weights(weights),
+                                  wl.steps, wl.fire_rate, wl.seed, ws, finals, segs)
+    torch.cuda.synchronize()
+    got_states, got_segs = to_np(finals), to_np(segs)
+    for b in range(batch):
+        want_state, want_seg = oracle.infer(images[b], weights, ndim=wl.ndim, n_in=wl.n_in,
+                                            channels=wl.channels, factors=wl.factors,
+                                            steps=wl.steps, fire_rate=wl.fire_rate,
+                                            seed=wl.seed, dtype=storage_dtype(wl), batch=b)
+        np.testing.assert_array_equal(got_states[b][..., :wl.n_in], images[b])
+        assert_state_close(got_states[b], want_state, wl.dtype)
+        assert_seg_close(got_segs[b], want_seg, want_state, wl.dtype)
+    single_state, single_seg = gpu_infer(wl, images[0], weights)
+    np.testing.assert_array_equal(got_states[0], to_np(single_state))
+    np.testing.assert_array_equal(got_segs[0], to_np(single_seg))
+    # image 1's masks differ from image 0's: same image, other batch index
+    same = np.stack([images[0], images[0]])
+    finals2 = torch.empty((2,) + tuple(wl.extent) + (wl.channels,), dtype=model.torch_dtype,
+                          device=gpu)
+    octnca.octree_nca_infer_batch(model, torch.from_numpy(same).to(gpu), wl.factors,
+                                  upload_weights(weights), wl.steps, wl.fire_rate, wl.seed, ws,
+                                  finals2, None)
+    torch.cuda.synchronize()
+    f2 = to_np(finals2)
+    np.testing.assert_array_equal(f2[0], got_states[0])
+    assert not np.array_equal(f2[1], f2[0])
+
+
 def test_infer_without_final_state_buffer(gpu):
     """final_state = NULL: both ping-pong buffers live in the workspace; the
     readout must be the same."""

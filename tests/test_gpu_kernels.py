@@ -156,6 +156,24 @@ def test_readout_matches_oracle(gpu):
     np.testing.assert_array_equal(to_np(seg), oracle.readout(s))
 
 
+@pytest.mark.parametrize("dt,classes,n_in", [("f32", 2, 3), ("f32", 5, 3), ("f32", 13, 3),
+                                              ("f16", 4, 1), ("f16", 15, 1)])
+def test_readout_classes_matches_oracle(gpu, dt, classes, n_in):
+    """Bit-exact against the oracle: values drawn from a few levels (frequent
+    ties), some NaNs, both storage types."""
+    rng = np.random.default_rng(4 + classes)
+    s = rng.integers(-3, 4, size=(3, 13, 29, C)).astype(NP_DT[dt])
+    s[0, 1, :7, C - classes] = np.nan
+    s[1, 2, :5, C - 1] = np.nan
+    seg = torch.empty((3, 13, 29), dtype=torch.uint8, device=gpu)
+    octnca.octree_nca_readout_classes(octnca.Model(ndim=3, n_in=n_in, dtype=dt), dev(s),
+                                      classes, seg)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(seg), oracle.readout_classes(s, classes))
+    if classes == 2:
+        np.testing.assert_array_equal(to_np(seg), oracle.readout(s))
+
+
 # ---------------------------------------------------------------------------
 # one step / one level
 # ---------------------------------------------------------------------------

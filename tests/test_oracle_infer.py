@@ -15,7 +15,7 @@ import os
 import numpy as np
 import pytest
 
-from oracle import infer, infer_window, readout, InferLog
+from oracle import infer, infer_window, readout, readout_classes, InferLog
 from synthetic import (make_image, make_weights, scaled, TINY_2D, VOLUME_3D, VIDEO_2DT,
                        PATHOLOGY_184MP, Workload)
 
@@ -122,6 +122,34 @@ def test_readout_ties_and_order():
     s[0, 0, 2, 14:] = (3.0, 3.0)    # tie -> 0
     s[0, 0, 3, 14:] = (-1.0, -0.5)  # -> 1
     np.testing.assert_array_equal(readout(s)[0, 0], [1, 0, 0, 1])
+
+
+def test_readout_classes_is_numpy_argmax_of_the_last_k_channels():
+    """Without NaNs the K-class readout is numpy's argmax over the last K
+    channels (numpy returns the first maximum, i.e. ties go to the lower
+    class); values are drawn from a few levels so that ties are frequent."""
+    rng = np.random.default_rng(5)
+    for k in (2, 3, 5, 13):
+        s = rng.integers(-2, 3, size=(2, 7, 9, 16)).astype(np.float32)
+        np.testing.assert_array_equal(readout_classes(s, k),
+                                      np.argmax(s[..., 16 - k:], axis=-1).astype(np.uint8))
+
+
+def test_readout_classes_with_two_classes_is_readout():
+    rng = np.random.default_rng(6)
+    s = rng.integers(-1, 2, size=(1, 11, 13, 16)).astype(np.float32)
+    s[0, 0, :3, 15] = np.nan
+    s[0, 1, :3, 14] = np.nan
+    np.testing.assert_array_equal(readout_classes(s, 2), readout(s))
+
+
+def test_readout_classes_nan_and_ties_by_hand():
+    s = np.zeros((1, 1, 4, 16), np.float32)
+    s[0, 0, 0, 13:] = (1.0, np.nan, 2.0)      # NaN skipped, 2.0 wins -> 2
+    s[0, 0, 1, 13:] = (np.nan, 5.0, 7.0)      # nothing beats a leading NaN -> 0
+    s[0, 0, 2, 13:] = (3.0, 3.0, 3.0)         # three-way tie -> 0
+    s[0, 0, 3, 13:] = (-4.0, -1.0, -1.0)      # tie of the two largest -> 1
+    np.testing.assert_array_equal(readout_classes(s, 3)[0, 0], [2, 0, 0, 1])
 
 
 def test_state_magnitude_log_and_tiny_config_finite():

@@ -103,6 +103,28 @@ def test_fire_bits_of_one_block_use_distinct_bits():
         assert int(got.sum()) == sum(h < thr for h in halves)
 
 
+def test_batch_index_is_counter_word_3():
+    """Image b of a batch draws from counter (idx >> 3, t, l, b); b = 0 is the
+    single-image mask."""
+    seed, lvl, t = 4, 1, 2
+    for b in (0, 1, 7):
+        m = fire_mask(seed, lvl, t, (1, 2, 16), 0.5, batch=b).reshape(-1)
+        for idx in range(32):
+            block = numpy_block((idx >> 3, t, lvl, b), (seed, 0))
+            word = block[(idx >> 1) & 3]
+            draw = (word >> 32) if idx & 1 else (word & 0xFFFFFFFF)
+            assert m[idx] == (draw < (1 << 31))
+    np.testing.assert_array_equal(fire_mask(seed, lvl, t, (2, 9, 13), 0.5),
+                                  fire_mask(seed, lvl, t, (2, 9, 13), 0.5, batch=0))
+
+
+def test_batch_masks_are_independent():
+    base = fire_mask(0, 0, 0, (1, 64, 64), 0.5)
+    for b in (1, 2):
+        agree = (base == fire_mask(0, 0, 0, (1, 64, 64), 0.5, batch=b)).mean()
+        assert 0.45 < agree < 0.55
+
+
 def test_fire_rate_is_binomial():
     n = 1 << 18
     for p in (0.5, 0.1, 0.9):
