@@ -220,6 +220,16 @@ int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_
                            size_t workspace_bytes, void *final_states, uint8_t *segs,
                            void *stream);
 
+/* Number of steps of the first (coarsest) level under the schedule rule of
+ * the paper's ablation (supplement S10): alpha0 * max(H, W, D) of that level,
+ * rounded down (the paper does not state the rounding; its alpha0 values are
+ * 1.0, 1.5 and 2.0).  With alpha0 = 1 this is the max(H, W) / 2^L steps that
+ * Sec. 3.2 names as enough to carry information across the coarsest level.
+ *   alpha0    >= 0 and finite;  coarsest  extent of level L-1 (d = 1 for 2D).
+ * Returns the step count, or -1 for invalid arguments or a count above
+ * INT32_MAX.  Host only: enqueues nothing. */
+int32_t octree_nca_first_level_steps(float alpha0, octnca_extent coarsest);
+
 /* Export the fire mask of one step of one level (test hook for the
  * generator described above): mask[idx] = 1 if cell idx fires, else 0.
  *   mask [extent] uint8, written.

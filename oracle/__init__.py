@@ -14,5 +14,5 @@ parts (brute-force per-cell loops, library routines, invariants).
 from .philox import philox4x64, mulhilo64
 from .octree_nca import (pool, build_pyramid, init_state, upsample_inject, fire_threshold,
                          fire_bits, fire_mask, tap_offsets, perceive, update, nca_step,
-                         run_level, readout, readout_classes, infer, infer_window, linear_index,
-                         to_storage, InferLog)
+                         run_level, readout, readout_classes, first_level_steps, infer,
+                         infer_window, linear_index, to_storage, InferLog)

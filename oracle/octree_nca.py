@@ -235,6 +235,13 @@ def run_level(state: np.ndarray, weights, n_in: int, ndim: int, level: int, step
 # readout and whole inference
 # --------------------------------------------------------------------------
 
+def first_level_steps(alpha0: float, coarsest: Sequence[int]) -> int:
+    """Steps of the first (coarsest) level, alpha0 * max(H, W, D) of that
+    level's extent (supplement S10 ablation; rounded down, a reading: the
+    paper does not state the rounding)."""
+    return int(np.floor(np.float64(np.float32(alpha0)) * max(int(v) for v in coarsest)))
+
+
 def readout(state: np.ndarray) -> np.ndarray:
     """Two-class segmentation: 1 where the last channel is strictly greater than
     the one before it, else 0 (ties, and any NaN, give 0)."""

@@ -22,8 +22,8 @@ __all__ = [
     "OctreeNCAError", "Model", "lib", "library_path", "level_weights_struct",
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
-    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_fire_mask", "octree_nca_strerror",
-    "octree_nca_abi_version", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL", "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
+    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL", "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
     "OCTNCA_EHIP", "OCTNCA_ESPACE", "OCTNCA_F32", "OCTNCA_F16",
 ]
 
@@ -34,8 +34,8 @@ OCTNCA_F32, OCTNCA_F16 = 0, 1
 EXPORTED_SYMBOLS = (
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
-    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_fire_mask", "octree_nca_strerror",
-    "octree_nca_abi_version",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
+    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
 )
 
 
@@ -84,6 +84,7 @@ _SIGS = {
                                       ctypes.c_size_t, _P, _P, _P]),
     "octree_nca_fire_mask": (_I32, [ctypes.c_uint64, _I32, _I32, _Extent, ctypes.c_float, _P,
                                     _P]),
+    "octree_nca_first_level_steps": (_I32, [ctypes.c_float, _Extent]),
     "octree_nca_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "octree_nca_abi_version": (ctypes.c_int, []),
 }
@@ -298,6 +299,14 @@ def octree_nca_infer_batch(model: Model, images, factors, weights, steps, fire_r
                                       _ptr(final_states, model.torch_dtype, "final_states"),
                                       _ptr(segs, torch.uint8, "segs"), _stream(stream))
     _check(st, "octree_nca_infer_batch")
+
+
+def octree_nca_first_level_steps(alpha0: float, coarsest) -> int:
+    """Steps of the coarsest level under the alpha0 * max(H, W, D) rule."""
+    n = lib().octree_nca_first_level_steps(float(alpha0), _extent(coarsest))
+    if n < 0:
+        raise OctreeNCAError("octree_nca_first_level_steps: invalid arguments", OCTNCA_EINVAL)
+    return int(n)
 
 
 def octree_nca_fire_mask(seed: int, level: int, step: int, extent, fire_rate: float, mask,

@@ -7,6 +7,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <cmath>
+#include <algorithm>
 #include "launch.h"
 #include "octree_nca.h"
 
@@ -245,6 +247,15 @@ int octree_nca_readout_classes(const octnca_model *model, const void *state, oct
     return hip_status(launch_readout_classes(dtype_of(model), state,
                                              extent.d * extent.h * extent.w, classes, seg,
                                              (hipStream_t)stream));
+}
+
+int32_t octree_nca_first_level_steps(float alpha0, octnca_extent coarsest) {
+    if (!(alpha0 >= 0.f) || !std::isfinite(alpha0)) return -1;
+    if (coarsest.d <= 0 || coarsest.h <= 0 || coarsest.w <= 0) return -1;
+    const int64_t m = std::max(coarsest.d, std::max(coarsest.h, coarsest.w));
+    const double steps = std::floor((double)alpha0 * (double)m);
+    if (steps > (double)INT32_MAX) return -1;
+    return (int32_t)steps;
 }
 
 int octree_nca_fire_mask(uint64_t seed, int32_t level, int32_t step, octnca_extent extent,

@@ -22,8 +22,8 @@ FAKE2 = ctypes.c_void_p(0x7f0000900000)
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^(?:int|size_t|const char \*)\s*(octree_nca_\w+)\s*\(",
-                                 text, flags=re.M)))
+    return sorted(set(re.findall(
+        r"^(?:int|int32_t|size_t|const char \*)\s*(octree_nca_\w+)\s*\(", text, flags=re.M)))
 
 
 @pytest.fixture(scope="module")
@@ -210,6 +210,18 @@ def test_infer_batch_argument_checks(lib):
     # an unsupported model is reported before anything else
     assert lib.octree_nca_infer_batch(model(c=12), images, 2, ext, L, f, ws, steps, 0.5, 0, wsp,
                                       need, finals, None, None) == EUNSUP
+
+
+def test_first_level_steps_matches_oracle(lib):
+    import oracle
+    for alpha in (0.0, 0.5, 1.0, 1.5, 2.0, 0.3, 3.7):
+        for ext in ((1, 352, 512), (24, 80, 80), (450, 15, 27), (1, 1, 1), (7, 3, 5)):
+            assert lib.octree_nca_first_level_steps(alpha, _Extent(*ext)) == \
+                oracle.first_level_steps(alpha, ext), (alpha, ext)
+    assert octnca.octree_nca_first_level_steps(1.0, (1, 352, 512)) == 512
+    for alpha, ext in ((-1.0, (1, 4, 4)), (math.nan, (1, 4, 4)), (math.inf, (1, 4, 4)),
+                       (1.0, (1, 0, 4)), (1.0, (-1, 4, 4)), (3e9, (1, 4, 4))):
+        assert lib.octree_nca_first_level_steps(alpha, _Extent(*ext)) == -1
 
 
 def test_python_binding_refuses_host_tensors(lib):

@@ -7,7 +7,11 @@
 * whole inference equals a brute-force cell-by-cell pipeline on tiny grids
   (2D, 3D, anisotropic pooling, fp16 storage);
 * the light-cone window evaluation equals the full-grid result cropped;
-* readout is the two-class argmax with ties to the lower channel.
+* readout is the two-class argmax with ties to the lower channel; the K-class
+  readout is numpy's argmax over the last K channels (and the two-class
+  readout for K = 2);
+* the first-level step rule alpha0 * max(H, W, D) gives, on the paper's level
+  table, the max(H, W) / 2^L steps named in Sec. 3.2.
 """
 import json
 import os
@@ -15,7 +19,8 @@ import os
 import numpy as np
 import pytest
 
-from oracle import infer, infer_window, readout, readout_classes, InferLog
+from oracle import (infer, infer_window, readout, readout_classes, first_level_steps,
+                    InferLog)
 from synthetic import (make_image, make_weights, scaled, TINY_2D, VOLUME_3D, VIDEO_2DT,
                        PATHOLOGY_184MP, Workload)
 
@@ -150,6 +155,32 @@ def test_readout_classes_nan_and_ties_by_hand():
     s[0, 0, 2, 13:] = (3.0, 3.0, 3.0)         # three-way tie -> 0
     s[0, 0, 3, 13:] = (-4.0, -1.0, -1.0)      # tie of the two largest -> 1
     np.testing.assert_array_equal(readout_classes(s, 3)[0, 0], [2, 0, 0, 1])
+
+
+def test_first_level_steps_match_the_papers_bound():
+    """With alpha0 = 1 the first level takes max(H, W, D) of its extent, which
+    for the paper's pyramids (supplement S7 table, tests/golden) is the finest
+    extent's largest side divided by 2 per halving: the max(H, W) / 2^L steps
+    of Sec. 3.2 (L counting the halvings)."""
+    tasks = json.load(open(os.path.join(GOLDEN, "paper_level_extents.json")))["tasks"]
+    for name, t in tasks.items():
+        ext = t["extents"]
+        halvings = len(ext) - 1
+        assert first_level_steps(1.0, ext[-1]) == max(ext[0]) // 2 ** halvings, name
+    assert first_level_steps(1.0, tasks["surgery"]["extents"][-1]) == 27
+
+
+@pytest.mark.parametrize("alpha0,want", [(1.0, 80), (1.5, 120), (2.0, 160)])
+def test_first_level_steps_ablation_values(alpha0, want):
+    """The ablation's alpha0 values on the prostate volume's coarsest level
+    (80 x 80 x 24 after two in-plane halvings of 320 x 320 x 24)."""
+    assert first_level_steps(alpha0, (24, 80, 80)) == want
+
+
+def test_first_level_steps_rounds_down_and_uses_all_axes():
+    assert first_level_steps(1.5, (1, 15, 27)) == 40          # 40.5 -> 40
+    assert first_level_steps(1.0, (450, 15, 27)) == 450       # time axis counts
+    assert first_level_steps(0.0, (3, 4, 5)) == 0
 
 
 def test_state_magnitude_log_and_tiny_config_finite():
