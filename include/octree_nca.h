@@ -76,8 +76,11 @@ typedef enum {
 typedef enum { OCTNCA_F32 = 0, OCTNCA_F16 = 1 } octnca_dtype;
 
 /* Architecture of one NCA (all levels share it; supplement S3 fixes C and H
- * at compile time).  Supported: ndim in {2, 3}, channels = 16, hidden = 64,
- * n_in in {1, 3}, state_dtype in {OCTNCA_F32, OCTNCA_F16}. */
+ * at compile time).  Supported: ndim in {2, 3}, (channels, hidden) in
+ * {(16, 64), (12, 48), (20, 100)} (the paper's model and the two other sizes
+ * of its ablation, supplement S10), n_in in {1, 3}, state_dtype in
+ * {OCTNCA_F32, OCTNCA_F16}.  The matrix-core step kernels serve C = 16,
+ * H = 64; the other sizes run on the one-thread-per-cell vector kernel. */
 typedef struct {
     int32_t ndim;        /* 2: 3x3 taps, d must be 1; 3: 3x3x3 taps */
     int32_t channels;    /* C: state channels per cell */

@@ -26,7 +26,13 @@ size_t align_up(size_t n) { return (n + kAlign - 1) / kAlign * kAlign; }
 int check_model(const octnca_model *m) {
     if (m == nullptr) return OCTNCA_EINVAL;
     if (m->ndim != 2 && m->ndim != 3) return OCTNCA_EUNSUPPORTED;
-    if (m->channels != kC || m->hidden != kH) return OCTNCA_EUNSUPPORTED;
+    // C / H: the paper's 16 / 64 and the 12 / 48 and 20 / 100 of its ablation
+    // (supplement S10); the matrix-core kernels serve 16 / 64, the vector
+    // kernel all three
+    const bool size_ok = (m->channels == 16 && m->hidden == 64) ||
+                         (m->channels == 12 && m->hidden == 48) ||
+                         (m->channels == 20 && m->hidden == 100);
+    if (!size_ok) return OCTNCA_EUNSUPPORTED;
     if (m->n_in != 1 && m->n_in != 3) return OCTNCA_EUNSUPPORTED;
     if (m->state_dtype != OCTNCA_F32 && m->state_dtype != OCTNCA_F16) return OCTNCA_EUNSUPPORTED;
     return OCTNCA_OK;
@@ -108,6 +114,8 @@ int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
     a.level = (uint32_t)level;
     a.seed = seed;
     a.threshold = threshold;
+    a.channels = m->channels;
+    a.hidden = m->hidden;
     void *bufs[2] = {b0, b1};
     for (int32_t t = 0; t < steps; ++t) {
         a.step = (uint32_t)t;
@@ -136,7 +144,7 @@ int make_plan(const octnca_model *m, octnca_extent finest, int32_t levels, const
         p->image_off[l] = off;
         off += align_up((size_t)(p->ext[l].d * p->ext[l].h * p->ext[l].w) * m->n_in * eb);
     }
-    const size_t state_bytes = align_up((size_t)(finest.d * finest.h * finest.w) * kC * eb);
+    const size_t state_bytes = align_up((size_t)(finest.d * finest.h * finest.w) * m->channels * eb);
     p->state_off[0] = off;
     off += state_bytes;
     p->state_off[1] = off;
@@ -197,15 +205,15 @@ int octree_nca_upsample(const octnca_model *model, const void *coarse_state, oct
     const octnca_extent fine{coarse.d * factor[0], coarse.h * factor[1], coarse.w * factor[2]};
     if ((st = check_extent(model, fine))) return st;
     const size_t eb = elem_bytes(model);
-    const size_t fine_bytes = (size_t)(fine.d * fine.h * fine.w) * kC * eb;
+    const size_t fine_bytes = (size_t)(fine.d * fine.h * fine.w) * model->channels * eb;
     if (overlap(fine_state, fine_bytes, coarse_state,
-                (size_t)(coarse.d * coarse.h * coarse.w) * kC * eb) ||
+                (size_t)(coarse.d * coarse.h * coarse.w) * model->channels * eb) ||
         overlap(fine_state, fine_bytes, fine_image,
                 (size_t)(fine.d * fine.h * fine.w) * model->n_in * eb))
         return OCTNCA_EINVAL;
     return hip_status(launch_upsample(dtype_of(model), coarse_state, ext3(fine), factor[0],
                                       factor[1], factor[2], fine_image, fine_state, model->n_in,
-                                      (hipStream_t)stream));
+                                      model->channels, (hipStream_t)stream));
 }
 
 int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octnca_extent extent,
@@ -218,7 +226,8 @@ int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octn
     if (buf0 == nullptr || buf1 == nullptr || !weights_ok(weights) || level < 0 || steps < 0 ||
         !fire_threshold(fire_rate, &threshold))
         return OCTNCA_EINVAL;
-    const size_t bytes = (size_t)(extent.d * extent.h * extent.w) * kC * elem_bytes(model);
+    const size_t bytes =
+        (size_t)(extent.d * extent.h * extent.w) * model->channels * elem_bytes(model);
     if (overlap(buf0, bytes, buf1, bytes)) return OCTNCA_EINVAL;
     st = run_steps(model, buf0, buf1, extent, weights, level, steps, seed, threshold,
                    (hipStream_t)stream);
@@ -233,8 +242,8 @@ int octree_nca_readout(const octnca_model *model, const void *state, octnca_exte
     if (st) return st;
     if ((st = check_extent(model, extent))) return st;
     if (state == nullptr || seg == nullptr) return OCTNCA_EINVAL;
-    return hip_status(launch_readout(dtype_of(model), state, extent.d * extent.h * extent.w, seg,
-                                     (hipStream_t)stream));
+    return hip_status(launch_readout(dtype_of(model), state, extent.d * extent.h * extent.w,
+                                     model->channels, seg, (hipStream_t)stream));
 }
 
 int octree_nca_readout_classes(const octnca_model *model, const void *state, octnca_extent extent,
@@ -242,11 +251,11 @@ int octree_nca_readout_classes(const octnca_model *model, const void *state, oct
     int st = check_model(model);
     if (st) return st;
     if ((st = check_extent(model, extent))) return st;
-    if (state == nullptr || seg == nullptr || classes < 2 || classes > kC - model->n_in)
+    if (state == nullptr || seg == nullptr || classes < 2 || classes > model->channels - model->n_in)
         return OCTNCA_EINVAL;
     return hip_status(launch_readout_classes(dtype_of(model), state,
-                                             extent.d * extent.h * extent.w, classes, seg,
-                                             (hipStream_t)stream));
+                                             extent.d * extent.h * extent.w, model->channels,
+                                             classes, seg, (hipStream_t)stream));
 }
 
 int32_t octree_nca_first_level_steps(float alpha0, octnca_extent coarsest) {
@@ -302,7 +311,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     }
     if (workspace_bytes < p.bytes) return OCTNCA_ESPACE;
     const size_t eb = elem_bytes(model);
-    const size_t state_bytes = (size_t)(finest.d * finest.h * finest.w) * kC * eb;
+    const size_t state_bytes = (size_t)(finest.d * finest.h * finest.w) * model->channels * eb;
     char *ws = (char *)workspace;
     if (final_state != nullptr &&
         (overlap(final_state, state_bytes, workspace, p.bytes) ||
@@ -333,13 +342,13 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     }
     int cur = (int)(((int64_t)(levels - 1) + total_steps) & 1);
     if (launch_upsample(dt, nullptr, ext3(p.ext[levels - 1]), 1, 1, 1, img[levels - 1], bufs[cur],
-                        model->n_in, s) != hipSuccess)
+                        model->n_in, model->channels, s) != hipSuccess)
         return OCTNCA_EHIP;
     for (int l = levels - 1; l >= 0; --l) {
         if (l < levels - 1) {
             const int32_t *f = factors + 3 * l;
             if (launch_upsample(dt, bufs[cur], ext3(p.ext[l]), f[0], f[1], f[2], img[l],
-                                bufs[cur ^ 1], model->n_in, s) != hipSuccess)
+                                bufs[cur ^ 1], model->n_in, model->channels, s) != hipSuccess)
                 return OCTNCA_EHIP;
             cur ^= 1;
         }
@@ -356,7 +365,8 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     }
     // cur == 0 here by construction of the seed buffer
     if (seg != nullptr &&
-        launch_readout(dt, bufs[cur], finest.d * finest.h * finest.w, seg, s) != hipSuccess)
+        launch_readout(dt, bufs[cur], finest.d * finest.h * finest.w, model->channels, seg, s) !=
+            hipSuccess)
         return OCTNCA_EHIP;
     return OCTNCA_OK;
 }
@@ -387,7 +397,8 @@ int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_
     if ((st = check_extent(model, finest))) return st;
     const size_t cells = (size_t)(finest.d * finest.h * finest.w);
     const size_t eb = elem_bytes(model);
-    const size_t image_bytes = cells * model->n_in * eb, state_bytes = cells * kC * eb;
+    const size_t image_bytes = cells * model->n_in * eb;
+    const size_t state_bytes = cells * model->channels * eb;
     // the batch's outputs must not overlap its inputs or the workspace
     if (final_states != nullptr &&
         (overlap(final_states, state_bytes * batch, images, image_bytes * batch) ||
@@ -436,6 +447,9 @@ namespace octnca {
 //                   forced to row streaming or to 16 x 32 tiles;
 //   "valu"          one thread per cell, fp32 FMAs on the vector ALUs.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+    // the matrix-core kernels are built for C = 16, H = 64; the other model
+    // sizes always run on the vector kernel
+    if (a.channels != kC || a.hidden != kH) return launch_step_valu(a, src, dst, stream);
     const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
     const Layout2d automatic = Layout2d::Auto;
     if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0)

@@ -64,27 +64,27 @@ __global__ __launch_bounds__(kBlock) void pool_kernel(const T *__restrict__ src,
 // per 16-byte chunk of a fine cell of a row (consecutive threads write
 // consecutive chunks).
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, typename Chunk>
 __global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ coarse, int fd,
                                                           int fh, int fw, int fz, int fy, int fx,
                                                           const T *__restrict__ img,
-                                                          T *__restrict__ fine, int n_in) {
-    constexpr int K = Storage<T>::kPerChunk;
-    constexpr int NQ = kC / K;
-    constexpr int kLgNQ = NQ == 4 ? 2 : 1;
+                                                          T *__restrict__ fine, int n_in,
+                                                          int channels) {
+    constexpr int K = (int)(sizeof(Chunk) / sizeof(T));   // channels per chunk
+    const int nq = channels / K;                           // chunks per cell
     const uint32_t i = blockIdx.x * (uint32_t)kBlock + threadIdx.x;   // chunk in the row
-    if ((uint64_t)i >= (uint64_t)fw * NQ) return;
-    const int q = (int)(i & (NQ - 1));
-    const uint32_t x = i >> kLgNQ;
+    if ((uint64_t)i >= (uint64_t)fw * nq) return;
+    const uint32_t x = i / (uint32_t)nq;
+    const int q = (int)(i - x * (uint32_t)nq);
     const int64_t ch = fh / fy, cw = fw / fx;
     const uint32_t px = x / (uint32_t)fx;
     for (int z = blockIdx.z; z < fd; z += gridDim.z) {
         for (int y = blockIdx.y; y < fh; y += gridDim.y) {
             const int64_t cell = ((int64_t)z * fh + y) * fw + x;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
+            Chunk v = {};
             if (coarse != nullptr) {
                 const int64_t parent = ((int64_t)(z / fz) * ch + y / fy) * cw + px;
-                v = reinterpret_cast<const uint4 *>(coarse + parent * kC)[q];
+                v = reinterpret_cast<const Chunk *>(coarse + parent * channels)[q];
             }
             if (q * K < n_in) {
                 // this chunk holds input channels: overwrite them with the level's image
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ 
                 for (int k = 0; k < K && q * K + k < n_in; ++k) vals[k] = img[cell * n_in + q * K + k];
                 __builtin_memcpy(&v, vals, sizeof(v));
             }
-            reinterpret_cast<uint4 *>(fine + cell * kC)[q] = v;
+            reinterpret_cast<Chunk *>(fine + cell * channels)[q] = v;
         }
     }
 }
@@ -106,11 +106,12 @@ __global__ __launch_bounds__(kBlock) void upsample_kernel(const T *__restrict__ 
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kBlock) void readout_classes_kernel(const T *__restrict__ state,
-                                                                 int64_t cells, int classes,
+                                                                 int64_t cells, int channels,
+                                                                 int classes,
                                                                  uint8_t *__restrict__ seg) {
     const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (p >= cells) return;
-    const T *s = state + p * kC + (kC - classes);
+    const T *s = state + p * channels + (channels - classes);
     float best = Storage<T>::to_float(s[0]);
     int best_k = 0;
     for (int k = 1; k < classes; ++k) {
@@ -128,12 +129,12 @@ __global__ __launch_bounds__(kBlock) void readout_classes_kernel(const T *__rest
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(kBlock) void readout_kernel(const T *__restrict__ state,
-                                                         int64_t cells,
+                                                         int64_t cells, int channels,
                                                          uint8_t *__restrict__ seg) {
     const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     if (p >= cells) return;
-    const float a = Storage<T>::to_float(state[p * kC + kC - 2]);
-    const float b = Storage<T>::to_float(state[p * kC + kC - 1]);
+    const float a = Storage<T>::to_float(state[p * channels + channels - 2]);
+    const float b = Storage<T>::to_float(state[p * channels + channels - 1]);
     seg[p] = (b > a) ? 1 : 0;
 }
 
@@ -164,42 +165,46 @@ hipError_t launch_pool(Dtype dt, const void *src, Extent3 e, void *dst, int fz, 
 }
 
 hipError_t launch_upsample(Dtype dt, const void *coarse, Extent3 e, int fz, int fy, int fx,
-                           const void *img, void *fine, int n_in, hipStream_t stream) {
-    const int nq = dt == Dtype::F32 ? kC / 4 : kC / 8;
+                           const void *img, void *fine, int n_in, int channels,
+                           hipStream_t stream) {
     if (e.cells() == 0) return hipSuccess;
+    const int esize = dt == Dtype::F32 ? 4 : 2;
+    const bool wide = (channels * esize) % 16 == 0;         // 16-byte chunks, else 8-byte
+    const int nq = channels * esize / (wide ? 16 : 8);
     const dim3 grid = row_grid(e.w * nq, e.h, e.d);
-    if (dt == Dtype::F32)
-        upsample_kernel<float><<<grid, kBlock, 0, stream>>>(
-            (const float *)coarse, (int)e.d, (int)e.h, (int)e.w, fz, fy, fx, (const float *)img,
-            (float *)fine, n_in);
-    else
-        upsample_kernel<__half><<<grid, kBlock, 0, stream>>>(
-            (const __half *)coarse, (int)e.d, (int)e.h, (int)e.w, fz, fy, fx,
-            (const __half *)img, (__half *)fine, n_in);
-    return hipGetLastError();
+    auto go = [&](auto tag, auto chunk) -> hipError_t {
+        using T = decltype(tag);
+        using Chunk = decltype(chunk);
+        upsample_kernel<T, Chunk><<<grid, kBlock, 0, stream>>>(
+            (const T *)coarse, (int)e.d, (int)e.h, (int)e.w, fz, fy, fx, (const T *)img,
+            (T *)fine, n_in, channels);
+        return hipGetLastError();
+    };
+    if (dt == Dtype::F32) return wide ? go(float{}, uint4{}) : go(float{}, uint2{});
+    return wide ? go(__half{}, uint4{}) : go(__half{}, uint2{});
 }
 
-hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, uint8_t *seg,
+hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, int channels, uint8_t *seg,
                           hipStream_t stream) {
     if (cells == 0) return hipSuccess;
     if (dt == Dtype::F32)
         readout_kernel<float><<<grid_for(cells), kBlock, 0, stream>>>((const float *)state,
-                                                                      cells, seg);
+                                                                      cells, channels, seg);
     else
         readout_kernel<__half><<<grid_for(cells), kBlock, 0, stream>>>((const __half *)state,
-                                                                       cells, seg);
+                                                                       cells, channels, seg);
     return hipGetLastError();
 }
 
-hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int classes,
-                                  uint8_t *seg, hipStream_t stream) {
+hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int channels,
+                                  int classes, uint8_t *seg, hipStream_t stream) {
     if (cells == 0) return hipSuccess;
     if (dt == Dtype::F32)
         readout_classes_kernel<float><<<grid_for(cells), kBlock, 0, stream>>>(
-            (const float *)state, cells, classes, seg);
+            (const float *)state, cells, channels, classes, seg);
     else
         readout_classes_kernel<__half><<<grid_for(cells), kBlock, 0, stream>>>(
-            (const __half *)state, cells, classes, seg);
+            (const __half *)state, cells, channels, classes, seg);
     return hipGetLastError();
 }
 

@@ -23,12 +23,12 @@ hipError_t launch_pool(Dtype dt, const void *src, Extent3 dst_ext, void *dst, in
 // Upsample + inject.  coarse == nullptr seeds the hidden channels with zeros
 // (coarsest level initialisation, factors then must be 1).
 hipError_t launch_upsample(Dtype dt, const void *coarse, Extent3 fine_ext, int fz, int fy, int fx,
-                           const void *fine_image, void *fine_state, int n_in, hipStream_t stream);
-
-hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, uint8_t *seg,
+                           const void *img, void *fine, int n_in, int channels,
+                           hipStream_t stream);
+hipError_t launch_readout(Dtype dt, const void *state, int64_t cells, int channels, uint8_t *seg,
                           hipStream_t stream);
-hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int classes,
-                                  uint8_t *seg, hipStream_t stream);
+hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, int channels,
+                                  int classes, uint8_t *seg, hipStream_t stream);
 
 hipError_t launch_fire_mask(uint64_t seed, uint32_t level, uint32_t step, int64_t cells,
                             uint64_t threshold, uint8_t *mask, hipStream_t stream);
@@ -43,6 +43,8 @@ struct StepArgs {
     uint32_t level;
     uint32_t step;
     uint32_t batch = 0;   // image index in a batch (fire-mask counter word 3)
+    int channels = kC;    // C and H of the model (the matrix-core kernels need 16 / 64)
+    int hidden = kH;
     uint64_t seed;
     uint64_t threshold;
 };

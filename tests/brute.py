@@ -42,7 +42,9 @@ def brute_upsample(coarse, f, fine_img):
 
 
 def brute_step(state, w, n_in, ndim, level, t, seed, fire_rate, dtype=np.float32):
-    """One step, cell by cell, with Python floats (float64)."""
+    """One step, cell by cell, with Python floats (float64).  C and H are read
+    from the weights' shapes."""
+    C, H = w.conv_w.shape[0], w.w1.shape[0]
     d, h, wd, _ = state.shape
     mask = fire_mask(seed, level, t, (d, h, wd), fire_rate)
     out = np.array(state, dtype=np.float64)

@@ -141,6 +141,23 @@ def test_workspace_bytes_layout(lib):
     assert lib.octree_nca_workspace_bytes(model(), _Extent(1, 63, 64), 3, f, 1) == 0
 
 
+def test_other_model_sizes_are_accepted(lib):
+    """C/H = 12/48 and 20/100 (the paper's ablation sizes) are supported: the
+    state buffers of the workspace scale with C; other pairs are refused."""
+    f = (ctypes.c_int32 * 3)(1, 2, 2)
+    ext = _Extent(1, 64, 64)
+    al = lambda n: (n + 255) // 256 * 256
+    img = al(32 * 32 * 3 * 4)
+    for c, h in ((12, 48), (16, 64), (20, 100)):
+        assert lib.octree_nca_workspace_bytes(model(c=c, h=h), ext, 2, f, 0) == \
+            img + 2 * al(64 * 64 * c * 4)
+    for c, h in ((12, 64), (20, 64), (16, 48), (8, 32)):
+        assert lib.octree_nca_workspace_bytes(model(c=c, h=h), ext, 2, f, 0) == 0
+    # the K-class readout range follows C
+    assert lib.octree_nca_readout_classes(model(c=12, h=48), FAKE, _Extent(1, 8, 8), 10, FAKE2,
+                                          None) == EINVAL
+
+
 def test_infer_rejects_small_workspace_and_bad_steps(lib):
     L = 3
     f = (ctypes.c_int32 * 6)(1, 2, 2, 1, 2, 2)

@@ -27,7 +27,8 @@ pytestmark = pytest.mark.gpu
 
 
 def gpu_infer(wl, image, weights, want_state=True):
-    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, channels=wl.channels,
+                         hidden=wl.hidden)
     run = Inference(model, wl.extent, wl.factors, want_state=want_state)
     state, seg = run(to_device_image(image, model), upload_weights(weights), wl.steps,
                      wl.fire_rate, wl.seed)
@@ -55,6 +56,12 @@ SMALL = [
     Workload(name="odd_steps_f16_2d", ndim=2, extent=(1, 48, 36), n_in=1,
              factors=((1, 2, 2), (1, 3, 3)), steps=(3, 1, 5), dtype="f16",
              image_kind="uniform"),
+    # the ablation's model sizes (supplement S10), on the vector kernel
+    Workload(name="c12h48_2d", ndim=2, extent=(1, 64, 96), n_in=3, factors=((1, 2, 2),) * 2,
+             steps=(4, 3, 5), image_kind="uniform", channels=12, hidden=48),
+    Workload(name="c20h100_3d_f16", ndim=3, extent=(8, 16, 24), n_in=3,
+             factors=((1, 2, 2), (2, 2, 2)), steps=(3, 2, 4), dtype="f16",
+             image_kind="uniform", channels=20, hidden=100),
 ]
 
 

@@ -20,14 +20,14 @@ NP_DT = {"f32": np.float32, "f16": np.float16}
 T_DT = {"f32": torch.float32, "f16": torch.float16}
 
 
-def rand_weights(rng, ndim, scale=0.1):
+def rand_weights(rng, ndim, scale=0.1, c=C, h=H):
     taps = 3 ** ndim
     return LevelWeights(
-        conv_w=rng.normal(0, scale, (C, taps)).astype(np.float32),
-        conv_b=rng.normal(0, scale, (C,)).astype(np.float32),
-        w1=rng.normal(0, scale, (H, 2 * C)).astype(np.float32),
-        b1=rng.normal(0, scale, (H,)).astype(np.float32),
-        w2=rng.normal(0, scale, (C, H)).astype(np.float32))
+        conv_w=rng.normal(0, scale, (c, taps)).astype(np.float32),
+        conv_b=rng.normal(0, scale, (c,)).astype(np.float32),
+        w1=rng.normal(0, scale, (h, 2 * c)).astype(np.float32),
+        b1=rng.normal(0, scale, (h,)).astype(np.float32),
+        w2=rng.normal(0, scale, (c, h)).astype(np.float32))
 
 
 def dev(a, dtype=None):
@@ -250,6 +250,29 @@ def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     want = oracle.run_level(s, w, n_in, ndim, 1, steps, 3, 0.5, NP_DT[dt])
     tol = STEP_TOL[(dt, step_kernel)][1]
     assert max_rel_err(got, want) <= tol
+
+
+@pytest.mark.parametrize("dt,ndim,n_in,c,h,shape", [
+    ("f32", 2, 3, 12, 48, (1, 37, 45)), ("f32", 3, 1, 20, 100, (5, 9, 17)),
+    ("f16", 2, 1, 20, 100, (1, 21, 30)), ("f16", 3, 3, 12, 48, (6, 11, 10)),
+    ("f32", 3, 3, 12, 48, (4, 10, 12)), ("f16", 2, 3, 12, 48, (1, 16, 40))])
+def test_other_model_sizes_match_oracle(gpu, dt, ndim, n_in, c, h, shape):
+    """The ablation's model sizes C/H = 12/48 and 20/100 (supplement S10) run on
+    the vector kernel: one step and nine steps against the oracle, input
+    channels unchanged, non-firing cells copied bit for bit."""
+    rng = np.random.default_rng(13)
+    w = rand_weights(rng, ndim, c=c, h=h)
+    s = rng.normal(0, 1, shape + (c,)).astype(NP_DT[dt])
+    model = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, channels=c, hidden=h)
+    got, which = run_level_gpu(model, s, w, 2, 1, 0.5, 42)
+    want = oracle.nca_step(s, w, n_in, ndim, 2, 0, 42, 0.5, NP_DT[dt])
+    assert max_rel_err(got, want) <= STEP_TOL[(dt, "valu")][0]
+    np.testing.assert_array_equal(got[..., :n_in], s[..., :n_in])
+    mask = oracle.fire_mask(42, 2, 0, shape, 0.5)
+    np.testing.assert_array_equal(got[~mask], s[~mask])
+    got9, _ = run_level_gpu(model, s, w, 1, 9, 0.5, 3)
+    want9 = oracle.run_level(s, w, n_in, ndim, 1, 9, 3, 0.5, NP_DT[dt])
+    assert max_rel_err(got9, want9) <= STEP_TOL[(dt, "valu")][1]
 
 
 def test_zero_steps_leave_state(gpu):

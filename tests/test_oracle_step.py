@@ -85,6 +85,22 @@ def test_step_matches_brute_force(ndim, shape, n_in):
     np.testing.assert_allclose(got, want, rtol=2e-7, atol=1e-7)
 
 
+@pytest.mark.parametrize("c,h,ndim,n_in", [(12, 48, 2, 3), (20, 100, 3, 1), (12, 48, 3, 3)])
+def test_step_matches_brute_force_other_model_sizes(c, h, ndim, n_in):
+    """The ablation's model sizes C/H = 12/48 and 20/100 (supplement S10)."""
+    rng = np.random.default_rng(8)
+    taps = 3 ** ndim
+    w = LevelWeights(conv_w=rng.normal(0, 0.1, (c, taps)).astype(np.float32),
+                     conv_b=rng.normal(0, 0.1, (c,)).astype(np.float32),
+                     w1=rng.normal(0, 0.1, (h, 2 * c)).astype(np.float32),
+                     b1=rng.normal(0, 0.1, (h,)).astype(np.float32),
+                     w2=rng.normal(0, 0.1, (c, h)).astype(np.float32))
+    s = rng.normal(0, 1, (2, 4, 5, c) if ndim == 3 else (1, 5, 6, c)).astype(np.float32)
+    got = nca_step(s, w, n_in, ndim, level=0, step=1, seed=2, fire_rate=0.5, dtype=np.float32)
+    want = brute_step(s, w, n_in, ndim, 0, 1, 2, 0.5)
+    np.testing.assert_allclose(got, want, rtol=2e-7, atol=1e-7)
+
+
 def layerwise_step(state, w, n_in, ndim, level, t, seed, fire_rate):
     """The layer-wise PyTorch pipeline, float64 on the CPU."""
     s = torch.from_numpy(state.astype(np.float64))
