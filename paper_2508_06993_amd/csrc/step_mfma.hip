@@ -770,7 +770,7 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
 // the ring.  An iteration takes two input rows; the loads of the next two are
 // issued at its start and written to LDS at its end.
 // ---------------------------------------------------------------------------
-constexpr int k2RunRows = 64;       // output rows per work item (largest)
+constexpr int k2RunRows = 128;      // output rows per work item
 constexpr int k2WavesPerSimd = 2;   // 255 VGPRs with the split-bf16 MLP
 
 // One halo row of a strip: kBody body loads (16 cells x 4 chunks in fp32,
@@ -1467,13 +1467,13 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     if (tiles == 0) return hipSuccess;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
     // Large levels: row streaming over strips of 32 cells and runs of
-    // k2RunRows rows, once there are at least two runs per wave slot.  Small
+    // k2RunRows rows, once there is at least one run per wave slot.  Small
     // levels: 16 x 32 tiles, where the per-run start-up of the row kernel
     // (two rows loaded and waited for) would not be amortised.
     const int64_t slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
     const int64_t runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
     const int64_t items = (int64_t)tiles_x * runs;
-    const bool rows = layout == Layout2d::Rows || (layout == Layout2d::Auto && items >= 2 * slots);
+    const bool rows = layout == Layout2d::Rows || (layout == Layout2d::Auto && items >= slots);
     if (rows) {
         if (items > INT32_MAX) return hipErrorInvalidValue;
         const int grid = (int)std::min<int64_t>(items, slots);
