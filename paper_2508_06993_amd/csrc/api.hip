@@ -100,10 +100,8 @@ LevelWeightsDev to_dev(const octnca_level_weights *w) {
 
 Dtype dtype_of(const octnca_model *m) { return m->state_dtype == OCTNCA_F16 ? Dtype::F16 : Dtype::F32; }
 
-// Enqueue `steps` steps; bufs[t % 2] -> bufs[(t + 1) % 2].
-int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
-              const octnca_level_weights *w, int32_t level, int32_t steps, uint64_t seed,
-              uint64_t threshold, hipStream_t stream, uint32_t batch = 0) {
+StepArgs step_args(const octnca_model *m, const octnca_extent &e, const octnca_level_weights *w,
+                   int32_t level, uint64_t seed, uint64_t threshold, uint32_t batch) {
     StepArgs a;
     a.batch = batch;
     a.dtype = dtype_of(m);
@@ -112,14 +110,25 @@ int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
     a.ext = ext3(e);
     a.w = to_dev(w);
     a.level = (uint32_t)level;
+    a.step = 0;
     a.seed = seed;
     a.threshold = threshold;
     a.channels = m->channels;
     a.hidden = m->hidden;
+    return a;
+}
+
+// Enqueue steps t0 .. t1-1 of a level; step t reads bufs[(t - t0) % 2] and
+// writes bufs[(t - t0 + 1) % 2].
+int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
+              const octnca_level_weights *w, int32_t level, int32_t t0, int32_t t1,
+              uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0) {
+    StepArgs a = step_args(m, e, w, level, seed, threshold, batch);
     void *bufs[2] = {b0, b1};
-    for (int32_t t = 0; t < steps; ++t) {
+    for (int32_t t = t0; t < t1; ++t) {
         a.step = (uint32_t)t;
-        const hipError_t err = launch_step(a, bufs[t & 1], bufs[(t + 1) & 1], stream);
+        const int k = (t - t0) & 1;
+        const hipError_t err = launch_step(a, bufs[k], bufs[k ^ 1], stream);
         if (err != hipSuccess) return OCTNCA_EHIP;
     }
     return OCTNCA_OK;
@@ -229,7 +238,7 @@ int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octn
     const size_t bytes =
         (size_t)(extent.d * extent.h * extent.w) * model->channels * elem_bytes(model);
     if (overlap(buf0, bytes, buf1, bytes)) return OCTNCA_EINVAL;
-    st = run_steps(model, buf0, buf1, extent, weights, level, steps, seed, threshold,
+    st = run_steps(model, buf0, buf1, extent, weights, level, 0, steps, seed, threshold,
                    (hipStream_t)stream);
     if (st) return st;
     if (result_in_buf1) *result_in_buf1 = steps & 1;
@@ -334,19 +343,29 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
 
     const hipStream_t s = (hipStream_t)stream;
     const Dtype dt = dtype_of(model);
+    // Levels whose first step reads the next coarser state directly (upsample
+    // + inject fused into the step): that transition flips no buffer.
+    bool fused[kMaxLevels] = {};
+    int n_fused = 0;
+    for (int l = 0; l + 1 < levels; ++l) {
+        if (steps[l] < 1) continue;
+        const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
+        fused[l] = step_fuses_upsample(a);
+        n_fused += fused[l] ? 1 : 0;
+    }
     for (int l = 1; l < levels; ++l) {
         const int32_t *f = factors + 3 * (l - 1);
         if (launch_pool(dt, img[l - 1], ext3(p.ext[l]), (void *)img[l], f[0], f[1], f[2],
                         model->n_in, s) != hipSuccess)
             return OCTNCA_EHIP;
     }
-    int cur = (int)(((int64_t)(levels - 1) + total_steps) & 1);
+    int cur = (int)(((int64_t)(levels - 1) + total_steps - n_fused) & 1);
     if (launch_upsample(dt, nullptr, ext3(p.ext[levels - 1]), 1, 1, 1, img[levels - 1], bufs[cur],
                         model->n_in, model->channels, s) != hipSuccess)
         return OCTNCA_EHIP;
     for (int l = levels - 1; l >= 0; --l) {
-        if (l < levels - 1) {
-            const int32_t *f = factors + 3 * l;
+        const int32_t *f = factors + 3 * l;
+        if (l < levels - 1 && !fused[l]) {
             if (launch_upsample(dt, bufs[cur], ext3(p.ext[l]), f[0], f[1], f[2], img[l],
                                 bufs[cur ^ 1], model->n_in, model->channels, s) != hipSuccess)
                 return OCTNCA_EHIP;
@@ -355,10 +374,20 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
         if (level_events && level_events[2 * l] &&
             hipEventRecord((hipEvent_t)level_events[2 * l], s) != hipSuccess)
             return OCTNCA_EHIP;
-        st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, steps[l], seed,
-                       threshold, s, batch);
+        int32_t t0 = 0;
+        if (fused[l]) {
+            // step 0 from the coarse state bufs[cur] (level l + 1) and image l
+            const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
+            if (launch_step_up(a, bufs[cur], (int)p.ext[l + 1].w, f[1], f[2], img[l],
+                               bufs[cur ^ 1], s) != hipSuccess)
+                return OCTNCA_EHIP;
+            cur ^= 1;
+            t0 = 1;
+        }
+        st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, t0, steps[l],
+                       seed, threshold, s, batch);
         if (st) return st;
-        cur ^= steps[l] & 1;
+        cur ^= (steps[l] - t0) & 1;
         if (level_events && level_events[2 * l + 1] &&
             hipEventRecord((hipEvent_t)level_events[2 * l + 1], s) != hipSuccess)
             return OCTNCA_EHIP;
@@ -446,25 +475,44 @@ namespace octnca {
 //   "mfma_rows", "mfma_tiles"  the default kernel with the 2D work layout
 //                   forced to row streaming or to 16 x 32 tiles;
 //   "valu"          one thread per cell, fp32 FMAs on the vector ALUs.
+struct Selection {
+    bool ok = true, valu = false;
+    MfmaMlp mlp = MfmaMlp::Default;
+    Layout2d layout = Layout2d::Auto;
+};
+
+Selection select_step_kernel() {
+    Selection r;
+    const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
+    if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0) return r;
+    if (strcmp(sel, "valu") == 0) r.valu = true;
+    else if (strcmp(sel, "mfma_f32") == 0) r.mlp = MfmaMlp::F32;
+    else if (strcmp(sel, "mfma_bf16x3") == 0) r.mlp = MfmaMlp::Bf16x3;
+    else if (strcmp(sel, "mfma_f16") == 0) r.mlp = MfmaMlp::F16;
+    else if (strcmp(sel, "mfma_rows") == 0) r.layout = Layout2d::Rows;
+    else if (strcmp(sel, "mfma_tiles") == 0) r.layout = Layout2d::Tiles;
+    else r.ok = false;
+    return r;
+}
+
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
     // the matrix-core kernels are built for C = 16, H = 64; the other model
     // sizes always run on the vector kernel
     if (a.channels != kC || a.hidden != kH) return launch_step_valu(a, src, dst, stream);
-    const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
-    const Layout2d automatic = Layout2d::Auto;
-    if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0)
-        return launch_step_mfma(a, MfmaMlp::Default, automatic, src, dst, stream);
-    if (strcmp(sel, "valu") == 0) return launch_step_valu(a, src, dst, stream);
-    if (strcmp(sel, "mfma_f32") == 0)
-        return launch_step_mfma(a, MfmaMlp::F32, automatic, src, dst, stream);
-    if (strcmp(sel, "mfma_bf16x3") == 0)
-        return launch_step_mfma(a, MfmaMlp::Bf16x3, automatic, src, dst, stream);
-    if (strcmp(sel, "mfma_f16") == 0)
-        return launch_step_mfma(a, MfmaMlp::F16, automatic, src, dst, stream);
-    if (strcmp(sel, "mfma_rows") == 0)
-        return launch_step_mfma(a, MfmaMlp::Default, Layout2d::Rows, src, dst, stream);
-    if (strcmp(sel, "mfma_tiles") == 0)
-        return launch_step_mfma(a, MfmaMlp::Default, Layout2d::Tiles, src, dst, stream);
-    return hipErrorInvalidValue;
+    const Selection sel = select_step_kernel();
+    if (!sel.ok) return hipErrorInvalidValue;
+    if (sel.valu) return launch_step_valu(a, src, dst, stream);
+    return launch_step_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+}
+
+bool step_fuses_upsample(const StepArgs &a) {
+    const Selection sel = select_step_kernel();
+    return sel.ok && !sel.valu && step_mfma_fuses_upsample(a, sel.mlp, sel.layout);
+}
+
+hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_w, int fy, int fx,
+                          const void *img, void *dst, hipStream_t stream) {
+    const Selection sel = select_step_kernel();
+    return launch_step_mfma_up(a, sel.layout, coarse, coarse_w, fy, fx, img, dst, stream);
 }
 }  // namespace octnca

@@ -831,15 +831,89 @@ struct RowStream {
         const int slot = lane < NQ ? 0 : (lane < 2 * NQ ? kHaloW - 1 : kDummy);
         put(planes, lane % NQ, slot, v[kBody]);
     }
+
+    // Upsample + inject fused into the load (Sec. 3.2; supplement S6): fine row
+    // y comes from the coarse state's row y / fy, cell x from coarse cell x / fx,
+    // and the NIN input channels from the fine image's row y (one image element
+    // per lane, kImg loads).  commit_up writes the coarse cells like commit()
+    // and then overwrites the input channels (all in channel quad 0) with the
+    // image values, so the ring holds exactly the upsampled fine state.
+    template <int NIN>
+    struct Image {
+        static constexpr int kElems = kHaloW * NIN;
+        static constexpr int kImg = (kElems + 63) / 64;
+        uint32_t e[kImg];
+    };
+
+    template <int NIN>
+    __device__ __forceinline__ void issue_up(const T *__restrict__ coarse, int cdw, int fy,
+                                             int fx, const T *__restrict__ img, Image<NIN> &im,
+                                             int y, int dh, int dw, int x0) {
+        const int lane = threadIdx.x & 63;
+        const bool row_ok = y >= 0 && y < dh;
+        const Rsrc r = make_rsrc(coarse + (int64_t)(row_ok ? y / fy : 0) * cdw * kC,
+                                 row_ok ? (uint32_t)cdw * kCellBytes : 0u);
+        const int cell = lane % kCellsPerBody, chunk = lane / kCellsPerBody;
+#pragma unroll
+        for (int k = 0; k < kBody; ++k) {
+            const int cx = x0 + k * kCellsPerBody + cell;
+            const uint32_t off =
+                cx < dw ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)chunk * 16 : kOut;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        {
+            const int cx = lane < NQ ? x0 - 1 : x0 + kTileW;
+            const bool ok = lane < 2 * NQ && cx >= 0 && cx < dw;
+            const uint32_t off =
+                ok ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)(lane % NQ) * 16 : kOut;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+            v[kBody] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const Rsrc ri = make_rsrc(img + (int64_t)(row_ok ? y : 0) * dw * NIN,
+                                  row_ok ? (uint32_t)dw * NIN * (uint32_t)sizeof(T) : 0u);
+#pragma unroll
+        for (int j = 0; j < Image<NIN>::kImg; ++j) {
+            const int e = lane + 64 * j;
+            const int fc = x0 - 1 + e / NIN;
+            const bool ok = e < Image<NIN>::kElems && fc >= 0 && fc < dw;
+            const uint32_t off = ok ? (uint32_t)(fc * NIN + e % NIN) * (uint32_t)sizeof(T) : kOut;
+            if constexpr (sizeof(T) == 4)
+                im.e[j] = __builtin_amdgcn_raw_buffer_load_b32(ri, off, 0, 0);
+            else
+                im.e[j] = __builtin_amdgcn_raw_buffer_load_b16(ri, off, 0, 0);
+        }
+    }
+
+    template <int NIN>
+    __device__ __forceinline__ void commit_up(float4 *planes, const Image<NIN> &im) const {
+        commit(planes);
+        const int lane = threadIdx.x & 63;
+#pragma unroll
+        for (int j = 0; j < Image<NIN>::kImg; ++j) {
+            const int e = lane + 64 * j;
+            const int slot = e < Image<NIN>::kElems ? e / NIN : kDummy;
+            float val;
+            if constexpr (sizeof(T) == 4)
+                val = __uint_as_float(im.e[j]);
+            else
+                val = __half2float(__ushort_as_half((unsigned short)im.e[j]));
+            reinterpret_cast<float *>(planes + slot)[e % NIN] = val;   // quad plane 0
+        }
+    }
 };
 
-template <typename T, int NIN, class Mlp, bool ALIGNED>
+// UP: the step's input is not a state of this level but the next coarser
+// level's state (src, width up_cdw) upsampled by (up_fy, up_fx) with the input
+// channels taken from up_img (the first step of a level, fused with the
+// upsample + inject).
+template <typename T, int NIN, class Mlp, bool ALIGNED, bool UP>
 __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int runs,
     int run_rows, int items, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
-    uint64_t threshold) {
+    uint64_t threshold, const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx) {
     using RS = RowStream<T>;
     __shared__ float4 ring[4][RS::kSlotWords];   // row y in slot y & 3
     __shared__ float4 tapw[9][4];                // [tap][quad] conv weights of channels 4q..4q+3
@@ -887,6 +961,19 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     int gq = g;
     RS ra, rb;
+    typename RS::template Image<NIN> ia, ib;   // used by UP only
+    auto issue = [&](RS &rs, typename RS::template Image<NIN> &im, int y, int x0) {
+        if constexpr (UP)
+            rs.template issue_up<NIN>(src, up_cdw, up_fy, up_fx, up_img, im, y, dh, dw, x0);
+        else
+            rs.issue(src, y, dh, dw, x0);
+    };
+    auto commit = [&](const RS &rs, const typename RS::template Image<NIN> &im, float4 *slot) {
+        if constexpr (UP)
+            rs.template commit_up<NIN>(slot, im);
+        else
+            rs.commit(slot);
+    };
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         const int sx = item % strips;
@@ -907,10 +994,10 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             }
 
         // rows y_begin - 1 and y_begin into the ring
-        ra.issue(src, y_begin - 1, dh, dw, x0);
-        rb.issue(src, y_begin, dh, dw, x0);
-        ra.commit(ring[(y_begin - 1) & 3]);
-        rb.commit(ring[y_begin & 3]);
+        issue(ra, ia, y_begin - 1, x0);
+        issue(rb, ib, y_begin, x0);
+        commit(ra, ia, ring[(y_begin - 1) & 3]);
+        commit(rb, ib, ring[y_begin & 3]);
 
         // Input row q with its x taps: output q + 1 takes the dy = -1 weights,
         // q the dy = 0 ones and q - 1 the dy = +1 ones.
@@ -992,16 +1079,16 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
         // input rows q, q + 1 per iteration, from y_begin - 1 through y_end
         // (plus one padding row when the count is odd)
         for (int q = y_begin - 1; q <= y_end; q += 2) {
-            ra.issue(src, q + 2, dh, dw, x0);
-            rb.issue(src, q + 3, dh, dw, x0);
+            issue(ra, ia, q + 2, x0);
+            issue(rb, ib, q + 3, x0);
             fold_row(q);
             finish_row(q - 1);
             __builtin_amdgcn_sched_barrier(0);
             fold_row(q + 1);
             finish_row(q);
             __builtin_amdgcn_sched_barrier(0);
-            ra.commit(ring[(q + 2) & 3]);
-            rb.commit(ring[(q + 3) & 3]);
+            commit(ra, ia, ring[(q + 2) & 3]);
+            commit(rb, ib, ring[(q + 3) & 3]);
         }
     }
 }
@@ -1458,6 +1545,47 @@ int device_cus() {
 
 constexpr int kBlocksPerCu = 2;
 
+// Work layout of a 2D level.  Large levels: row streaming over strips of 32
+// cells and runs of k2RunRows rows, once there is at least one run per wave
+// slot.  Small levels: 16 x 32 tiles, where the per-run start-up of the row
+// kernel (two rows loaded and waited for) would not be amortised.
+struct RowsPlan {
+    int tiles_x;
+    int64_t runs, items, slots;
+};
+
+RowsPlan rows_plan(const StepArgs &a) {
+    RowsPlan r;
+    r.tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
+    r.slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
+    r.runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
+    r.items = (int64_t)r.tiles_x * r.runs;
+    return r;
+}
+
+bool uses_rows(const StepArgs &a, Layout2d layout) {
+    return layout == Layout2d::Rows ||
+           (layout == Layout2d::Auto && rows_plan(a).items >= rows_plan(a).slots);
+}
+
+// Row kernel launch; UP: the first step of a level fused with the upsample
+// from the coarse state src (width cdw) by (fy, fx) and the image img.
+template <typename T, int NIN, class Mlp, bool UP>
+hipError_t launch_rows(const StepArgs &a, const void *src, void *dst, const void *img, int cdw,
+                       int fy, int fx, hipStream_t stream) {
+    const RowsPlan r = rows_plan(a);
+    if (r.items == 0) return hipSuccess;
+    if (r.items > INT32_MAX) return hipErrorInvalidValue;
+    const int grid = (int)std::min<int64_t>(r.items, r.slots);
+    auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_2d_rows<T, NIN, Mlp, true, UP>
+                                 : nca_step_mfma_2d_rows<T, NIN, Mlp, false, UP>;
+    kern<<<grid, 64, 0, stream>>>(
+        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, (int)r.runs, k2RunRows,
+        (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
+        a.seed, a.threshold, (const T *)img, cdw, fy, fx);
+    return hipGetLastError();
+}
+
 template <typename T, int NIN, class Mlp>
 hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *dst,
                      hipStream_t stream) {
@@ -1466,30 +1594,12 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     const int64_t tiles = (int64_t)tiles_x * tiles_y;
     if (tiles == 0) return hipSuccess;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
-    // Large levels: row streaming over strips of 32 cells and runs of
-    // k2RunRows rows, once there is at least one run per wave slot.  Small
-    // levels: 16 x 32 tiles, where the per-run start-up of the row kernel
-    // (two rows loaded and waited for) would not be amortised.
-    const int64_t slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
-    const int64_t runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
-    const int64_t items = (int64_t)tiles_x * runs;
-    const bool rows = layout == Layout2d::Rows || (layout == Layout2d::Auto && items >= slots);
-    if (rows) {
-        if (items > INT32_MAX) return hipErrorInvalidValue;
-        const int grid = (int)std::min<int64_t>(items, slots);
-        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_2d_rows<T, NIN, Mlp, true>
-                                     : nca_step_mfma_2d_rows<T, NIN, Mlp, false>;
-        kern<<<grid, 64, 0, stream>>>(
-            (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)runs, k2RunRows,
-            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
-            a.threshold);
-    } else {
-        const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
-        nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
-            (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles,
-            a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
-            a.threshold);
-    }
+    if (uses_rows(a, layout))
+        return launch_rows<T, NIN, Mlp, false>(a, src, dst, nullptr, 0, 1, 1, stream);
+    const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
+    nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
+        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles, a.w.conv_w,
+        a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold);
     return hipGetLastError();
 }
 
@@ -1534,13 +1644,43 @@ hipError_t dispatch(const StepArgs &a, Layout2d layout, const void *src, void *d
 
 }  // namespace
 
-hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
-                            void *dst, hipStream_t stream) {
+bool mfma_fits(const StepArgs &a) {
     // Buffer descriptors address a tile's rows with 32-bit offsets: rows of
     // more than (2^32 / 18 rows) bytes go to the vector kernel instead.
     const int64_t cell_bytes = (int64_t)kC * (a.dtype == Dtype::F32 ? 4 : 2);
-    if ((int64_t)(k2TY + 2) * a.ext.w * cell_bytes >= (int64_t(1) << 32))
-        return launch_step_valu(a, src, dst, stream);
+    return (int64_t)(k2TY + 2) * a.ext.w * cell_bytes < (int64_t(1) << 32);
+}
+
+bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
+    return a.ndim == 2 && a.channels == kC && a.hidden == kH && mlp == MfmaMlp::Default &&
+           mfma_fits(a) && uses_rows(a, layout);
+}
+
+hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *coarse,
+                               int coarse_w, int fy, int fx, const void *img, void *dst,
+                               hipStream_t stream) {
+    if (!step_mfma_fuses_upsample(a, MfmaMlp::Default, layout)) return hipErrorInvalidValue;
+    if (a.dtype == Dtype::F32) {
+        if (a.n_in == 1)
+            return launch_rows<float, 1, MlpBf16x3, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                          stream);
+        if (a.n_in == 3)
+            return launch_rows<float, 3, MlpBf16x3, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                          stream);
+    } else {
+        if (a.n_in == 1)
+            return launch_rows<__half, 1, MlpF16, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                        stream);
+        if (a.n_in == 3)
+            return launch_rows<__half, 3, MlpF16, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                        stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
+                            void *dst, hipStream_t stream) {
+    if (!mfma_fits(a)) return launch_step_valu(a, src, dst, stream);
     if (mlp == MfmaMlp::Default)
         mlp = a.dtype == Dtype::F32 ? MfmaMlp::Bf16x3 : MfmaMlp::F16;
     if (a.dtype == Dtype::F32) {

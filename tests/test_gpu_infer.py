@@ -127,6 +127,53 @@ def test_infer_batch_matches_oracle(gpu, step_kernel, wl):
     assert not np.array_equal(f2[1], f2[0])
 
 
+FUSION_CASES = [scaled(TINY_2D, (1, 64, 96), steps=(3, 2, 4)),
+                Workload(name="fused_f16_nin1", ndim=2, extent=(1, 48, 72), n_in=1,
+                         factors=((1, 2, 3), (1, 3, 2)), steps=(2, 3, 1), dtype="f16",
+                         image_kind="uniform"),
+                Workload(name="fused_zero_steps", ndim=2, extent=(1, 40, 64), n_in=3,
+                         factors=((1, 2, 2), (1, 2, 2)), steps=(3, 0, 2),
+                         image_kind="uniform")]
+
+
+@pytest.mark.parametrize("wl", FUSION_CASES, ids=lambda w: w.name)
+def test_fused_first_step_equals_separate_upsample(gpu, monkeypatch, wl):
+    """With the 2D row layout, octree_nca_infer fuses each level's first step
+    with the upsample + inject.  The same pipeline built from the separate
+    entry points (pyramid, upsample, run_level: the same row kernel without
+    fusion) must give the same bits."""
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    image = make_image(wl)
+    weights = make_weights(wl)
+    fused_state, fused_seg = gpu_infer(wl, image, weights)
+
+    levels = len(wl.steps)
+    dev_img = to_device_image(image, model)
+    exts = [tuple(wl.extent)]
+    for f in wl.factors:
+        exts.append(tuple(a // b for a, b in zip(exts[-1], f)))
+    pyr = [dev_img] + [torch.empty(e + (wl.n_in,), dtype=model.torch_dtype, device=gpu)
+                       for e in exts[1:]]
+    octnca.octree_nca_build_pyramid(model, dev_img, wl.factors, pyr[1:])
+    w_dev = upload_weights(weights)
+    state = torch.zeros(exts[-1] + (wl.channels,), dtype=model.torch_dtype, device=gpu)
+    state[..., :wl.n_in] = pyr[-1]
+    for lvl in range(levels - 1, -1, -1):
+        if lvl < levels - 1:
+            fine = torch.empty(exts[lvl] + (wl.channels,), dtype=model.torch_dtype, device=gpu)
+            octnca.octree_nca_upsample(model, state, wl.factors[lvl], pyr[lvl], fine)
+            state = fine
+        other = torch.empty_like(state)
+        which = octnca.octree_nca_run_level(model, state, other, w_dev[lvl], lvl,
+                                            wl.steps[lvl], wl.fire_rate, wl.seed)
+        state = other if which else state
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(fused_state), to_np(state))
+    want_state, want_seg = oracle_infer(wl, image, weights)
+    assert_state_close(to_np(fused_state), want_state, wl.dtype)
+
+
 def test_infer_without_final_state_buffer(gpu):
     """final_state = NULL: both ping-pong buffers live in the workspace; the
     readout must be the same."""
