@@ -378,8 +378,8 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
         if (fused[l]) {
             // step 0 from the coarse state bufs[cur] (level l + 1) and image l
             const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
-            if (launch_step_up(a, bufs[cur], (int)p.ext[l + 1].w, f[1], f[2], img[l],
-                               bufs[cur ^ 1], s) != hipSuccess)
+            if (launch_step_up(a, bufs[cur], (int)p.ext[l + 1].h, (int)p.ext[l + 1].w, f[0],
+                               f[1], f[2], img[l], bufs[cur ^ 1], s) != hipSuccess)
                 return OCTNCA_EHIP;
             cur ^= 1;
             t0 = 1;
@@ -510,9 +510,11 @@ bool step_fuses_upsample(const StepArgs &a) {
     return sel.ok && !sel.valu && step_mfma_fuses_upsample(a, sel.mlp, sel.layout);
 }
 
-hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_w, int fy, int fx,
-                          const void *img, void *dst, hipStream_t stream) {
+hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, int coarse_w,
+                          int fz, int fy, int fx, const void *img, void *dst,
+                          hipStream_t stream) {
     const Selection sel = select_step_kernel();
-    return launch_step_mfma_up(a, sel.layout, coarse, coarse_w, fy, fx, img, dst, stream);
+    return launch_step_mfma_up(a, sel.layout, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
+                               stream);
 }
 }  // namespace octnca

@@ -52,8 +52,9 @@ hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_
 // Whether launch_step would fuse a level's first step with the upsample from
 // the next coarser level (see launch_step_mfma_up), and that fused launch.
 bool step_fuses_upsample(const StepArgs &a);
-hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_w, int fy, int fx,
-                          const void *img, void *dst, hipStream_t stream);
+hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, int coarse_w,
+                          int fz, int fy, int fx, const void *img, void *dst,
+                          hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 // MLP operand precision of the MFMA step kernel.  Default: split bf16 (x3)
 // for fp32 states, fp16 for fp16 states.
@@ -64,13 +65,14 @@ enum class Layout2d : int { Auto = 0, Rows = 1, Tiles = 2 };
 hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                             void *dst, hipStream_t stream);
 // The first step of a level fused with the upsample + inject from the next
-// coarser level (2D row-streaming kernel, default operand policy only):
+// coarser level (2D row-streaming kernel and fp16 3D kernel, default operand
+// policy only):
 // step_mfma_fuses_upsample says whether launch_step_mfma would run that kernel
 // for `a`; launch_step_mfma_up then reads the coarse state (width coarse_w,
 // factors fy, fx) and the level's image instead of a state of the level.
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
 hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *coarse,
-                               int coarse_w, int fy, int fx, const void *img, void *dst,
-                               hipStream_t stream);
+                               int coarse_h, int coarse_w, int fz, int fy, int fx,
+                               const void *img, void *dst, hipStream_t stream);
 
 }  // namespace octnca

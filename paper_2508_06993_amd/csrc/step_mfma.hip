@@ -531,6 +531,94 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
         planes[(2 * c + 1) * PS16 + cell] = make_uint2(x.z, x.w);
     }
 
+    // Upsample + inject fused into the load (3D first step of a level; fp16
+    // planes): plane z, row gy and cell gx of the fine level come from the
+    // coarse state's plane z / fz, row gy / fy and cell gx / fx (gathered per
+    // lane); the NIN input channels from the fine image, one element per
+    // thread and load, written over channel quad 0 by commit_up_raw.
+    static constexpr int kThreadsPerBlock = 256;
+    template <int NIN>
+    struct Image {
+        static constexpr int kElems = HY * kHaloW * NIN;
+        static constexpr int kImg = (kElems + kThreadsPerBlock - 1) / kThreadsPerBlock;
+        uint32_t e[kImg];
+    };
+
+    template <int NIN>
+    __device__ __forceinline__ void issue_up(const T *__restrict__ coarse, int cdh, int cdw,
+                                             int fz, int fy, int fx, const T *__restrict__ img,
+                                             Image<NIN> &im, int z, int dd, int dh, int dw,
+                                             int y0, int x0, bool active = true) {
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int gy0 = y0 - 1;
+        const int base_row = gy0 > 0 ? gy0 : 0;
+        const int rows =
+            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
+        // coarse rows base_row / fy .. (base_row + rows - 1) / fy of plane z / fz
+        const int cbase = base_row / fy;
+        const int crows = rows > 0 ? (base_row + rows - 1) / fy - cbase + 1 : 0;
+        const uint32_t crow_bytes = (uint32_t)cdw * kCellBytes;
+        const Rsrc r = make_rsrc(coarse + ((int64_t)(max(z, 0) / fz) * cdh + cbase) * cdw * kC,
+                                 (uint32_t)crows * crow_bytes);
+        const int cell = body_cell(lane);
+        const uint32_t chunk_off = (uint32_t)body_chunk(lane) * 16;
+#pragma unroll
+        for (int k = 0; k < kBodySlots; ++k) {
+            const int J = wave + 4 * k;
+            const int gy = gy0 + J / kBodyPerRow;
+            const int cx = x0 + (J % kBodyPerRow) * kCellsPerBody + cell;
+            const bool ok = J < kBody && gy >= 0 && cx < dw;
+            const uint32_t off = (uint32_t)(gy / fy - cbase) * crow_bytes +
+                                 (uint32_t)(cx / fx) * kCellBytes + chunk_off;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        {
+            const int s = 3 - wave;
+            const int row = s * kRowsPerSide + lane / (2 * NQ);
+            const int gy = gy0 + row;
+            const int gx = ((lane / NQ) & 1) ? x0 + kTileW : x0 - 1;
+            const bool ok = s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw;
+            const uint32_t off = (uint32_t)(gy / fy - cbase) * crow_bytes +
+                                 (uint32_t)(gx / fx) * kCellBytes + (uint32_t)(lane % NQ) * 16;
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
+            v[kBodySlots] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const uint32_t irow_bytes = (uint32_t)dw * NIN * (uint32_t)sizeof(T);
+        const Rsrc ri = make_rsrc(img + ((int64_t)max(z, 0) * dh + base_row) * dw * NIN,
+                                  (uint32_t)rows * irow_bytes);
+#pragma unroll
+        for (int j = 0; j < Image<NIN>::kImg; ++j) {
+            const int e = (int)threadIdx.x + kThreadsPerBlock * j;
+            const int row = e / (kHaloW * NIN);
+            const int rem = e - row * (kHaloW * NIN);
+            const int gy = gy0 + row;
+            const int gx = x0 - 1 + rem / NIN;
+            const bool ok = e < Image<NIN>::kElems && gy >= 0 && gx >= 0 && gx < dw;
+            const uint32_t off = (uint32_t)(gy - base_row) * irow_bytes +
+                                 (uint32_t)(gx * NIN + rem % NIN) * (uint32_t)sizeof(T);
+            im.e[j] = __builtin_amdgcn_raw_buffer_load_b16(ri, ok ? off : kOut, 0, 0);
+        }
+    }
+
+    // Called by every thread of the block: the coarse words of a cell and its
+    // image channels are written by different waves, so a barrier orders them.
+    template <int NIN>
+    __device__ __forceinline__ void commit_up_raw(uint2 *planes, const Image<NIN> &im) const {
+        commit_raw(planes);
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < Image<NIN>::kImg; ++j) {
+            const int e = (int)threadIdx.x + kThreadsPerBlock * j;
+            const int row = e / (kHaloW * NIN);
+            const int rem = e - row * (kHaloW * NIN);
+            const int slot = e < Image<NIN>::kElems ? row * kHaloW + rem / NIN : kDummyCell;
+            reinterpret_cast<unsigned short *>(planes + slot)[rem % NIN] =
+                (unsigned short)im.e[j];   // channel quad plane 0
+        }
+    }
+
     __device__ __forceinline__ void commit_raw(uint2 *planes) const {
         static_assert(NQ == 2, "raw fp16 planes");
         const int lane = threadIdx.x & 63;
@@ -1322,13 +1410,19 @@ __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uin
 
 constexpr int k3hBlocksPerCu = 3;
 
-template <int NIN, bool ALIGNED>
-__global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16(
+// UP: the first step of a level fused with the upsample + inject: src is the
+// next coarser level's state (extent up_cdh x up_cdw per plane), upsampled by
+// (up_fz, up_fy, up_fx), with the input channels from up_img.
+// (The UP variant runs one step per level and needs more registers for its
+// extra loads: it is built for 2 blocks per CU, the plain one for 3.)
+template <int NIN, bool ALIGNED, bool UP>
+__global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mfma_3d_f16(
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
     int tiles_x, int tiles_y, int items, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
-    uint64_t threshold) {
+    uint64_t threshold, const __half *__restrict__ up_img, int up_cdh, int up_cdw, int up_fz,
+    int up_fy, int up_fx) {
     using Loader = RowLoader<__half, k3TY + 2>;
     __shared__ uint2 ring[3][4 * Loader::PS16];
     __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
@@ -1371,7 +1465,22 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     const int zruns = (dd + k3ZRun - 1) / k3ZRun;
+    int y0_cur = 0, x0_cur = 0;   // the current item's tile origin (for the loads)
     Loader ld;
+    typename Loader::template Image<NIN> im;   // used by UP only
+    auto issue = [&](int z, bool active) {
+        if constexpr (UP)
+            ld.template issue_up<NIN>(src, up_cdh, up_cdw, up_fz, up_fy, up_fx, up_img, im, z,
+                                      dd, dh, dw, y0_cur, x0_cur, active);
+        else
+            ld.issue(src, z, dd, dh, dw, y0_cur, x0_cur, active);
+    };
+    auto commit = [&](uint2 *slot) {
+        if constexpr (UP)
+            ld.template commit_up_raw<NIN>(slot, im);
+        else
+            ld.commit_raw(slot);
+    };
     int centre[4];
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp)
@@ -1384,6 +1493,8 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
         const int tx = rest % tiles_x;
         const int ty = rest / tiles_x;
         const int y0 = ty * k3TY, x0 = tx * kTileW;
+        y0_cur = y0;
+        x0_cur = x0;
         const int z_begin = zr * k3ZRun;
         const int z_end = min(dd, z_begin + k3ZRun);
         // store offsets of the lane's 4 cells within an output plane's tile rows
@@ -1409,9 +1520,9 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
             }
 
         __syncthreads();
-        ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
-        ld.commit_raw(ring[0]);
-        ld.issue(src, z_begin, dd, dh, dw, y0, x0);
+        issue(z_begin - 1, true);
+        commit(ring[0]);
+        issue(z_begin, true);
         __syncthreads();
 
         int slot = 0, slot_prev = 2;
@@ -1520,8 +1631,8 @@ __global__ __launch_bounds__(kThreads, k3hBlocksPerCu) void nca_step_mfma_3d_f16
                 }
 
             const int slot_next = 3 - slot - slot_prev;
-            ld.commit_raw(ring[slot_next]);
-            ld.issue(src, p + 2, dd, dh, dw, y0, x0, p + 2 <= z_end);
+            commit(ring[slot_next]);
+            issue(p + 2, p + 2 <= z_end);
             __syncthreads();
             slot_prev = slot;
             slot = slot_next;
@@ -1613,12 +1724,12 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     if (items > INT32_MAX) return hipErrorInvalidValue;
     if constexpr (std::is_same_v<T, __half> && std::is_same_v<Mlp, MlpF16>) {
         const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * k3hBlocksPerCu);
-        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true>
-                                     : nca_step_mfma_3d_f16<NIN, false>;
+        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, false>
+                                     : nca_step_mfma_3d_f16<NIN, false, false>;
         kern<<<grid, kThreads, 0, stream>>>(
             (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
-            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
-            a.seed, a.threshold);
+            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
+            a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1);
     } else {
         const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * kBlocksPerCu);
         nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
@@ -1626,6 +1737,27 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
             (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
             a.threshold);
     }
+    return hipGetLastError();
+}
+
+// fp16 3D first step fused with the upsample from the coarse state (planes of
+// cdh x cdw cells, factors fz, fy, fx) and the level's image img.
+template <int NIN>
+hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int cdw, int fz,
+                            int fy, int fx, const void *img, void *dst, hipStream_t stream) {
+    const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
+    const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
+    const int64_t zruns = (a.ext.d + k3ZRun - 1) / k3ZRun;
+    const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
+    if (items == 0) return hipSuccess;
+    if (items > INT32_MAX) return hipErrorInvalidValue;
+    const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * 2);
+    auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, true>
+                                 : nca_step_mfma_3d_f16<NIN, false, true>;
+    kern<<<grid, kThreads, 0, stream>>>(
+        (const __half *)coarse, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
+        tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
+        a.batch, a.seed, a.threshold, (const __half *)img, cdh, cdw, fz, fy, fx);
     return hipGetLastError();
 }
 
@@ -1652,14 +1784,25 @@ bool mfma_fits(const StepArgs &a) {
 }
 
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
-    return a.ndim == 2 && a.channels == kC && a.hidden == kH && mlp == MfmaMlp::Default &&
-           mfma_fits(a) && uses_rows(a, layout);
+    if (a.channels != kC || a.hidden != kH || mlp != MfmaMlp::Default || !mfma_fits(a))
+        return false;
+    if (a.ndim == 2) return uses_rows(a, layout);
+    return a.dtype == Dtype::F16;   // the fp16 3D step
 }
 
 hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *coarse,
-                               int coarse_w, int fy, int fx, const void *img, void *dst,
-                               hipStream_t stream) {
+                               int coarse_h, int coarse_w, int fz, int fy, int fx,
+                               const void *img, void *dst, hipStream_t stream) {
     if (!step_mfma_fuses_upsample(a, MfmaMlp::Default, layout)) return hipErrorInvalidValue;
+    if (a.ndim == 3) {
+        if (a.n_in == 1)
+            return launch_3d_f16_up<1>(a, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
+                                       stream);
+        if (a.n_in == 3)
+            return launch_3d_f16_up<3>(a, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
+                                       stream);
+        return hipErrorInvalidValue;
+    }
     if (a.dtype == Dtype::F32) {
         if (a.n_in == 1)
             return launch_rows<float, 1, MlpBf16x3, true>(a, coarse, dst, img, coarse_w, fy, fx,

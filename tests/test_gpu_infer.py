@@ -133,15 +133,23 @@ FUSION_CASES = [scaled(TINY_2D, (1, 64, 96), steps=(3, 2, 4)),
                          image_kind="uniform"),
                 Workload(name="fused_zero_steps", ndim=2, extent=(1, 40, 64), n_in=3,
                          factors=((1, 2, 2), (1, 2, 2)), steps=(3, 0, 2),
+                         image_kind="uniform"),
+                # the fp16 3D step fuses the upsample too (time pooled, anisotropic)
+                Workload(name="fused_3d_f16", ndim=3, extent=(36, 16, 40), n_in=3,
+                         factors=((1, 2, 2), (2, 2, 2)), steps=(2, 3, 2), dtype="f16",
+                         image_kind="uniform"),
+                Workload(name="fused_3d_f16_nin1", ndim=3, extent=(12, 18, 24), n_in=1,
+                         factors=((3, 1, 2), (1, 3, 1)), steps=(1, 2, 3), dtype="f16",
                          image_kind="uniform")]
 
 
 @pytest.mark.parametrize("wl", FUSION_CASES, ids=lambda w: w.name)
 def test_fused_first_step_equals_separate_upsample(gpu, monkeypatch, wl):
-    """With the 2D row layout, octree_nca_infer fuses each level's first step
-    with the upsample + inject.  The same pipeline built from the separate
-    entry points (pyramid, upsample, run_level: the same row kernel without
-    fusion) must give the same bits."""
+    """octree_nca_infer fuses each level's first step with the upsample +
+    inject where the level runs the 2D row-streaming kernel (forced here) or
+    the fp16 3D kernel.  The same pipeline built from the separate entry points
+    (pyramid, upsample, run_level: the same kernels without fusion) must give
+    the same bits."""
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
     model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
     image = make_image(wl)
