@@ -418,6 +418,22 @@ __device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, kRsrcWord3);
 }
 
+// Workgroups go to the eight XCDs in turn (blockIdx % 8) and each XCD has an
+// L2 of its own.  The grid-stride loops of the 3D step kernels map their index
+// u to a work item such that the workgroups of one XCD that run at the same
+// time take consecutive items (neighbouring tiles of one z run), which then
+// find each other's halo rows and columns in that L2 instead of fetching the
+// same lines again (measured: 1% off the video step; the 2D row kernel, where
+// it measured 2% slower, keeps the plain order).  A bijection of
+// [0, rounds * grid) when grid % 8 == 0, the identity otherwise.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int64_t xcd_item(int64_t u, int grid) {
+    if (grid % kXcds) return u;
+    const int64_t r = u / grid;
+    const int b = (int)(u - r * grid);
+    return (r * kXcds + b % kXcds) * (grid / kXcds) + b / kXcds;
+}
+
 template <typename T, int HY>
 struct RowLoader {
     static constexpr int NQ = CellChunks<T>::N;
@@ -1194,6 +1210,9 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
 // ---------------------------------------------------------------------------
 constexpr int k3TY = 8;
 constexpr int k3ZRun = 32;    // output planes per work item
+// Work item i of a 3D step is tile (tx, ty) of z run zr, with
+// i = (zr * tiles_y + ty) * tiles_x + tx.
+
 
 template <typename T, int NIN, class Mlp>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
@@ -1248,7 +1267,6 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
-    const int zruns = (dd + k3ZRun - 1) / k3ZRun;
     Loader ld;
     // LDS word of group grp's cell (row 2 wave + grp / 2, column 16 (grp % 2) + n)
     // in the quad plane of this lane, relative to a plane slot.
@@ -1257,10 +1275,13 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     for (int grp = 0; grp < 4; ++grp)
         centre[grp] = g * Loader::PS + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
 
-    for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        int rest = item;
-        const int zr = rest % zruns;
-        rest /= zruns;
+    const int64_t span = ((int64_t)items + gridDim.x - 1) / gridDim.x * gridDim.x;
+    for (int64_t u = blockIdx.x; u < span; u += gridDim.x) {
+        const int64_t it = xcd_item(u, (int)gridDim.x);
+        if (it >= items) continue;                       // uniform over the block
+        const int tiles = tiles_x * tiles_y;
+        const int zr = (int)it / tiles;
+        const int rest = (int)it - zr * tiles;
         const int tx = rest % tiles_x;
         const int ty = rest / tiles_x;
         const int y0 = ty * k3TY, x0 = tx * kTileW;
@@ -1464,7 +1485,6 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     constexpr int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
-    const int zruns = (dd + k3ZRun - 1) / k3ZRun;
     int y0_cur = 0, x0_cur = 0;   // the current item's tile origin (for the loads)
     Loader ld;
     typename Loader::template Image<NIN> im;   // used by UP only
@@ -1486,10 +1506,13 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     for (int grp = 0; grp < 4; ++grp)
         centre[grp] = g * Loader::PS16 + (2 * wave + (grp >> 1) + 1) * kHaloW + (grp & 1) * 16 + n + 1;
 
-    for (int item = blockIdx.x; item < items; item += gridDim.x) {
-        int rest = item;
-        const int zr = rest % zruns;
-        rest /= zruns;
+    const int64_t span = ((int64_t)items + gridDim.x - 1) / gridDim.x * gridDim.x;
+    for (int64_t u = blockIdx.x; u < span; u += gridDim.x) {
+        const int64_t it = xcd_item(u, (int)gridDim.x);
+        if (it >= items) continue;                       // uniform over the block
+        const int tiles = tiles_x * tiles_y;
+        const int zr = (int)it / tiles;
+        const int rest = (int)it - zr * tiles;
         const int tx = rest % tiles_x;
         const int ty = rest / tiles_x;
         const int y0 = ty * k3TY, x0 = tx * kTileW;
