@@ -65,8 +65,12 @@ def step_kernel_arithmetic(wl):
         return "nca_step_mfma / fp32 MFMA", "fp32 MFMA", FP32_MFMA_PEAK_TFLOPS
     if sel == "mfma_f16" or (sel == "mfma" and wl.dtype == "f16"):
         return "nca_step_mfma / fp16 MFMA", "fp16 MFMA", FP16_MFMA_PEAK_TFLOPS
-    return "nca_step_mfma / split-bf16 MFMA", "bf16 MFMA (3 products per fp32 product)", \
-        BF16_MFMA_PEAK_TFLOPS
+    if sel == "mfma_bf16x3":
+        return "nca_step_mfma / split-bf16 MFMA", "bf16 MFMA (3 products per fp32 product)", \
+            BF16_MFMA_PEAK_TFLOPS
+    return "nca_step_mfma / scaled-fp16 MFMA", \
+        "fp16 MFMA (fp16 activations x split fp16 weights, 2 products per fp32 product)", \
+        FP16_MFMA_PEAK_TFLOPS
 
 
 STEP_SOURCES = ("paper_2508_06993_amd/csrc/step_mfma.hip", "paper_2508_06993_amd/csrc/device_common.h")

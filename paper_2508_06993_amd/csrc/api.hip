@@ -489,6 +489,7 @@ Selection select_step_kernel() {
     else if (strcmp(sel, "mfma_f32") == 0) r.mlp = MfmaMlp::F32;
     else if (strcmp(sel, "mfma_bf16x3") == 0) r.mlp = MfmaMlp::Bf16x3;
     else if (strcmp(sel, "mfma_f16") == 0) r.mlp = MfmaMlp::F16;
+    else if (strcmp(sel, "mfma_f16s") == 0) r.mlp = MfmaMlp::F16S;
     else if (strcmp(sel, "mfma_rows") == 0) r.layout = Layout2d::Rows;
     else if (strcmp(sel, "mfma_tiles") == 0) r.layout = Layout2d::Tiles;
     else r.ok = false;

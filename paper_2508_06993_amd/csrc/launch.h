@@ -56,9 +56,9 @@ hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, i
                           int fz, int fy, int fx, const void *img, void *dst,
                           hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
-// MLP operand precision of the MFMA step kernel.  Default: split bf16 (x3)
-// for fp32 states, fp16 for fp16 states.
-enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3 };
+// MLP operand precision of the MFMA step kernel.  Default: scaled fp16
+// activations with split fp16 weights (F16S) for fp32 states, fp16 for fp16 states.
+enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3, F16S = 4 };
 // Work layout of the 2D MFMA step.  Auto: row streaming on large levels,
 // 16 x 32 tiles on small ones; Rows / Tiles force one (3D steps ignore it).
 enum class Layout2d : int { Auto = 0, Rows = 1, Tiles = 2 };

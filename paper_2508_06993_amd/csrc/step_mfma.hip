@@ -321,6 +321,93 @@ struct MlpF16 {
     }
 };
 
+// Scaled fp16 activations with split fp16 weights (for fp32 states).  The
+// features and the hidden units are rounded to fp16 after a scaling by 2^-8
+// (a power of two: exact), which keeps fp32 states of magnitude up to
+// 65504 * 2^8 in fp16 range; the weights are hi + lo fp16 pairs (W1 as is,
+// b1 times 2^-8 as the accumulator start, W2 times 2^8 so that u comes out
+// unscaled), two products per weight: 8 + 4 MFMAs per 16 cells and no
+// activation split.  The activations keep fp16's 2^-12 relative rounding,
+// the weights about 2^-22.
+constexpr float kF16ActScale = 1.f / 256.f;
+struct MlpF16S {
+    v8h w1h[4], w1l[4];   // [jt] slot s: W1[jt*16 + n][feature(s, g)], hi + lo
+    v4f b1[4];            // b1 * 2^-8
+    v8h w2h[2], w2l[2];   // [p] slot s: 2^8 W2[n][hidden(p, s, g)], hi + lo
+
+    __device__ __forceinline__ void pin_all() {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            pin(w1h[jt]);
+            pin(w1l[jt]);
+            pin(b1[jt]);
+        }
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            pin(w2h[p]);
+            pin(w2l[p]);
+        }
+    }
+
+    __device__ static __forceinline__ void split(const v8f &x, v8h &hi, v8h &lo) {
+        hi = __builtin_convertvector(x, v8h);
+        lo = __builtin_convertvector(x - __builtin_convertvector(hi, v8f), v8h);
+    }
+
+    __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
+                                         const float *__restrict__ W2, int n, int g) {
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt) {
+            v8f x;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) x[s] = W1[(jt * 16 + n) * 2 * kC + feature_of(s, g)];
+            split(x, w1h[jt], w1l[jt]);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) b1[jt][i] = B1[jt * 16 + 4 * g + i] * kF16ActScale;
+        }
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            v8f x;
+#pragma unroll
+            for (int s = 0; s < 8; ++s)
+                x[s] = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)] * (1.f / kF16ActScale);
+            split(x, w2h[p], w2l[p]);
+        }
+    }
+
+    __device__ __forceinline__ void layer1(const float f[8], v4f acc[4]) const {
+        v8f fx;
+#pragma unroll
+        for (int s = 0; s < 8; ++s) fx[s] = f[s] * kF16ActScale;
+        const v8h fh = __builtin_convertvector(fx, v8h);
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1l[jt], fh, b1[jt], 0, 0, 0);
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+            acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1h[jt], fh, acc[jt], 0, 0, 0);
+    }
+
+    // ReLU as packed fp16 max after the rounding (as in MlpF16)
+    __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
+        v4f u[2];
+        const v8h zero = {};
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            v8f x;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) x[s] = acc[2 * p + s / 4][s % 4];
+            const v8h h = __builtin_elementwise_max(__builtin_convertvector(x, v8h), zero);
+            u[p] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2l[p], h, v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+            u[p] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2h[p], h, u[p], 0, 0, 0);
+        }
+        return u[0] + u[1];
+    }
+};
+
+// The MLP policy of fp32 states when none is asked for.
+using MlpF32State = MlpF16S;
+
 // Fire bits.  One Philox4x64-10 evaluation gives the draws of a block of 8
 // consecutive cells, so a wave evaluates one block per lane and spreads the
 // bits with eight ballots (ballot b holds the bit of cell b of each lane's
@@ -1828,11 +1915,11 @@ hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *c
     }
     if (a.dtype == Dtype::F32) {
         if (a.n_in == 1)
-            return launch_rows<float, 1, MlpBf16x3, true>(a, coarse, dst, img, coarse_w, fy, fx,
-                                                          stream);
+            return launch_rows<float, 1, MlpF32State, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                            stream);
         if (a.n_in == 3)
-            return launch_rows<float, 3, MlpBf16x3, true>(a, coarse, dst, img, coarse_w, fy, fx,
-                                                          stream);
+            return launch_rows<float, 3, MlpF32State, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                            stream);
     } else {
         if (a.n_in == 1)
             return launch_rows<__half, 1, MlpF16, true>(a, coarse, dst, img, coarse_w, fy, fx,
@@ -1848,11 +1935,12 @@ hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, con
                             void *dst, hipStream_t stream) {
     if (!mfma_fits(a)) return launch_step_valu(a, src, dst, stream);
     if (mlp == MfmaMlp::Default)
-        mlp = a.dtype == Dtype::F32 ? MfmaMlp::Bf16x3 : MfmaMlp::F16;
+        mlp = a.dtype == Dtype::F32 ? MfmaMlp::F16S : MfmaMlp::F16;
     if (a.dtype == Dtype::F32) {
         switch (mlp) {
             case MfmaMlp::F32: return dispatch<float, MlpF32>(a, layout, src, dst, stream);
             case MfmaMlp::Bf16x3: return dispatch<float, MlpBf16x3>(a, layout, src, dst, stream);
+            case MfmaMlp::F16S: return dispatch<float, MlpF32State>(a, layout, src, dst, stream);
             default: return hipErrorInvalidValue;   // fp16 operands are too coarse for fp32 states
         }
     }

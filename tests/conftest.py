@@ -42,17 +42,18 @@ def gpu():
     return torch.device("cuda", 0)
 
 
-STEP_KERNELS = ("mfma", "mfma_rows", "mfma_tiles", "mfma_f32", "valu")
+STEP_KERNELS = ("mfma", "mfma_rows", "mfma_tiles", "mfma_f32", "mfma_bf16x3", "valu")
 
 
 @pytest.fixture(params=STEP_KERNELS)
 def step_kernel(request, monkeypatch):
     """Run a test once per fused-step kernel (the library reads
     OCTREE_NCA_STEP_KERNEL at every launch).  "mfma" is the default kernel:
-    split-bf16 MLP operands for fp32 states, fp16 operands for fp16 states,
-    and for 2D the work layout chosen by level size; "mfma_rows" and
-    "mfma_tiles" force the 2D layout (row streaming, 16 x 32 tiles) so both
-    are covered at test sizes; "mfma_f32" uses fp32 MLP operands; "valu" is
-    the one-thread-per-cell vector kernel."""
+    scaled fp16 activations with split fp16 weights for fp32 states, fp16
+    operands for fp16 states, and for 2D the work layout chosen by level
+    size; "mfma_rows" and "mfma_tiles" force the 2D layout (row streaming,
+    16 x 32 tiles) so both are covered at test sizes; "mfma_f32" uses fp32 MLP
+    operands, "mfma_bf16x3" split-bf16 ones; "valu" is the one-thread-per-cell
+    vector kernel."""
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", request.param)
     return request.param

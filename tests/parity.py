@@ -2,10 +2,12 @@
 
 State: max relative error = max |g - o| / max |o| over all cells and channels;
 bound 1e-3 for fp32 storage, 1e-2 for fp16 storage.
-Readout: agreement fraction >= 0.9999 (fp32) / 0.999 (fp16) over the compared
-cells, and every disagreeing cell must be a near tie of the oracle's last two
-channels (margin within the state bound), since there the argmax is not
-determined by the method to better than rounding.
+Readout: agreement >= 0.9999 (fp32) / 0.999 (fp16) as a rate over the
+compared cells: on N cells at most ceil((1 - rate) N) disagreements (one on a
+case of fewer than 10^4 cells, where the rate allows no whole cell), and every
+disagreeing cell must be a near tie of the oracle's last two channels (margin
+within the state bound), since there the argmax is not determined by the
+method to better than rounding.
 Input channels, masks and indices: bit-exact.
 """
 import numpy as np
@@ -46,5 +48,7 @@ def assert_seg_close(got_seg, ref_seg, ref_state, dtype: str, min_agree=None, wh
     scale = float(np.max(np.abs(o))) if o.size else 0.0
     not_ties = bad & (margin > 2 * STATE_TOL[dtype] * scale)
     assert not np.any(not_ties), f"{what}: {int(not_ties.sum())} clear argmax disagreements"
-    assert agree >= min_agree, f"{what}: agreement {agree:.6f} < {min_agree}"
+    allowed = int(np.ceil((1.0 - min_agree) * bad.size - 1e-9))
+    assert int(bad.sum()) <= allowed, (f"{what}: agreement {agree:.6f} < {min_agree} "
+                                      f"({int(bad.sum())} of {bad.size} cells, {allowed} allowed)")
     return agree
