@@ -70,7 +70,11 @@ __device__ __forceinline__ void pin(V &x) {
 // its 8 features in two halves: layer1 (features -> hidden accumulators, all
 // MFMA) and layer2 (ReLU, hidden -> update).  Splitting them lets a wave
 // issue the next group's perception while layer 1's MFMAs run.  All
-// accumulate in fp32.
+// accumulate in fp32.  The second layer has outputs for the hidden channels
+// only (Sec. 3.1): load() gathers the W2 rows of the nin input channels as
+// zeros, so their update is exactly +0 and the residual needs no per-channel
+// mask.  kPerceptionScale: the factor the kernel applies to the perception
+// weights and bias (features 4..7 arrive multiplied by it).
 // ---------------------------------------------------------------------------
 
 // ReLU as an integer max on the float's bits: negative floats (sign bit set)
@@ -81,6 +85,7 @@ __device__ __forceinline__ float relu(float x) {
 
 // fp32 operands: v_mfma_f32_16x16x4_f32, 32 + 16 MFMAs per 16 cells.
 struct MlpF32 {
+    static constexpr float kPerceptionScale = 1.f;
     float w1[4][8];   // [jt][kc] = W1[jt*16 + n][feature(kc, g)]
     v4f b1[4];        // [jt][i]  = b1[jt*16 + 4g + i]
     float w2[4][4];   // [jt][i]  = W2[n][jt*16 + 4g + i]   (n = output channel)
@@ -97,7 +102,7 @@ struct MlpF32 {
     }
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
-                                         const float *__restrict__ W2, int n, int g) {
+                                         const float *__restrict__ W2, int n, int g, int nin) {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
 #pragma unroll
@@ -105,7 +110,7 @@ struct MlpF32 {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 b1[jt][i] = B1[jt * 16 + 4 * g + i];
-                w2[jt][i] = W2[n * kH + jt * 16 + 4 * g + i];
+                w2[jt][i] = n < nin ? 0.f : W2[n * kH + jt * 16 + 4 * g + i];
             }
         }
     }
@@ -167,6 +172,7 @@ __device__ __forceinline__ void split_bf16(const v8f &x, v8bf &hi, v8bf &lo) {
 }
 
 struct MlpBf16x3 {
+    static constexpr float kPerceptionScale = 1.f;
     v8bf w1h[4], w1l[4];   // [jt] slot s: W1[jt*16 + n][feature(s, g)]
     v4f b1[4];
     v8bf w2h[2], w2l[2];   // [p] slot s: W2[n][hidden(p, s, g)]
@@ -192,7 +198,7 @@ struct MlpBf16x3 {
     }
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
-                                         const float *__restrict__ W2, int n, int g) {
+                                         const float *__restrict__ W2, int n, int g, int nin) {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             v8f x;
@@ -206,7 +212,7 @@ struct MlpBf16x3 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = W2[n * kH + hidden_of(p, s, g)];
+            for (int s = 0; s < 8; ++s) x[s] = n < nin ? 0.f : W2[n * kH + hidden_of(p, s, g)];
             split_bf16(x, w2h[p], w2l[p]);
         }
     }
@@ -255,6 +261,7 @@ struct MlpBf16x3 {
 // hidden activations rounded to fp16, products accumulated in fp32 on
 // v_mfma_f32_16x16x32_f16; 4 + 2 MFMAs per 16 cells.
 struct MlpF16 {
+    static constexpr float kPerceptionScale = 1.f;
     v8h w1[4];
     v4f b1[4];
     v8h w2[2];
@@ -270,7 +277,7 @@ struct MlpF16 {
     }
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
-                                         const float *__restrict__ W2, int n, int g) {
+                                         const float *__restrict__ W2, int n, int g, int nin) {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             v8f x;
@@ -284,7 +291,8 @@ struct MlpF16 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];
+            for (int s = 0; s < 8; ++s)
+                x[s] = n < nin ? 0.f : W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];
             w2[p] = __builtin_convertvector(x, v8h);
         }
     }
@@ -331,6 +339,7 @@ struct MlpF16 {
 // the weights about 2^-22.
 constexpr float kF16ActScale = 1.f / 256.f;
 struct MlpF16S {
+    static constexpr float kPerceptionScale = kF16ActScale;
     v8h w1h[4], w1l[4];   // [jt] slot s: W1[jt*16 + n][feature(s, g)], hi + lo
     v4f b1[4];            // b1 * 2^-8
     v8h w2h[2], w2l[2];   // [p] slot s: 2^8 W2[n][hidden(p, s, g)], hi + lo
@@ -355,7 +364,7 @@ struct MlpF16S {
     }
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
-                                         const float *__restrict__ W2, int n, int g) {
+                                         const float *__restrict__ W2, int n, int g, int nin) {
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt) {
             v8f x;
@@ -370,15 +379,15 @@ struct MlpF16S {
             v8f x;
 #pragma unroll
             for (int s = 0; s < 8; ++s)
-                x[s] = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)] * (1.f / kF16ActScale);
+                x[s] = n < nin ? 0.f : W2[n * kH + MlpBf16x3::hidden_of(p, s, g)] * (1.f / kF16ActScale);
             split(x, w2h[p], w2l[p]);
         }
     }
 
     __device__ __forceinline__ void layer1(const float f[8], v4f acc[4]) const {
-        v8f fx;
+        v8f fx;   // state features scaled here, the perception arrives scaled
 #pragma unroll
-        for (int s = 0; s < 8; ++s) fx[s] = f[s] * kF16ActScale;
+        for (int s = 0; s < 8; ++s) fx[s] = s < 4 ? f[s] * kF16ActScale : f[s];
         const v8h fh = __builtin_convertvector(fx, v8h);
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
@@ -390,7 +399,7 @@ struct MlpF16S {
 
     // ReLU as packed fp16 max after the rounding (as in MlpF16)
     __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
-        v4f u[2];
+        v4f u = {0.f, 0.f, 0.f, 0.f};
         const v8h zero = {};
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -398,10 +407,10 @@ struct MlpF16S {
 #pragma unroll
             for (int s = 0; s < 8; ++s) x[s] = acc[2 * p + s / 4][s % 4];
             const v8h h = __builtin_elementwise_max(__builtin_convertvector(x, v8h), zero);
-            u[p] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2l[p], h, v4f{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
-            u[p] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2h[p], h, u[p], 0, 0, 0);
+            u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2l[p], h, u, 0, 0, 0);
+            u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2h[p], h, u, 0, 0, 0);
         }
-        return u[0] + u[1];
+        return u;
     }
 };
 
@@ -743,9 +752,9 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
 
 // Residual update and store of the lane's 4 channels (fp32 values, stored in
 // the storage type) through the tile's store descriptor; `off` is the byte
-// offset of the cell in it, or kOut for a cell outside the grid.  upd[k] is
-// 0 for input channels, 1 otherwise; with m * upd = 0 the fma returns the
-// state bit for bit (u is finite).
+// offset of the cell in it, or kOut for a cell outside the grid.  u is +0 for
+// the input channels (zero W2 rows) and m is 0 for a cell that does not
+// fire: then the fma returns the state bit for bit (u finite).
 __device__ __forceinline__ void store_quad(float *, Rsrc w, uint32_t off, int g, const v4f &v) {
     const v4u x = {__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
                    __float_as_uint(v[3])};
@@ -758,13 +767,13 @@ __device__ __forceinline__ void store_quad(__half *, Rsrc w, uint32_t off, int g
 
 template <typename T>
 __device__ __forceinline__ void update_store(T *tag, Rsrc w, uint32_t off, int g, const float f[8],
-                                             const v4f &u, const float upd[4], bool fire) {
+                                             const v4f &u, bool fire) {
     const float m = fire ? 1.f : 0.f;
     v4f out;
-    out[0] = fmaf(m * upd[0], u[0], f[0]);
-    out[1] = fmaf(m * upd[1], u[1], f[1]);
-    out[2] = fmaf(m * upd[2], u[2], f[2]);
-    out[3] = fmaf(m * upd[3], u[3], f[3]);
+    out[0] = fmaf(m, u[0], f[0]);
+    out[1] = fmaf(m, u[1], f[1]);
+    out[2] = fmaf(m, u[2], f[2]);
+    out[3] = fmaf(m, u[3], f[3]);
     store_quad(tag, w, off, g, out);
 }
 
@@ -837,27 +846,21 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     {
         const int i = min((int)threadIdx.x, 9 * 4 - 1);
         const int t = i / 4, q = i % 4;
-        const float4 tw = make_float4(conv_w[(4 * q + 0) * 9 + t], conv_w[(4 * q + 1) * 9 + t],
-                                      conv_w[(4 * q + 2) * 9 + t], conv_w[(4 * q + 3) * 9 + t]);
+        constexpr float ps = Mlp::kPerceptionScale;
+        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
+                                      ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
         if (threadIdx.x < 9 * 4) tapw[t][q] = tw;
     }
     Mlp mlp;
-    mlp.load(w1, b1, w2, n, g);
+    mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
-    float upd[4];   // channels < NIN are copied, never updated
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        cb[k] = conv_b[4 * g + k];
-        upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
-    }
+    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
     // all weight loads done before the tile loop (keeps the compiler's
     // vector-memory counting exact inside it)
     mlp.pin_all();
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        pin(cb[k]);
-        pin(upd[k]);
-    }
+    for (int k = 0; k < 4; ++k) pin(cb[k]);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -938,7 +941,7 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
             const uint64_t idx = (uint64_t)y * dw + x;
             const uint64_t row_b0 = ((uint64_t)y * dw + x0) >> 3;
             const uint32_t off = x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-            update_store(dst, wr, off, g, f, u, upd, fire.bit(slot0 + r, idx, row_b0));
+            update_store(dst, wr, off, g, f, u, fire.bit(slot0 + r, idx, row_b0));
 #pragma unroll
             for (int k = 0; k < 8; ++k) f[k] = fn[k];
             // keep the scheduler from interleaving whole groups (register pressure)
@@ -1116,25 +1119,19 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     {
         const int i = min(lane, 9 * 4 - 1);
         const int t = i / 4, q = i % 4;
-        const float4 tw = make_float4(conv_w[(4 * q + 0) * 9 + t], conv_w[(4 * q + 1) * 9 + t],
-                                      conv_w[(4 * q + 2) * 9 + t], conv_w[(4 * q + 3) * 9 + t]);
+        constexpr float ps = Mlp::kPerceptionScale;
+        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
+                                      ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
         if (lane < 9 * 4) tapw[t][q] = tw;
     }
     Mlp mlp;
-    mlp.load(w1, b1, w2, n, g);
+    mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
-    float upd[4];   // channels < NIN are copied, never updated
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        cb[k] = conv_b[4 * g + k];
-        upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
-    }
+    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
     mlp.pin_all();
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        pin(cb[k]);
-        pin(upd[k]);
-    }
+    for (int k = 0; k < 4; ++k) pin(cb[k]);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -1255,7 +1252,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
                     const uint64_t idx = (uint64_t)yc * dw + x;
                     fires = fire.bit(phase, idx, row_b0);
                 }
-                update_store(dst, wr, off, g, f[grp], u, upd, fires);
+                update_store(dst, wr, off, g, f[grp], u, fires);
             }
 #pragma unroll
             for (int grp = 0; grp < 2; ++grp)
@@ -1320,25 +1317,19 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     {
         const int i = min((int)threadIdx.x, 27 * 4 - 1);
         const int t = i / 4, q = i % 4;
-        const float4 tw = make_float4(conv_w[(4 * q + 0) * 27 + t], conv_w[(4 * q + 1) * 27 + t],
-                                      conv_w[(4 * q + 2) * 27 + t], conv_w[(4 * q + 3) * 27 + t]);
+        constexpr float ps = Mlp::kPerceptionScale;
+        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 27 + t], ps * conv_w[(4 * q + 1) * 27 + t],
+                                      ps * conv_w[(4 * q + 2) * 27 + t], ps * conv_w[(4 * q + 3) * 27 + t]);
         if (threadIdx.x < 27 * 4) tapw[t][q] = tw;
     }
     Mlp mlp;
-    mlp.load(w1, b1, w2, n, g);
+    mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
-    float upd[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        cb[k] = conv_b[4 * g + k];
-        upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
-    }
+    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
     mlp.pin_all();
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        pin(cb[k]);
-        pin(upd[k]);
-    }
+    for (int k = 0; k < 4; ++k) pin(cb[k]);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -1478,7 +1469,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                     x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
                 const uint64_t fw = fire_words[wave][idx & 7];
                 const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
-                update_store(dst, wr, off, g, f, u, upd, fires);
+                update_store(dst, wr, off, g, f, u, fires);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
@@ -1549,18 +1540,15 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
         if (threadIdx.x < 27 * 4) tapw[t][q] = make_uint2(as_u32(lo), as_u32(hi));
     }
     MlpF16 mlp;
-    mlp.load(w1, b1, w2, n, g);
+    mlp.load(w1, b1, w2, n, g, NIN);
     h2 cb[2];
-    float upd[4];
     cb[0] = h2{(_Float16)conv_b[4 * g + 0], (_Float16)conv_b[4 * g + 1]};
     cb[1] = h2{(_Float16)conv_b[4 * g + 2], (_Float16)conv_b[4 * g + 3]};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) upd[k] = (4 * g + k) >= NIN ? 1.f : 0.f;
+    float one = 1.f;
     mlp.pin_all();
     pin(cb[0]);
     pin(cb[1]);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) pin(upd[k]);
+    pin(one);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_sched_barrier(0);
@@ -1720,13 +1708,14 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                     fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
                 }
                 const uint32_t off = offs[grp];
-                // state + update in fp32, rounded once to fp16 (upd[k] = 0 keeps an
+                // state + update in fp32, rounded once to fp16 (u = +0 keeps an
                 // input channel exactly); a cell that does not fire keeps its
                 // stored bits
-                const h2 n01 = {(_Float16)fmaf(upd[0], u[0], (float)s01[0]),
-                                (_Float16)fmaf(upd[1], u[1], (float)s01[1])};
-                const h2 n23 = {(_Float16)fmaf(upd[2], u[2], (float)s23[0]),
-                                (_Float16)fmaf(upd[3], u[3], (float)s23[1])};
+                // (as fmas with a register 1.0: one mixed-precision fma per value)
+                const h2 n01 = {(_Float16)fmaf(one, u[0], (float)s01[0]),
+                                (_Float16)fmaf(one, u[1], (float)s01[1])};
+                const h2 n23 = {(_Float16)fmaf(one, u[2], (float)s23[0]),
+                                (_Float16)fmaf(one, u[3], (float)s23[1])};
                 const v2u out = {fires ? as_u32(n01) : sp.x, fires ? as_u32(n23) : sp.y};
                 __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
             }
