@@ -103,9 +103,10 @@ def measured_traffic(wl, selector: str):
     return float(rec["traffic_bytes_per_launch"])
 
 
-def cpu_baseline(wl, seconds_hint=10.0):
+def cpu_baseline(wl, seconds_hint=10.0, max_steps=200):
     """Time the CPU oracle on a crop of the finest level (random state, the
-    workload's level-0 weights), a few NCA steps."""
+    workload's level-0 weights): consecutive NCA steps until about
+    `seconds_hint` seconds of CPU work (at least 4 steps, at most max_steps)."""
     import numpy as np
     import oracle
     from synthetic import make_weights, storage_dtype
@@ -119,13 +120,14 @@ def cpu_baseline(wl, seconds_hint=10.0):
         shape = (1, 512, 1024)
     else:
         shape = (16, 128, 256)
-    steps = 4
     dt = storage_dtype(wl)
     state = rng.normal(0, 1, shape + (wl.channels,)).astype(dt)
     w = make_weights(wl)[0]
+    steps = 0
     t0 = time.perf_counter()
-    for t in range(steps):
-        state = oracle.nca_step(state, w, wl.n_in, wl.ndim, 0, t, wl.seed, wl.fire_rate, dt)
+    while steps < max_steps and (steps < 4 or time.perf_counter() - t0 < seconds_hint):
+        state = oracle.nca_step(state, w, wl.n_in, wl.ndim, 0, steps, wl.seed, wl.fire_rate, dt)
+        steps += 1
     dt_s = time.perf_counter() - t0
     cells = shape[0] * shape[1] * shape[2]
     return {"value": cells * steps / dt_s, "unit": "cell-steps/s", "cores": int(threads),
