@@ -16,3 +16,5 @@ from .octree_nca import (pool, build_pyramid, init_state, upsample_inject, fire_
                          fire_bits, fire_mask, tap_offsets, perceive, update, nca_step,
                          run_level, readout, readout_classes, first_level_steps, infer,
                          infer_window, linear_index, to_storage, InferLog)
+from .train import (LevelGrads, step_vjp, level_states, level_vjp, upsample_vjp, Tape,
+                    train_forward, train_backward, readout_mse)
