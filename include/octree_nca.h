@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define OCTNCA_ABI_VERSION 2
+#define OCTNCA_ABI_VERSION 3
 
 typedef enum {
     OCTNCA_OK = 0,
@@ -239,6 +239,89 @@ int32_t octree_nca_first_level_steps(float alpha0, octnca_extent coarsest);
  * Errors: EINVAL, ESHAPE, EHIP. */
 int octree_nca_fire_mask(uint64_t seed, int32_t level, int32_t step, octnca_extent extent,
                          float fire_rate, uint8_t *mask, void *stream);
+
+/* ---------------------------------------------------------------------------
+ * Training gradients (fp32 states only).  The paper trains OctreeNCA end to
+ * end by backpropagation through every step of every level (Sec. 3.2,
+ * efficient training; supplement S7).  These calls give the gradient of a
+ * scalar loss with respect to each level's weights, recomputing a step's
+ * activations from its input state (only states are kept).  Other storage
+ * types return OCTNCA_EUNSUPPORTED.
+ * ------------------------------------------------------------------------- */
+
+/* One level's weight gradients, fp32, device memory, the layouts of
+ * octnca_level_weights. */
+typedef struct {
+    float *conv_w; /* [C][3^ndim] */
+    float *conv_b; /* [C] */
+    float *w1;     /* [H][2C] */
+    float *b1;     /* [H] */
+    float *w2;     /* [C][H]; rows c < n_in receive 0 */
+} octnca_level_grads;
+
+/* Bytes of workspace octree_nca_step_backward needs for `extent` (0 if the
+ * model or extent is invalid). */
+size_t octree_nca_step_backward_workspace_bytes(const octnca_model *model, octnca_extent extent);
+
+/* Backward of one NCA step (Sec. 3.1 step; supplement S3 Listing 1):
+ *   state      [extent][C] fp32, the state the step read (level `level`, step `step`);
+ *   grad_out   [extent][C] fp32, dL/dS' of the step's output;
+ *   grad_in    [extent][C] fp32, receives dL/dS of its input; may be grad_out itself
+ *              (in place), must not overlap state or workspace otherwise;
+ *   grads      the step's weight gradients are ADDED to these (zero them first);
+ *   fire_rate, seed, level, step  as for octree_nca_run_level (same fire mask).
+ * dL/dS = G' + [W1^T ga]_state + transposed depthwise conv of [W1^T ga]_perception,
+ * with ga = (W2^T m G'_hidden) * [W1 f + b1 > 0]; ReLU' is 0 at 0.
+ * Errors: EINVAL (null, aliasing, level/step < 0, fire rate), ESPACE, ESHAPE,
+ * EUNSUPPORTED (fp16), EHIP. */
+int octree_nca_step_backward(const octnca_model *model, const void *state, const void *grad_out,
+                             octnca_extent extent, const octnca_level_weights *weights,
+                             int32_t level, int32_t step, float fire_rate, uint64_t seed,
+                             void *grad_in, const octnca_level_grads *grads, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/* Adjoint of octree_nca_upsample (Sec. 3.2): grad_coarse[q][c] = sum of
+ * grad_fine over q's fz*fy*fx children for c >= n_in, 0 for c < n_in (the input
+ * channels are overwritten by the image).  grad_fine [coarse * factor][C],
+ * grad_coarse [coarse][C], fp32, not overlapping.  Errors: EINVAL, ESHAPE,
+ * EUNSUPPORTED, EHIP. */
+int octree_nca_upsample_backward(const octnca_model *model, const void *grad_fine,
+                                 octnca_extent coarse, const int32_t *factor, void *grad_coarse,
+                                 void *stream);
+
+/* Bytes of workspace octree_nca_readout_mse needs (0 for an invalid extent). */
+size_t octree_nca_readout_mse_workspace_bytes(octnca_extent extent);
+
+/* Synthetic training loss on the readout channels (the last two, Sec. 3.2):
+ *   L = 1/2 sum over cells and k in {0, 1} of (state[p][C-2+k] - target[p][k])^2.
+ *   target [extent][2] fp32; grad [extent][C] fp32 receives dL/dS (zero in the
+ *   other channels); *loss (device double) receives L, summed in fp64.
+ * Errors: EINVAL, ESPACE, ESHAPE, EUNSUPPORTED, EHIP. */
+int octree_nca_readout_mse(const octnca_model *model, const void *state, const float *target,
+                           octnca_extent extent, void *grad, double *loss, void *workspace,
+                           size_t workspace_bytes, void *stream);
+
+/* Bytes of workspace octree_nca_train_step needs: pyramid images, every state
+ * of every level, two finest-size gradients and the step-backward workspace
+ * (0 if an argument is invalid). */
+size_t octree_nca_train_workspace_bytes(const octnca_model *model, octnca_extent finest,
+                                        int32_t levels, const int32_t *factors,
+                                        const int32_t *steps);
+
+/* One fused training step: the inference of octree_nca_infer (same arguments,
+ * fp32 MLP operands) keeping every state, the readout MSE against `target`,
+ * and the backward through all steps and levels (finest first, the upsample's
+ * adjoint between levels).
+ *   grads   host array of `levels` gradient sets (index = level), OVERWRITTEN;
+ *   loss    device double, receives L;
+ *   final_state  [finest][C] fp32 or NULL: receives the forward's final state.
+ * Errors: EINVAL, ESPACE, ESHAPE, EUNSUPPORTED (fp16), EHIP. */
+int octree_nca_train_step(const octnca_model *model, const void *image, octnca_extent finest,
+                          int32_t levels, const int32_t *factors,
+                          const octnca_level_weights *weights, const int32_t *steps,
+                          float fire_rate, uint64_t seed, const float *target, void *workspace,
+                          size_t workspace_bytes, const octnca_level_grads *grads, double *loss,
+                          void *final_state, void *stream);
 
 /* Static text for a status code; never NULL. */
 const char *octree_nca_strerror(int status);

@@ -23,7 +23,12 @@ __all__ = [
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
     "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
-    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL", "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
+    "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
+    "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
+    "octree_nca_upsample_backward", "octree_nca_readout_mse_workspace_bytes",
+    "octree_nca_readout_mse", "octree_nca_train_workspace_bytes", "octree_nca_train_step",
+    "level_grads_struct", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL",
+    "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
     "OCTNCA_EHIP", "OCTNCA_ESPACE", "OCTNCA_F32", "OCTNCA_F16",
 ]
 
@@ -36,6 +41,9 @@ EXPORTED_SYMBOLS = (
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
     "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
     "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
+    "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
+    "octree_nca_upsample_backward", "octree_nca_readout_mse_workspace_bytes",
+    "octree_nca_readout_mse", "octree_nca_train_workspace_bytes", "octree_nca_train_step",
 )
 
 
@@ -56,6 +64,11 @@ class _Extent(ctypes.Structure):
 
 
 class _LevelWeights(ctypes.Structure):
+    _fields_ = [("conv_w", ctypes.c_void_p), ("conv_b", ctypes.c_void_p),
+                ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p)]
+
+
+class _LevelGrads(ctypes.Structure):
     _fields_ = [("conv_w", ctypes.c_void_p), ("conv_b", ctypes.c_void_p),
                 ("w1", ctypes.c_void_p), ("b1", ctypes.c_void_p), ("w2", ctypes.c_void_p)]
 
@@ -85,6 +98,25 @@ _SIGS = {
     "octree_nca_fire_mask": (_I32, [ctypes.c_uint64, _I32, _I32, _Extent, ctypes.c_float, _P,
                                     _P]),
     "octree_nca_first_level_steps": (_I32, [ctypes.c_float, _Extent]),
+    "octree_nca_step_backward_workspace_bytes": (ctypes.c_size_t,
+                                                 [ctypes.POINTER(_Model), _Extent]),
+    "octree_nca_step_backward": (_I32, [ctypes.POINTER(_Model), _P, _P, _Extent,
+                                        ctypes.POINTER(_LevelWeights), _I32, _I32,
+                                        ctypes.c_float, ctypes.c_uint64, _P,
+                                        ctypes.POINTER(_LevelGrads), _P, ctypes.c_size_t, _P]),
+    "octree_nca_upsample_backward": (_I32, [ctypes.POINTER(_Model), _P, _Extent,
+                                            ctypes.POINTER(_I32), _P, _P]),
+    "octree_nca_readout_mse_workspace_bytes": (ctypes.c_size_t, [_Extent]),
+    "octree_nca_readout_mse": (_I32, [ctypes.POINTER(_Model), _P, _P, _Extent, _P, _P, _P,
+                                      ctypes.c_size_t, _P]),
+    "octree_nca_train_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(_Model), _Extent, _I32,
+                                                           ctypes.POINTER(_I32),
+                                                           ctypes.POINTER(_I32)]),
+    "octree_nca_train_step": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32,
+                                     ctypes.POINTER(_I32), ctypes.POINTER(_LevelWeights),
+                                     ctypes.POINTER(_I32), ctypes.c_float, ctypes.c_uint64, _P,
+                                     _P, ctypes.c_size_t, ctypes.POINTER(_LevelGrads), _P, _P,
+                                     _P]),
     "octree_nca_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "octree_nca_abi_version": (ctypes.c_int, []),
 }
@@ -315,3 +347,93 @@ def octree_nca_fire_mask(seed: int, level: int, step: int, extent, fire_rate: fl
                                     float(fire_rate), _ptr(mask, torch.uint8, "mask"),
                                     _stream(stream))
     _check(st, "octree_nca_fire_mask")
+
+
+# ---------------------------------------------------------------------------
+# training gradients (fp32 states)
+# ---------------------------------------------------------------------------
+
+def level_grads_struct(g) -> _LevelGrads:
+    """``g`` has device fp32 tensors conv_w, conv_b, w1, b1, w2 shaped like the
+    weights (attributes or a dict); the library writes into them."""
+    get = (lambda k: g[k]) if isinstance(g, dict) else (lambda k: getattr(g, k))
+    return _LevelGrads(*(_ptr(get(k), torch.float32, k) for k in
+                         ("conv_w", "conv_b", "w1", "b1", "w2")))
+
+
+def octree_nca_step_backward_workspace_bytes(model: Model, extent) -> int:
+    return int(lib().octree_nca_step_backward_workspace_bytes(ctypes.byref(model.struct()),
+                                                              _extent(extent)))
+
+
+def octree_nca_step_backward(model: Model, state, grad_out, weights, level: int, step: int,
+                             fire_rate: float, seed: int, grad_in, grads, workspace,
+                             stream=None) -> None:
+    """Backward of one step: grad_in <- dL/dS, grads += the weight gradients."""
+    d, h, w = state.shape[:3]
+    st = lib().octree_nca_step_backward(
+        ctypes.byref(model.struct()), _ptr(state, torch.float32, "state"),
+        _ptr(grad_out, torch.float32, "grad_out"), _extent((d, h, w)),
+        ctypes.byref(level_weights_struct(weights)), int(level), int(step), float(fire_rate),
+        int(seed), _ptr(grad_in, torch.float32, "grad_in"), ctypes.byref(level_grads_struct(grads)),
+        _ptr(workspace, None, "workspace"), workspace.numel() * workspace.element_size(),
+        _stream(stream))
+    _check(st, "octree_nca_step_backward")
+
+
+def octree_nca_upsample_backward(model: Model, grad_fine, factor, grad_coarse,
+                                 stream=None) -> None:
+    d, h, w = grad_coarse.shape[:3]
+    f = (_I32 * 3)(*[int(v) for v in factor])
+    st = lib().octree_nca_upsample_backward(ctypes.byref(model.struct()),
+                                            _ptr(grad_fine, torch.float32, "grad_fine"),
+                                            _extent((d, h, w)), f,
+                                            _ptr(grad_coarse, torch.float32, "grad_coarse"),
+                                            _stream(stream))
+    _check(st, "octree_nca_upsample_backward")
+
+
+def octree_nca_readout_mse_workspace_bytes(extent) -> int:
+    return int(lib().octree_nca_readout_mse_workspace_bytes(_extent(extent)))
+
+
+def octree_nca_readout_mse(model: Model, state, target, grad, loss, workspace,
+                           stream=None) -> None:
+    """loss: device float64 tensor of one element."""
+    d, h, w = state.shape[:3]
+    st = lib().octree_nca_readout_mse(ctypes.byref(model.struct()),
+                                      _ptr(state, torch.float32, "state"),
+                                      _ptr(target, torch.float32, "target"), _extent((d, h, w)),
+                                      _ptr(grad, torch.float32, "grad"),
+                                      _ptr(loss, torch.float64, "loss"),
+                                      _ptr(workspace, None, "workspace"),
+                                      workspace.numel() * workspace.element_size(),
+                                      _stream(stream))
+    _check(st, "octree_nca_readout_mse")
+
+
+def octree_nca_train_workspace_bytes(model: Model, finest, factors, steps) -> int:
+    levels = len(steps)
+    s = (_I32 * levels)(*[int(v) for v in steps])
+    return int(lib().octree_nca_train_workspace_bytes(ctypes.byref(model.struct()),
+                                                      _extent(finest), levels, _factors(factors),
+                                                      s))
+
+
+def octree_nca_train_step(model: Model, image, factors, weights, steps, fire_rate: float,
+                          seed: int, target, workspace, grads, loss, final_state=None,
+                          stream=None) -> None:
+    """One training step; ``grads`` is a list (index = level) of gradient sets,
+    overwritten; ``loss`` a device float64 tensor of one element."""
+    levels = len(steps)
+    d, h, w = image.shape[:3]
+    ws = (_LevelWeights * levels)(*[level_weights_struct(x) for x in weights])
+    gs = (_LevelGrads * levels)(*[level_grads_struct(x) for x in grads])
+    s = (_I32 * levels)(*[int(v) for v in steps])
+    st = lib().octree_nca_train_step(
+        ctypes.byref(model.struct()), _ptr(image, torch.float32, "image"), _extent((d, h, w)),
+        levels, _factors(factors), ws, s, float(fire_rate), int(seed),
+        _ptr(target, torch.float32, "target"), _ptr(workspace, None, "workspace"),
+        workspace.numel() * workspace.element_size(), gs, _ptr(loss, torch.float64, "loss"),
+        _ptr(final_state, torch.float32, "final_state"), _stream(stream))
+    _check(st, "octree_nca_train_step")

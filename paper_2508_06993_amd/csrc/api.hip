@@ -9,6 +9,7 @@
 
 #include <cmath>
 #include <algorithm>
+#include <utility>
 #include "launch.h"
 #include "octree_nca.h"
 
@@ -463,12 +464,262 @@ int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_
     return OCTNCA_OK;
 }
 
+// ---------------------------------------------------------------------------
+// Training (fp32 states): backward of a step, of the upsample, a readout MSE
+// and the whole training step (Sec. 3.2 efficient training; supplement S7).
+// ---------------------------------------------------------------------------
+
+size_t octree_nca_step_backward_workspace_bytes(const octnca_model *model, octnca_extent extent) {
+    if (check_model(model) || check_extent(model, extent)) return 0;
+    return step_backward_workspace_floats(model->ndim, model->channels, model->hidden,
+                                          extent.d * extent.h * extent.w) *
+           sizeof(float);
+}
+
+int octree_nca_step_backward(const octnca_model *model, const void *state, const void *grad_out,
+                             octnca_extent extent, const octnca_level_weights *weights,
+                             int32_t level, int32_t step, float fire_rate, uint64_t seed,
+                             void *grad_in, const octnca_level_grads *grads, void *workspace,
+                             size_t workspace_bytes, void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if (model->state_dtype != OCTNCA_F32) return OCTNCA_EUNSUPPORTED;
+    if ((st = check_extent(model, extent))) return st;
+    uint64_t threshold;
+    if (state == nullptr || grad_out == nullptr || grad_in == nullptr || workspace == nullptr ||
+        !weights_ok(weights) || grads == nullptr || !grads->conv_w || !grads->conv_b ||
+        !grads->w1 || !grads->b1 || !grads->w2 || level < 0 || step < 0 ||
+        !fire_threshold(fire_rate, &threshold))
+        return OCTNCA_EINVAL;
+    const size_t need = octree_nca_step_backward_workspace_bytes(model, extent);
+    if (workspace_bytes < need) return OCTNCA_ESPACE;
+    const size_t bytes = (size_t)(extent.d * extent.h * extent.w) * model->channels * sizeof(float);
+    if (overlap(grad_in, bytes, state, bytes) || overlap(workspace, need, state, bytes) ||
+        overlap(workspace, need, grad_in, bytes) || overlap(workspace, need, grad_out, bytes))
+        return OCTNCA_EINVAL;
+    if (grad_in != grad_out && overlap(grad_in, bytes, grad_out, bytes)) return OCTNCA_EINVAL;
+    StepArgs a = step_args(model, extent, weights, level, seed, threshold, 0);
+    a.step = (uint32_t)step;
+    const LevelGradsDev g{grads->conv_w, grads->conv_b, grads->w1, grads->b1, grads->w2};
+    return hip_status(launch_step_backward(a, (const float *)state, (const float *)grad_out,
+                                           (float *)grad_in, g, (float *)workspace,
+                                           (hipStream_t)stream));
+}
+
+int octree_nca_upsample_backward(const octnca_model *model, const void *grad_fine,
+                                 octnca_extent coarse, const int32_t *factor, void *grad_coarse,
+                                 void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if (model->state_dtype != OCTNCA_F32) return OCTNCA_EUNSUPPORTED;
+    if (grad_fine == nullptr || grad_coarse == nullptr || factor == nullptr) return OCTNCA_EINVAL;
+    if ((st = check_extent(model, coarse)) || (st = check_factor(model, factor))) return st;
+    const octnca_extent fine{coarse.d * factor[0], coarse.h * factor[1], coarse.w * factor[2]};
+    if ((st = check_extent(model, fine))) return st;
+    if (overlap(grad_coarse, (size_t)(coarse.d * coarse.h * coarse.w) * model->channels * 4,
+                grad_fine, (size_t)(fine.d * fine.h * fine.w) * model->channels * 4))
+        return OCTNCA_EINVAL;
+    return hip_status(launch_upsample_adjoint((const float *)grad_fine, ext3(coarse), factor[0],
+                                              factor[1], factor[2], model->n_in, model->channels,
+                                              (float *)grad_coarse, (hipStream_t)stream));
+}
+
+size_t octree_nca_readout_mse_workspace_bytes(octnca_extent extent) {
+    if (extent.d <= 0 || extent.h <= 0 || extent.w <= 0) return 0;
+    return mse_workspace_doubles(extent.d * extent.h * extent.w) * sizeof(double);
+}
+
+int octree_nca_readout_mse(const octnca_model *model, const void *state, const float *target,
+                           octnca_extent extent, void *grad, double *loss, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    int st = check_model(model);
+    if (st) return st;
+    if (model->state_dtype != OCTNCA_F32) return OCTNCA_EUNSUPPORTED;
+    if ((st = check_extent(model, extent))) return st;
+    if (state == nullptr || target == nullptr || grad == nullptr || loss == nullptr ||
+        workspace == nullptr)
+        return OCTNCA_EINVAL;
+    const int64_t cells = extent.d * extent.h * extent.w;
+    if (workspace_bytes < octree_nca_readout_mse_workspace_bytes(extent)) return OCTNCA_ESPACE;
+    const size_t bytes = (size_t)cells * model->channels * sizeof(float);
+    if (overlap(grad, bytes, state, bytes) || overlap(grad, bytes, target, (size_t)cells * 8) ||
+        overlap(workspace, workspace_bytes, grad, bytes))
+        return OCTNCA_EINVAL;
+    return hip_status(launch_readout_mse((const float *)state, target, cells, model->channels,
+                                         (float *)grad, loss, (double *)workspace,
+                                         (hipStream_t)stream));
+}
+
+}  // extern "C"
+
+namespace {
+
+// Workspace of a training step: pyramid images 1..L-1, the states of every
+// level (before each step and after the last), two finest-size gradient
+// buffers, the step-backward workspace (finest size) and the loss partials.
+struct TrainPlan {
+    octnca_extent ext[kMaxLevels];
+    size_t image_off[kMaxLevels];
+    size_t tape_off[kMaxLevels];    // state t of level l at tape_off[l] + t * state bytes of l
+    size_t grad_off[2], bwd_off, mse_off, bytes;
+};
+
+int make_train_plan(const octnca_model *m, octnca_extent finest, int32_t levels,
+                    const int32_t *factors, const int32_t *steps, TrainPlan *p) {
+    int st = check_model(m);
+    if (st) return st;
+    if (m->state_dtype != OCTNCA_F32) return OCTNCA_EUNSUPPORTED;
+    if ((st = level_extents(m, finest, levels, factors, p->ext))) return st;
+    if (steps == nullptr) return OCTNCA_EINVAL;
+    for (int l = 0; l < levels; ++l)
+        if (steps[l] < 0) return OCTNCA_EINVAL;
+    size_t off = 0;
+    p->image_off[0] = 0;
+    for (int l = 1; l < levels; ++l) {
+        p->image_off[l] = off;
+        off += align_up((size_t)(p->ext[l].d * p->ext[l].h * p->ext[l].w) * m->n_in * 4);
+    }
+    for (int l = 0; l < levels; ++l) {
+        p->tape_off[l] = off;
+        const size_t sb = (size_t)(p->ext[l].d * p->ext[l].h * p->ext[l].w) * m->channels * 4;
+        off += align_up(sb * ((size_t)steps[l] + 1));
+    }
+    const int64_t cells = finest.d * finest.h * finest.w;
+    const size_t gb = align_up((size_t)cells * m->channels * 4);
+    p->grad_off[0] = off;
+    off += gb;
+    p->grad_off[1] = off;
+    off += gb;
+    p->bwd_off = off;
+    off += align_up(step_backward_workspace_floats(m->ndim, m->channels, m->hidden, cells) * 4);
+    p->mse_off = off;
+    off += align_up(mse_workspace_doubles(cells) * sizeof(double));
+    p->bytes = off;
+    return OCTNCA_OK;
+}
+
+// Forward step of a training pass: exact fp32 MLP operands (the matrix-core
+// kernel for C = 16, H = 64, the vector kernel otherwise).
+hipError_t train_forward_step(const StepArgs &a, const void *src, void *dst, hipStream_t s) {
+    if (a.channels == kC && a.hidden == kH)
+        return launch_step_mfma(a, MfmaMlp::F32, Layout2d::Auto, src, dst, s);
+    return launch_step_valu(a, src, dst, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t octree_nca_train_workspace_bytes(const octnca_model *model, octnca_extent finest,
+                                        int32_t levels, const int32_t *factors,
+                                        const int32_t *steps) {
+    TrainPlan p;
+    return make_train_plan(model, finest, levels, factors, steps, &p) ? 0 : p.bytes;
+}
+
+int octree_nca_train_step(const octnca_model *model, const void *image, octnca_extent finest,
+                          int32_t levels, const int32_t *factors,
+                          const octnca_level_weights *weights, const int32_t *steps,
+                          float fire_rate, uint64_t seed, const float *target, void *workspace,
+                          size_t workspace_bytes, const octnca_level_grads *grads, double *loss,
+                          void *final_state, void *stream) {
+    TrainPlan p;
+    int st = make_train_plan(model, finest, levels, factors, steps, &p);
+    if (st) return st;
+    uint64_t threshold;
+    if (image == nullptr || weights == nullptr || target == nullptr || workspace == nullptr ||
+        grads == nullptr || loss == nullptr || !fire_threshold(fire_rate, &threshold))
+        return OCTNCA_EINVAL;
+    for (int l = 0; l < levels; ++l)
+        if (!weights_ok(&weights[l]) || !grads[l].conv_w || !grads[l].conv_b || !grads[l].w1 ||
+            !grads[l].b1 || !grads[l].w2)
+            return OCTNCA_EINVAL;
+    if (workspace_bytes < p.bytes) return OCTNCA_ESPACE;
+    const int64_t cells = finest.d * finest.h * finest.w;
+    const size_t state_bytes = (size_t)cells * model->channels * 4;
+    if (overlap(workspace, p.bytes, image, (size_t)cells * model->n_in * 4) ||
+        overlap(workspace, p.bytes, target, (size_t)cells * 8) ||
+        (final_state && overlap(workspace, p.bytes, final_state, state_bytes)))
+        return OCTNCA_EINVAL;
+
+    const hipStream_t s = (hipStream_t)stream;
+    char *ws = (char *)workspace;
+    auto img = [&](int l) { return l == 0 ? image : (const void *)(ws + p.image_off[l]); };
+    auto cells_of = [&](int l) { return p.ext[l].d * p.ext[l].h * p.ext[l].w; };
+    auto tape = [&](int l, int t) {
+        return (float *)(ws + p.tape_off[l]) + (size_t)t * cells_of(l) * model->channels;
+    };
+    auto ok = [](hipError_t e) { return e == hipSuccess; };
+
+    // forward, keeping every state
+    for (int l = 1; l < levels; ++l) {
+        const int32_t *f = factors + 3 * (l - 1);
+        if (!ok(launch_pool(Dtype::F32, img(l - 1), ext3(p.ext[l]), ws + p.image_off[l], f[0],
+                            f[1], f[2], model->n_in, s)))
+            return OCTNCA_EHIP;
+    }
+    for (int l = levels - 1; l >= 0; --l) {
+        const hipError_t e =
+            l == levels - 1
+                ? launch_upsample(Dtype::F32, nullptr, ext3(p.ext[l]), 1, 1, 1, img(l), tape(l, 0),
+                                  model->n_in, model->channels, s)
+                : launch_upsample(Dtype::F32, tape(l + 1, steps[l + 1]), ext3(p.ext[l]),
+                                  factors[3 * l], factors[3 * l + 1], factors[3 * l + 2], img(l),
+                                  tape(l, 0), model->n_in, model->channels, s);
+        if (!ok(e)) return OCTNCA_EHIP;
+        StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, 0);
+        for (int t = 0; t < steps[l]; ++t) {
+            a.step = (uint32_t)t;
+            if (!ok(train_forward_step(a, tape(l, t), tape(l, t + 1), s))) return OCTNCA_EHIP;
+        }
+    }
+    const float *final_fine = tape(0, steps[0]);
+    float *g = (float *)(ws + p.grad_off[0]);
+    float *g_other = (float *)(ws + p.grad_off[1]);
+    if (!ok(launch_readout_mse(final_fine, target, cells, model->channels, g, loss,
+                               (double *)(ws + p.mse_off), s)))
+        return OCTNCA_EHIP;
+    if (final_state &&
+        !ok(hipMemcpyAsync(final_state, final_fine, state_bytes, hipMemcpyDeviceToDevice, s)))
+        return OCTNCA_EHIP;
+
+    // backward, finest level first
+    const int taps = model->ndim == 3 ? 27 : 9;
+    for (int l = 0; l < levels; ++l) {
+        const int64_t c = model->channels, h = model->hidden;
+        const octnca_level_grads &gr = grads[l];
+        if (!ok(launch_fill_zero(gr.conv_w, c * taps, s)) || !ok(launch_fill_zero(gr.conv_b, c, s)) ||
+            !ok(launch_fill_zero(gr.w1, h * 2 * c, s)) || !ok(launch_fill_zero(gr.b1, h, s)) ||
+            !ok(launch_fill_zero(gr.w2, c * h, s)))
+            return OCTNCA_EHIP;
+    }
+    for (int l = 0; l < levels; ++l) {
+        StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, 0);
+        const LevelGradsDev gd{grads[l].conv_w, grads[l].conv_b, grads[l].w1, grads[l].b1,
+                               grads[l].w2};
+        for (int t = steps[l] - 1; t >= 0; --t) {
+            a.step = (uint32_t)t;
+            if (!ok(launch_step_backward(a, tape(l, t), g, g, gd, (float *)(ws + p.bwd_off), s)))
+                return OCTNCA_EHIP;
+        }
+        if (l + 1 < levels) {
+            if (!ok(launch_upsample_adjoint(g, ext3(p.ext[l + 1]), factors[3 * l],
+                                            factors[3 * l + 1], factors[3 * l + 2], model->n_in,
+                                            model->channels, g_other, s)))
+                return OCTNCA_EHIP;
+            std::swap(g, g_other);
+        }
+    }
+    return OCTNCA_OK;
+}
+
 }  // extern "C"
 
 namespace octnca {
 // Step kernel selection, read at every launch from OCTREE_NCA_STEP_KERNEL:
-//   unset / "mfma"  matrix-core kernel, MLP operands split bf16 (x3) for fp32
-//                   states and fp16 for fp16 states;
+//   unset / "mfma"  matrix-core kernel, MLP operands scaled fp16 activations x
+//                   split fp16 weights for fp32 states and fp16 for fp16 states;
+//   "mfma_f16s"     the fp32-state default MLP operands, named;
 //   "mfma_f32"      matrix-core kernel with fp32 MLP operands;
 //   "mfma_bf16x3"   matrix-core kernel with split bf16 operands (any storage);
 //   "mfma_f16"      matrix-core kernel with fp16 operands (fp16 states only);

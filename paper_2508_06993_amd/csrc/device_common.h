@@ -127,4 +127,13 @@ struct LevelWeightsDev {
     const float *w2;       // [C][H]
 };
 
+// Gradients of one level's weights (same layouts), accumulated by the backward.
+struct LevelGradsDev {
+    float *conv_w;
+    float *conv_b;
+    float *w1;
+    float *b1;
+    float *w2;
+};
+
 }  // namespace octnca

@@ -56,6 +56,22 @@ hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, i
                           int fz, int fy, int fx, const void *img, void *dst,
                           hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+
+// Training (fp32 states): backward of one step (state `src` before the step,
+// gout = dL/dS'), writing gin = dL/dS (may alias gout) and adding the weight
+// gradients to g; ws holds step_backward_workspace_floats floats.
+size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_t cells);
+hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,
+                                float *gin, LevelGradsDev g, float *ws, hipStream_t stream);
+// Adjoint of the upsample + inject from `coarse` (extent of the coarse level).
+hipError_t launch_upsample_adjoint(const float *gfine, Extent3 coarse, int fz, int fy, int fx,
+                                   int n_in, int channels, float *gcoarse, hipStream_t stream);
+// Readout-channel MSE: grad = dL/dS, *loss = L (device); ws holds
+// mse_workspace_doubles doubles.
+size_t mse_workspace_doubles(int64_t cells);
+hipError_t launch_readout_mse(const float *state, const float *target, int64_t cells, int channels,
+                              float *grad, double *loss, double *ws, hipStream_t stream);
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t stream);
 // MLP operand precision of the MFMA step kernel.  Default: scaled fp16
 // activations with split fp16 weights (F16S) for fp32 states, fp16 for fp16 states.
 enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3, F16S = 4 };

@@ -1,0 +1,403 @@
+// Training gradients of OctreeNCA (Sec. 3.2, efficient training; supplement
+// S7): the backward of one NCA step for fp32 states, the adjoint of the
+// upsample + inject, and a readout-channel MSE as the synthetic loss.
+//
+// One step S -> S' = S + m * u (hidden channels, Sec. 3.1) is taken back,
+// for G' = dL/dS', by recomputing its activations from S (nothing of the
+// forward but the states is kept):
+//   gu = m G' (hidden channels), dW2 += gu h^T, ga = (W2^T gu) * [a > 0],
+//   dW1 += ga f^T, db1 += ga, [gS, gP] = W1^T ga, dconv_b += gP,
+//   dK[c][t] += gP[p][c] S[p + o_t][c], dL/dS = G' + gS + conv^T(gP).
+// Four launches:
+//   1. bwd_cell: one thread per cell (halo tile of S in LDS, as the vector
+//      step kernel): perception, then the 64 hidden units streamed once,
+//      each giving a, h, gh and ga; writes G' + gS and the cell's record
+//      [f | h | ga | gu | gP] for the weight gradients;
+//   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
+//      gP (halo tile of gP in LDS);
+//   3. wgrad_partials: per chunk of 32 consecutive cells, the chunk's sums of
+//      every weight-gradient entry (records staged in LDS);
+//   4. wgrad_reduce: the chunk sums added in chunk order, in fp64, to the
+//      caller's gradients (accumulated, so the steps of a level sum up).
+#include "launch.h"
+
+namespace octnca {
+
+namespace {
+
+constexpr int kBwdThreads = 256;
+constexpr int kChunk = 32;   // cells per weight-gradient partial sum
+
+template <int NDIM> struct BwdTile;
+template <> struct BwdTile<2> { static constexpr int TZ = 1, TY = 8, TX = 32; };
+template <> struct BwdTile<3> { static constexpr int TZ = 4, TY = 8, TX = 8; };
+
+// Record of a cell: f (2C) | h (H) | ga (H) | gu (C) | gP (C), stored field
+// by field (entry k of cell p at rec[k * cells + p]) so that neighbouring
+// cells' entries are neighbouring words.
+template <int C, int H> struct Rec {
+    static constexpr int F = 0, Hh = 2 * C, GA = 2 * C + H, GU = 2 * C + 2 * H,
+                         GP = 3 * C + 2 * H, N = 4 * C + 2 * H;
+};
+
+// Number of weight-gradient entries: dW1 (H x 2C), dW2 (C x H), db1 (H),
+// dconv_b (C), dconv_w (C x taps), in that order.
+template <int C, int H, int TAPS> struct WG {
+    static constexpr int W1 = 0, W2 = 2 * C * H, B1 = 3 * C * H, CB = 3 * C * H + H,
+                         CW = 3 * C * H + H + C, N = 3 * C * H + H + C + C * TAPS;
+};
+
+template <int NDIM, int NIN, int C, int H>
+__global__ __launch_bounds__(kBwdThreads) void bwd_cell(
+    const float *__restrict__ src, const float *__restrict__ gout, int dd, int dh, int dw,
+    int tiles_x, int tiles_y, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
+    const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
+    float *__restrict__ gpart, float *__restrict__ rec, int64_t cells) {
+    using T = BwdTile<NDIM>;
+    using R = Rec<C, H>;
+    constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
+    constexpr int NCELL = HZ * HY * HX;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    static_assert(T::TZ * T::TY * T::TX == kBwdThreads, "one thread per tile cell");
+    __shared__ float tile[C][NCELL];   // channel-major: neighbouring threads, neighbouring words
+
+    int b = blockIdx.x;
+    const int bx = b % tiles_x;
+    b /= tiles_x;
+    const int by = b % tiles_y;
+    const int bz = b / tiles_y;
+    const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
+    for (int i = threadIdx.x; i < NCELL * C; i += kBwdThreads) {
+        const int c = i / NCELL, cell = i % NCELL;
+        const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+        const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+        float v = 0.f;
+        if (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
+            v = src[(((int64_t)gz * dh + gy) * dw + gx) * C + c];
+        tile[c][cell] = v;
+    }
+    __syncthreads();
+
+    const int tx = threadIdx.x % T::TX, ty = (threadIdx.x / T::TX) % T::TY,
+              tz = threadIdx.x / (T::TX * T::TY);
+    const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
+    if (x >= dw || y >= dh || z >= dd) return;
+    const int centre = ((tz + (NDIM == 3 ? 1 : 0)) * HY + ty + 1) * HX + tx + 1;
+    const int64_t idx = ((int64_t)z * dh + y) * dw + x;
+
+    float f[2 * C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        f[c] = tile[c][centre];
+        f[C + c] = conv_b[c];
+    }
+#pragma unroll 1
+    for (int t = 0; t < TAPS; ++t) {
+        const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+        const int nb = centre + (dz * HY + dy) * HX + dx;
+#pragma unroll
+        for (int c = 0; c < C; ++c) f[C + c] = fmaf(conv_w[c * TAPS + t], tile[c][nb], f[C + c]);
+    }
+    const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
+    const float *g = gout + idx * C;
+    float gu[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) gu[c] = (c >= NIN && fire) ? g[c] : 0.f;
+
+    float *r = rec + idx;   // entry k at r[k * cells]
+    float gf[2 * C];
+#pragma unroll
+    for (int k = 0; k < 2 * C; ++k) gf[k] = 0.f;
+#pragma unroll 2
+    for (int j = 0; j < H; ++j) {
+        float a = b1[j];
+#pragma unroll
+        for (int k = 0; k < 2 * C; ++k) a = fmaf(w1[j * 2 * C + k], f[k], a);
+        float gh = 0.f;
+#pragma unroll
+        for (int c = NIN; c < C; ++c) gh = fmaf(w2[c * H + j], gu[c], gh);
+        const float ga = a > 0.f ? gh : 0.f;
+#pragma unroll
+        for (int k = 0; k < 2 * C; ++k) gf[k] = fmaf(w1[j * 2 * C + k], ga, gf[k]);
+        r[(R::Hh + j) * cells] = fmaxf(a, 0.f);
+        r[(R::GA + j) * cells] = ga;
+    }
+#pragma unroll
+    for (int k = 0; k < 2 * C; ++k) r[(R::F + k) * cells] = f[k];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        r[(R::GU + c) * cells] = gu[c];
+        r[(R::GP + c) * cells] = gf[C + c];
+        gpart[idx * C + c] = g[c] + gf[c];
+    }
+}
+
+template <int NDIM, int C, int H>
+__global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
+    const float *__restrict__ gpart, const float *__restrict__ rec, int dd, int dh, int dw,
+    int tiles_x, int tiles_y, const float *__restrict__ conv_w, float *__restrict__ gin,
+    int64_t cells) {
+    using T = BwdTile<NDIM>;
+    using R = Rec<C, H>;
+    constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
+    constexpr int NCELL = HZ * HY * HX;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    __shared__ float tile[C][NCELL];   // gP of the tile and its halo
+
+    int b = blockIdx.x;
+    const int bx = b % tiles_x;
+    b /= tiles_x;
+    const int by = b % tiles_y;
+    const int bz = b / tiles_y;
+    const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
+    for (int i = threadIdx.x; i < NCELL * C; i += kBwdThreads) {
+        const int c = i / NCELL, cell = i % NCELL;
+        const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+        const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+        float v = 0.f;
+        if (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
+            v = rec[(R::GP + c) * cells + ((int64_t)gz * dh + gy) * dw + gx];
+        tile[c][cell] = v;
+    }
+    __syncthreads();
+
+    const int tx = threadIdx.x % T::TX, ty = (threadIdx.x / T::TX) % T::TY,
+              tz = threadIdx.x / (T::TX * T::TY);
+    const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
+    if (x >= dw || y >= dh || z >= dd) return;
+    const int centre = ((tz + (NDIM == 3 ? 1 : 0)) * HY + ty + 1) * HX + tx + 1;
+    const int64_t idx = ((int64_t)z * dh + y) * dw + x;
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        float v = gpart[idx * C + c];
+#pragma unroll
+        for (int t = 0; t < TAPS; ++t) {
+            // cell q receives K[c][t] gP[q - o_t]
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            v = fmaf(conv_w[c * TAPS + t], tile[c][centre - (dz * HY + dy) * HX - dx], v);
+        }
+        gin[idx * C + c] = v;
+    }
+}
+
+// Sums over the chunk's cells of every weight-gradient entry.
+template <int NDIM, int C, int H>
+__global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
+    const float *__restrict__ src, const float *__restrict__ rec, int dd, int dh, int dw,
+    int64_t cells, float *__restrict__ partial) {
+    using R = Rec<C, H>;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    using G = WG<C, H, TAPS>;
+    __shared__ float recs[R::N][kChunk + 1];   // [entry][cell]
+    const int64_t first = (int64_t)blockIdx.x * kChunk;
+    const int n = (int)min<int64_t>(kChunk, cells - first);
+    for (int i = threadIdx.x; i < kChunk * R::N; i += kBwdThreads) {
+        const int k = i / kChunk, cell = i % kChunk;
+        recs[k][cell] = cell < n ? rec[k * cells + first + cell] : 0.f;
+    }
+    __syncthreads();
+    float *out = partial + (int64_t)blockIdx.x * G::N;
+    for (int o = threadIdx.x; o < G::N; o += kBwdThreads) {
+        float s = 0.f;
+        if (o < G::W2) {                       // dW1[j][k] = sum ga[j] f[k]
+            const int j = o / (2 * C), k = o % (2 * C);
+            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
+        } else if (o < G::B1) {                // dW2[c][j] = sum gu[c] h[j]
+            const int c = (o - G::W2) / H, j = (o - G::W2) % H;
+            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
+        } else if (o < G::CB) {                // db1[j] = sum ga[j]
+            const int j = o - G::B1;
+            for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
+        } else if (o < G::CW) {                // dconv_b[c] = sum gP[c]
+            const int c = o - G::CB;
+            for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
+        } else {                               // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
+            const int c = (o - G::CW) / TAPS, t = (o - G::CW) % TAPS;
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            for (int i = 0; i < n; ++i) {
+                const int64_t p = first + i;
+                const int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
+                const int gx = x + dx, gy = y + dy, gz = z + dz;
+                const float sv = (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
+                                     ? src[(((int64_t)gz * dh + gy) * dw + gx) * C + c]
+                                     : 0.f;
+                s = fmaf(recs[R::GP + c][i], sv, s);
+            }
+        }
+        out[o] = s;
+    }
+}
+
+// grads += sum over chunks (in chunk order, fp64) of the partial sums.
+template <int C, int H, int TAPS>
+__global__ __launch_bounds__(kBwdThreads) void wgrad_reduce(const float *__restrict__ partial,
+                                                            int64_t chunks, LevelGradsDev g) {
+    using G = WG<C, H, TAPS>;
+    const int o = blockIdx.x * kBwdThreads + threadIdx.x;
+    if (o >= G::N) return;
+    double s = 0.0;
+    for (int64_t b = 0; b < chunks; ++b) s += (double)partial[b * G::N + o];
+    float *dst;
+    if (o < G::W2) dst = g.w1 + o;
+    else if (o < G::B1) dst = g.w2 + (o - G::W2);
+    else if (o < G::CB) dst = g.b1 + (o - G::B1);
+    else if (o < G::CW) dst = g.conv_b + (o - G::CB);
+    else dst = g.conv_w + (o - G::CW);
+    *dst = (float)((double)*dst + s);
+}
+
+template <int NDIM, int NIN, int C, int H>
+hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, float *gin,
+                      LevelGradsDev g, float *ws, hipStream_t stream) {
+    using T = BwdTile<NDIM>;
+    using R = Rec<C, H>;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    using G = WG<C, H, TAPS>;
+    const int64_t cells = a.ext.cells();
+    const int tiles_x = (int)((a.ext.w + T::TX - 1) / T::TX);
+    const int tiles_y = (int)((a.ext.h + T::TY - 1) / T::TY);
+    const int tiles_z = (int)((a.ext.d + T::TZ - 1) / T::TZ);
+    const int64_t blocks = (int64_t)tiles_x * tiles_y * tiles_z;
+    const int64_t chunks = (cells + kChunk - 1) / kChunk;
+    if (cells == 0) return hipSuccess;
+    float *gpart = ws;
+    float *rec = gpart + cells * C;
+    float *partial = rec + cells * R::N;
+    bwd_cell<NDIM, NIN, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
+        src, gout, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w,
+        a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold, gpart,
+        rec, cells);
+    bwd_conv_t<NDIM, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
+        gpart, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w, gin,
+        cells);
+    wgrad_partials<NDIM, C, H><<<(unsigned)chunks, kBwdThreads, 0, stream>>>(
+        src, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, cells, partial);
+    wgrad_reduce<C, H, TAPS><<<(G::N + kBwdThreads - 1) / kBwdThreads, kBwdThreads, 0, stream>>>(
+        partial, chunks, g);
+    return hipGetLastError();
+}
+
+template <int NDIM, int C, int H>
+hipError_t bwd_nin(const StepArgs &a, const float *src, const float *gout, float *gin,
+                   LevelGradsDev g, float *ws, hipStream_t stream) {
+    if (a.n_in == 1) return launch_bwd<NDIM, 1, C, H>(a, src, gout, gin, g, ws, stream);
+    if (a.n_in == 3) return launch_bwd<NDIM, 3, C, H>(a, src, gout, gin, g, ws, stream);
+    return hipErrorInvalidValue;
+}
+
+template <int NDIM>
+hipError_t bwd_size(const StepArgs &a, const float *src, const float *gout, float *gin,
+                    LevelGradsDev g, float *ws, hipStream_t stream) {
+    if (a.channels == 16 && a.hidden == 64) return bwd_nin<NDIM, 16, 64>(a, src, gout, gin, g, ws, stream);
+    if (a.channels == 12 && a.hidden == 48) return bwd_nin<NDIM, 12, 48>(a, src, gout, gin, g, ws, stream);
+    if (a.channels == 20 && a.hidden == 100)
+        return bwd_nin<NDIM, 20, 100>(a, src, gout, gin, g, ws, stream);
+    return hipErrorInvalidValue;
+}
+
+// Adjoint of the upsample + inject: one thread per coarse cell and channel.
+__global__ __launch_bounds__(256) void upsample_adjoint(const float *__restrict__ gfine,
+                                                        Extent3 cext, int fz, int fy, int fx,
+                                                        int n_in, int channels,
+                                                        float *__restrict__ gcoarse) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t total = cext.d * cext.h * cext.w * channels;
+    if (i >= total) return;
+    const int c = (int)(i % channels);
+    const int64_t q = i / channels;
+    const int64_t cx = q % cext.w, cy = (q / cext.w) % cext.h, cz = q / (cext.w * cext.h);
+    const int64_t fh = cext.h * fy, fw = cext.w * fx;
+    double s = 0.0;
+    if (c >= n_in)
+        for (int a = 0; a < fz; ++a)
+            for (int b = 0; b < fy; ++b)
+                for (int d = 0; d < fx; ++d)
+                    s += gfine[(((cz * fz + a) * fh + cy * fy + b) * fw + cx * fx + d) * channels + c];
+    gcoarse[i] = (float)s;
+}
+
+// Readout MSE: grad (all channels, zero but the last two) and per-block loss
+// partials (fp64); then loss = their sum in block order.
+__global__ __launch_bounds__(256) void mse_grad(const float *__restrict__ state,
+                                                const float *__restrict__ target, int64_t cells,
+                                                int channels, float *__restrict__ grad,
+                                                double *__restrict__ block_loss) {
+    __shared__ double part[256];
+    const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    double l = 0.0;
+    if (p < cells) {
+        for (int c = 0; c < channels - 2; ++c) grad[p * channels + c] = 0.f;
+        for (int k = 0; k < 2; ++k) {
+            // the difference of two fp32 values is exact in fp64; the gradient
+            // is its correctly rounded fp32 value
+            const double d = (double)state[p * channels + channels - 2 + k] - (double)target[p * 2 + k];
+            grad[p * channels + channels - 2 + k] = (float)d;
+            l += 0.5 * d * d;
+        }
+    }
+    part[threadIdx.x] = l;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if (threadIdx.x < s) part[threadIdx.x] += part[threadIdx.x + s];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) block_loss[blockIdx.x] = part[0];
+}
+
+__global__ __launch_bounds__(64) void sum_losses(const double *__restrict__ block_loss,
+                                                 int64_t blocks, double *__restrict__ loss) {
+    if (threadIdx.x != 0) return;
+    double s = 0.0;
+    for (int64_t b = 0; b < blocks; ++b) s += block_loss[b];
+    *loss = s;
+}
+
+__global__ __launch_bounds__(256) void fill_zero(float *__restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) p[i] = 0.f;
+}
+
+}  // namespace
+
+size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_t cells) {
+    const int taps = ndim == 3 ? 27 : 9;
+    const int64_t rec_n = 4 * channels + 2 * hidden;
+    const int64_t wg_n = 3 * channels * hidden + hidden + channels + channels * taps;
+    const int64_t chunks = (cells + kChunk - 1) / kChunk;
+    return (size_t)(cells * channels + cells * rec_n + chunks * wg_n);
+}
+
+hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,
+                                float *gin, LevelGradsDev g, float *ws, hipStream_t stream) {
+    return a.ndim == 2 ? bwd_size<2>(a, src, gout, gin, g, ws, stream)
+                       : bwd_size<3>(a, src, gout, gin, g, ws, stream);
+}
+
+hipError_t launch_upsample_adjoint(const float *gfine, Extent3 coarse, int fz, int fy, int fx,
+                                   int n_in, int channels, float *gcoarse, hipStream_t stream) {
+    const int64_t total = coarse.cells() * channels;
+    if (total == 0) return hipSuccess;
+    upsample_adjoint<<<(unsigned)((total + 255) / 256), 256, 0, stream>>>(
+        gfine, coarse, fz, fy, fx, n_in, channels, gcoarse);
+    return hipGetLastError();
+}
+
+size_t mse_workspace_doubles(int64_t cells) { return (size_t)((cells + 255) / 256); }
+
+hipError_t launch_readout_mse(const float *state, const float *target, int64_t cells, int channels,
+                              float *grad, double *loss, double *ws, hipStream_t stream) {
+    const int64_t blocks = (cells + 255) / 256;
+    if (blocks > 0)
+        mse_grad<<<(unsigned)blocks, 256, 0, stream>>>(state, target, cells, channels, grad, ws);
+    sum_losses<<<1, 64, 0, stream>>>(ws, blocks, loss);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    fill_zero<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(p, n);
+    return hipGetLastError();
+}
+
+}  // namespace octnca

@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib, library_path):
 
 def test_version_and_strerror(lib):
     declared = int(re.search(r"#define OCTNCA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.octree_nca_abi_version() == declared == 2
+    assert lib.octree_nca_abi_version() == declared == 3
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.octree_nca_strerror(st).decode() not in ("", "unknown status")
     assert lib.octree_nca_strerror(17).decode() == "unknown status"
@@ -247,3 +247,92 @@ def test_python_binding_refuses_host_tensors(lib):
     with pytest.raises(octnca.OctreeNCAError):
         octnca.octree_nca_readout(m, torch.zeros(1, 4, 4, 16), torch.zeros(1, 4, 4,
                                                                             dtype=torch.uint8))
+
+
+# ---------------------------------------------------------------------------
+# training entry points (fp32 states only): validation before any launch
+# ---------------------------------------------------------------------------
+
+from paper_2508_06993_amd import _LevelGrads   # noqa: E402
+
+
+def grads():
+    return ctypes.byref(_LevelGrads(FAKE, FAKE, FAKE, FAKE, FAKE))
+
+
+def bwd_ws_floats(cells, c=16, h=64, taps=9):
+    chunks = (cells + 31) // 32
+    return cells * c + cells * (4 * c + 2 * h) + chunks * (3 * c * h + h + c + c * taps)
+
+
+def test_step_backward_workspace_bytes(lib):
+    assert lib.octree_nca_step_backward_workspace_bytes(model(), _Extent(1, 8, 10)) == \
+        4 * bwd_ws_floats(80)
+    assert lib.octree_nca_step_backward_workspace_bytes(model(ndim=3, n_in=1), _Extent(3, 5, 7)) \
+        == 4 * bwd_ws_floats(105, taps=27)
+    assert lib.octree_nca_step_backward_workspace_bytes(model(ndim=4), _Extent(1, 8, 8)) == 0
+
+
+def step_bwd(lib, m=None, state=FAKE, gout=FAKE2, ext=(1, 8, 8), level=0, step=0, rate=0.5,
+             gin=ctypes.c_void_p(0x7f0010000000), gr=None, ws=ctypes.c_void_p(0x7f0020000000),
+             ws_bytes=1 << 30):
+    return lib.octree_nca_step_backward(m if m is not None else model(), state, gout,
+                                        _Extent(*ext), weights(), level, step, rate, 0, gin,
+                                        gr if gr is not None else grads(), ws, ws_bytes, None)
+
+
+def test_step_backward_rejects_bad_arguments(lib):
+    assert step_bwd(lib, m=model(dt=1)) == EUNSUP                 # fp16 states
+    assert step_bwd(lib, state=None) == EINVAL
+    assert step_bwd(lib, gr=ctypes.byref(_LevelGrads(FAKE, None, FAKE, FAKE, FAKE))) == EINVAL
+    assert step_bwd(lib, step=-1) == EINVAL
+    assert step_bwd(lib, rate=1.5) == EINVAL
+    assert step_bwd(lib, ws_bytes=100) == ESPACE
+    assert step_bwd(lib, gin=FAKE) == EINVAL                      # grad_in overlaps state
+    assert step_bwd(lib, ws=FAKE2) == EINVAL                      # workspace overlaps grad_out
+    assert step_bwd(lib, ext=(1, 0, 8)) == ESHAPE
+
+
+def test_upsample_backward_rejects_bad_arguments(lib):
+    f = (ctypes.c_int32 * 3)(1, 2, 2)
+    assert lib.octree_nca_upsample_backward(model(dt=1), FAKE, _Extent(1, 4, 4), f, FAKE2,
+                                            None) == EUNSUP
+    assert lib.octree_nca_upsample_backward(model(), None, _Extent(1, 4, 4), f, FAKE2,
+                                            None) == EINVAL
+    bad = (ctypes.c_int32 * 3)(2, 2, 2)                          # fz != 1 in 2D
+    assert lib.octree_nca_upsample_backward(model(), FAKE, _Extent(1, 4, 4), bad, FAKE2,
+                                            None) == ESHAPE
+    assert lib.octree_nca_upsample_backward(model(), FAKE, _Extent(1, 4, 4), f, FAKE,
+                                            None) == EINVAL     # in place
+
+
+def test_readout_mse_rejects_bad_arguments(lib):
+    assert lib.octree_nca_readout_mse_workspace_bytes(_Extent(1, 16, 20)) == 8 * 2
+    assert lib.octree_nca_readout_mse_workspace_bytes(_Extent(1, 0, 20)) == 0
+    ws = ctypes.c_void_p(0x7f0030000000)
+    assert lib.octree_nca_readout_mse(model(), FAKE, FAKE2, _Extent(1, 16, 20),
+                                      ctypes.c_void_p(0x7f0010000000), ws, ws, 8,
+                                      None) == ESPACE
+    assert lib.octree_nca_readout_mse(model(dt=1), FAKE, FAKE2, _Extent(1, 16, 20),
+                                      ctypes.c_void_p(0x7f0010000000), ws, ws, 64,
+                                      None) == EUNSUP
+    assert lib.octree_nca_readout_mse(model(), FAKE, FAKE2, _Extent(1, 16, 20), None, ws, ws,
+                                      64, None) == EINVAL
+
+
+def test_train_workspace_and_step_validation(lib):
+    f = (ctypes.c_int32 * 3)(1, 2, 2)
+    steps = (ctypes.c_int32 * 2)(3, 2)
+    n = lib.octree_nca_train_workspace_bytes(model(), _Extent(1, 8, 8), 2, f, steps)
+    assert n > 4 * (4 * 64 * 16 + 3 * 16 * 16)        # at least the tape of both levels
+    assert lib.octree_nca_train_workspace_bytes(model(dt=1), _Extent(1, 8, 8), 2, f, steps) == 0
+    neg = (ctypes.c_int32 * 2)(3, -1)
+    assert lib.octree_nca_train_workspace_bytes(model(), _Extent(1, 8, 8), 2, f, neg) == 0
+    ws = (_LevelWeights * 2)(*[_LevelWeights(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    gs = (_LevelGrads * 2)(*[_LevelGrads(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    big = ctypes.c_void_p(0x7f4000000000)
+    args = lambda wsb: (model(), FAKE, _Extent(1, 8, 8), 2, f, ws, steps, 0.5, 0, FAKE2, big,
+                        wsb, gs, ctypes.c_void_p(0x7f0050000000), None, None)
+    assert lib.octree_nca_train_step(*args(n - 1)) == ESPACE
+    assert lib.octree_nca_train_step(model(), FAKE, _Extent(1, 8, 8), 2, f, ws, steps, 0.5, 0,
+                                     FAKE2, big, n, gs, None, None, None) == EINVAL
