@@ -49,6 +49,25 @@ def algorithmic_flop_per_cell_step(wl) -> int:
     return 2 * (c * taps + 2 * c * h + h * hid) + c + h + h + hid
 
 
+def algorithmic_train_flop_per_cell_step(wl) -> int:
+    """Forward and backward of one training step per cell: the forward
+    (algorithmic_flop_per_cell_step) twice (once in the forward pass, once
+    recomputed by the backward), then W2^T gu (2 H (C-n_in)), the ReLU mask
+    (H), W1^T ga (2 H 2C), dW1 += ga f^T (2 H 2C), dW2 += gu h^T (2 (C-n_in) H),
+    db1 (H), dconv_b (C), dconv_w (2 C taps), the transposed convolution
+    (2 C taps) and the state-gradient adds (2 C)."""
+    c, h, taps, hid = wl.channels, wl.hidden, wl.taps(), wl.channels - wl.n_in
+    bwd = 2 * h * hid + h + 2 * h * 2 * c + 2 * h * 2 * c + 2 * hid * h + h + c + \
+        2 * c * taps + 2 * c * taps + 2 * c
+    return 2 * algorithmic_flop_per_cell_step(wl) + bwd
+
+
+def algorithmic_train_bytes_per_cell_step(wl) -> int:
+    """fp32 state of C channels: the forward reads a state and writes the next
+    (kept), the backward reads that state and dL/dS' and writes dL/dS."""
+    return 5 * wl.channels * 4
+
+
 def algorithmic_bytes_per_cell_step(wl) -> int:
     """Read C channels, write the C - n_in hidden channels."""
     eb = 2 if wl.dtype == "f16" else 4
@@ -138,6 +157,133 @@ def cpu_baseline(wl, seconds_hint=10.0, max_steps=200):
                       f"affinity={len(os.sched_getaffinity(0))} cpus"}
 
 
+def cpu_train_baseline(wl, seconds_hint=10.0):
+    """Time the CPU oracle's training step (forward keeping every state, the
+    readout MSE, backward through all steps and levels) on the workload's
+    structure at a reduced extent, repeated until about `seconds_hint` s."""
+    import numpy as np
+    import oracle
+    from synthetic import make_image, make_target, make_weights, scaled
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:   # pragma: no cover
+        threads = 1
+    small = scaled(wl, (1, 160, 160)) if wl.ndim == 2 else scaled(wl, wl.extent)
+    image = make_image(small)
+    target = make_target(small, image)
+    ws = make_weights(small)
+    kw = dict(ndim=small.ndim, n_in=small.n_in, factors=small.factors, seed=small.seed,
+              fire_rate=small.fire_rate)
+    runs = 0
+    t0 = time.perf_counter()
+    while runs < 1 or time.perf_counter() - t0 < seconds_hint:
+        tape = oracle.train_forward(image, ws, channels=small.channels, steps=small.steps,
+                                    dtype=np.float32, **kw)
+        _, g = oracle.readout_mse(tape.final, target)
+        oracle.train_backward(tape, ws, g_final=g, **kw)
+        runs += 1
+    dt_s = time.perf_counter() - t0
+    cs = small.cell_steps()
+    return {"value": cs * runs / dt_s, "unit": "cell-steps/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{runs} training step(s) (forward + backward) of the workload's structure "
+                      f"at {small.extent[1]}x{small.extent[2]} ({cs} cell-steps each, "
+                      f"{dt_s:.1f} s), numpy float64, BLAS threads={threads}, "
+                      f"affinity={len(os.sched_getaffinity(0))} cpus"}
+
+
+def train_bench(args):
+    """--train: the fused training step (octree_nca_train_step) on a training
+    workload; one step = forward keeping every state + loss + backward."""
+    import numpy as np
+    import torch
+    import paper_2508_06993_amd as octnca
+    from paper_2508_06993_amd.runtime import upload_weights
+    from synthetic import TRAIN_WORKLOADS, make_image, make_target, make_weights
+
+    wl = TRAIN_WORKLOADS[args.train_workload]
+    torch.cuda.set_device(0)
+    octnca.lib()
+    print(f"# training workload {wl.name}: extent {wl.extent}, levels {wl.levels}, "
+          f"steps {wl.steps}", file=sys.stderr, flush=True)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in)
+    image_np = make_image(wl)
+    image = torch.from_numpy(image_np).cuda()
+    target = torch.from_numpy(make_target(wl, image_np)).cuda()
+    wts = make_weights(wl)
+    weights = upload_weights(wts)
+    grads = [{k: torch.zeros(np.shape(getattr(w, k)), dtype=torch.float32, device="cuda")
+              for k in ("conv_w", "conv_b", "w1", "b1", "w2")} for w in wts]
+    loss = torch.zeros(1, dtype=torch.float64, device="cuda")
+    torch.cuda.reset_peak_memory_stats()
+    work = torch.empty(octnca.octree_nca_train_workspace_bytes(model, wl.extent, wl.factors,
+                                                               wl.steps),
+                       dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def one():
+        octnca.octree_nca_train_step(model, image, wl.factors, weights, wl.steps, wl.fire_rate,
+                                     wl.seed, target, work, grads, loss, stream=stream)
+
+    for _ in range(args.warmup):
+        one()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record(stream)
+        one()
+        b.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = sum(a.elapsed_time(b) for a, b in ev)
+    cs = wl.cell_steps()
+    flop = algorithmic_train_flop_per_cell_step(wl) * cs * args.steps
+    byts = algorithmic_train_bytes_per_cell_step(wl) * cs * args.steps
+    tflops = flop / (gpu_ms * 1e-3) / 1e12
+    gbs = byts / (gpu_ms * 1e-3) / 1e9
+    # the backward, most of the FLOPs, runs on the vector ALUs in fp32
+    t_alu = flop / (FP32_SCALAR_FMA_PEAK_TFLOPS * 1e12)
+    t_hbm = byts / (HBM_PEAK_GBS * 1e9)
+    if t_alu >= t_hbm:
+        bound, achieved, peak, unit = "alu", tflops, FP32_SCALAR_FMA_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        bound, achieved, peak, unit = "hbm", gbs, HBM_PEAK_GBS, "GB/s"
+    out = {
+        "metric": "NCA training cell-steps/sec",
+        "value": cs * args.steps / wall,
+        "unit": "cell-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "extent_dhw": list(wl.extent), "levels": wl.levels,
+                   "steps_per_level": list(wl.steps), "cells_per_level": wl.cells_per_level(),
+                   "cell_steps_per_step": cs, "channels": wl.channels, "hidden": wl.hidden,
+                   "n_in": wl.n_in, "fire_rate": wl.fire_rate, "loss": "readout MSE",
+                   "parallelism": "single GPU"},
+        "roofline": {"kernel": "octree_nca_train_step (forward fp32 MFMA, backward fp32 VALU)",
+                     "bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1),
+                     "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                     "achieved_tflops": round(tflops, 3), "achieved_hbm_gbs": round(gbs, 1),
+                     "gpu_ms_per_step": round(gpu_ms / args.steps, 3),
+                     "flop_per_cell_step": algorithmic_train_flop_per_cell_step(wl),
+                     "bytes_per_cell_step": algorithmic_train_bytes_per_cell_step(wl)},
+        "peak_vram_gb": round(torch.cuda.max_memory_allocated() / 1e9, 3),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_train_baseline(wl)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -145,6 +291,9 @@ def main(argv=None):
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="pathology184mp")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--train", action="store_true",
+                    help="time the fused training step instead of the inference")
+    ap.add_argument("--train-workload", default="pathology_train320")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 3 times (calibrates the HBM "
                          "byte counters of a profiler against a kernel of known traffic)")
@@ -159,6 +308,8 @@ def main(argv=None):
     import numpy as np
     import torch
 
+    if args.train:
+        return train_bench(args)
     if args.copy_probe:
         n = args.copy_probe * (1 << 20)
         a = torch.empty(n, dtype=torch.uint8, device="cuda")

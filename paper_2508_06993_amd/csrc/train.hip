@@ -15,10 +15,12 @@
 //      [f | h | ga | gu | gP] for the weight gradients;
 //   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
 //      gP (halo tile of gP in LDS);
-//   3. wgrad_partials: per chunk of 32 consecutive cells, the chunk's sums of
-//      every weight-gradient entry (records staged in LDS);
-//   4. wgrad_reduce: the chunk sums added in chunk order, in fp64, to the
-//      caller's gradients (accumulated, so the steps of a level sum up).
+//   3. wgrad_partials: per block of 64 consecutive cells, the sums of every
+//      weight-gradient entry (records staged in LDS 32 cells at a time, sums
+//      in registers), stored entry-major;
+//   4. wgrad_reduce: one wave per entry adds the block sums in fp64 (lane l
+//      takes blocks l, l + 64, ... in order, then a fixed shuffle tree) to
+//      the caller's gradients (accumulated, so the steps of a level sum up).
 #include "launch.h"
 
 namespace octnca {
@@ -26,7 +28,8 @@ namespace octnca {
 namespace {
 
 constexpr int kBwdThreads = 256;
-constexpr int kChunk = 32;   // cells per weight-gradient partial sum
+constexpr int kChunk = 32;          // cells staged in LDS at a time
+constexpr int kChunksPerBlock = 2;   // chunks summed by one block (64 cells)
 
 template <int NDIM> struct BwdTile;
 template <> struct BwdTile<2> { static constexpr int TZ = 1, TY = 8, TX = 32; };
@@ -181,7 +184,9 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
     }
 }
 
-// Sums over the chunk's cells of every weight-gradient entry.
+// Sums over a block's cells (kChunksPerBlock chunks of kChunk cells, staged
+// in LDS one chunk at a time) of every weight-gradient entry; thread t owns
+// entries t, t + 256, ... and keeps their sums in registers.
 template <int NDIM, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     const float *__restrict__ src, const float *__restrict__ rec, int dd, int dh, int dw,
@@ -189,55 +194,79 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     using R = Rec<C, H>;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
     using G = WG<C, H, TAPS>;
+    constexpr int KO = (G::N + kBwdThreads - 1) / kBwdThreads;   // entries per thread
     __shared__ float recs[R::N][kChunk + 1];   // [entry][cell]
-    const int64_t first = (int64_t)blockIdx.x * kChunk;
-    const int n = (int)min<int64_t>(kChunk, cells - first);
-    for (int i = threadIdx.x; i < kChunk * R::N; i += kBwdThreads) {
-        const int k = i / kChunk, cell = i % kChunk;
-        recs[k][cell] = cell < n ? rec[k * cells + first + cell] : 0.f;
-    }
-    __syncthreads();
-    float *out = partial + (int64_t)blockIdx.x * G::N;
-    for (int o = threadIdx.x; o < G::N; o += kBwdThreads) {
-        float s = 0.f;
-        if (o < G::W2) {                       // dW1[j][k] = sum ga[j] f[k]
-            const int j = o / (2 * C), k = o % (2 * C);
-            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
-        } else if (o < G::B1) {                // dW2[c][j] = sum gu[c] h[j]
-            const int c = (o - G::W2) / H, j = (o - G::W2) % H;
-            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
-        } else if (o < G::CB) {                // db1[j] = sum ga[j]
-            const int j = o - G::B1;
-            for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
-        } else if (o < G::CW) {                // dconv_b[c] = sum gP[c]
-            const int c = o - G::CB;
-            for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
-        } else {                               // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
-            const int c = (o - G::CW) / TAPS, t = (o - G::CW) % TAPS;
-            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
-            for (int i = 0; i < n; ++i) {
-                const int64_t p = first + i;
-                const int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
-                const int gx = x + dx, gy = y + dy, gz = z + dz;
-                const float sv = (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
-                                     ? src[(((int64_t)gz * dh + gy) * dw + gx) * C + c]
-                                     : 0.f;
-                s = fmaf(recs[R::GP + c][i], sv, s);
-            }
+    float acc[KO];
+#pragma unroll
+    for (int q = 0; q < KO; ++q) acc[q] = 0.f;
+    for (int ch = 0; ch < kChunksPerBlock; ++ch) {
+        const int64_t first = ((int64_t)blockIdx.x * kChunksPerBlock + ch) * kChunk;
+        if (first >= cells) break;                       // uniform over the block
+        const int n = (int)min<int64_t>(kChunk, cells - first);
+        __syncthreads();                                 // previous chunk consumed
+        for (int i = threadIdx.x; i < kChunk * R::N; i += kBwdThreads) {
+            const int k = i / kChunk, cell = i % kChunk;
+            recs[k][cell] = cell < n ? rec[k * cells + first + cell] : 0.f;
         }
-        out[o] = s;
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < KO; ++q) {
+            const int o = threadIdx.x + q * kBwdThreads;
+            float s = acc[q];
+            if (o < G::W2) {                       // dW1[j][k] = sum ga[j] f[k]
+                const int j = o / (2 * C), k = o % (2 * C);
+                for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
+            } else if (o < G::B1) {                // dW2[c][j] = sum gu[c] h[j]
+                const int c = (o - G::W2) / H, j = (o - G::W2) % H;
+                for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
+            } else if (o < G::CB) {                // db1[j] = sum ga[j]
+                const int j = o - G::B1;
+                for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
+            } else if (o < G::CW) {                // dconv_b[c] = sum gP[c]
+                const int c = o - G::CB;
+                for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
+            } else if (o < G::N) {                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
+                const int c = (o - G::CW) / TAPS, t = (o - G::CW) % TAPS;
+                const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+                int64_t p = first;
+                int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
+                for (int i = 0; i < n; ++i) {
+                    const int gx = x + dx, gy = y + dy, gz = z + dz;
+                    const float sv = (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
+                                         ? src[(((int64_t)gz * dh + gy) * dw + gx) * C + c]
+                                         : 0.f;
+                    s = fmaf(recs[R::GP + c][i], sv, s);
+                    if (++x == dw) {               // next cell in row-major order
+                        x = 0;
+                        if (++y == dh) { y = 0; ++z; }
+                    }
+                }
+            }
+            acc[q] = s;
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < KO; ++q) {
+        const int o = threadIdx.x + q * kBwdThreads;
+        if (o < G::N) partial[(int64_t)o * gridDim.x + blockIdx.x] = acc[q];   // [entry][block]
     }
 }
 
-// grads += sum over chunks (in chunk order, fp64) of the partial sums.
+// grads += the sum of the block partial sums of each entry: one wave per
+// entry, lane l summing blocks l, l + 64, ... in order in fp64, then a fixed
+// butterfly over the lanes (deterministic).
 template <int C, int H, int TAPS>
 __global__ __launch_bounds__(kBwdThreads) void wgrad_reduce(const float *__restrict__ partial,
-                                                            int64_t chunks, LevelGradsDev g) {
+                                                            int64_t blocks, LevelGradsDev g) {
     using G = WG<C, H, TAPS>;
-    const int o = blockIdx.x * kBwdThreads + threadIdx.x;
-    if (o >= G::N) return;
+    const int o = blockIdx.x * (kBwdThreads / 64) + (int)(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (o >= G::N) return;                               // uniform over the wave
     double s = 0.0;
-    for (int64_t b = 0; b < chunks; ++b) s += (double)partial[b * G::N + o];
+    for (int64_t b = lane; b < blocks; b += 64) s += (double)partial[(int64_t)o * blocks + b];
+#pragma unroll
+    for (int m = 32; m > 0; m >>= 1) s += __shfl_xor(s, m);
+    if (lane != 0) return;
     float *dst;
     if (o < G::W2) dst = g.w1 + o;
     else if (o < G::B1) dst = g.w2 + (o - G::W2);
@@ -259,7 +288,7 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
     const int tiles_y = (int)((a.ext.h + T::TY - 1) / T::TY);
     const int tiles_z = (int)((a.ext.d + T::TZ - 1) / T::TZ);
     const int64_t blocks = (int64_t)tiles_x * tiles_y * tiles_z;
-    const int64_t chunks = (cells + kChunk - 1) / kChunk;
+    const int64_t chunks = (cells + kChunk * kChunksPerBlock - 1) / (kChunk * kChunksPerBlock);
     if (cells == 0) return hipSuccess;
     float *gpart = ws;
     float *rec = gpart + cells * C;
@@ -273,8 +302,9 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
         cells);
     wgrad_partials<NDIM, C, H><<<(unsigned)chunks, kBwdThreads, 0, stream>>>(
         src, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, cells, partial);
-    wgrad_reduce<C, H, TAPS><<<(G::N + kBwdThreads - 1) / kBwdThreads, kBwdThreads, 0, stream>>>(
-        partial, chunks, g);
+    constexpr int kWavesPerBlock = kBwdThreads / 64;
+    wgrad_reduce<C, H, TAPS><<<(G::N + kWavesPerBlock - 1) / kWavesPerBlock, kBwdThreads, 0,
+                               stream>>>(partial, chunks, g);
     return hipGetLastError();
 }
 
@@ -364,8 +394,8 @@ size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_
     const int taps = ndim == 3 ? 27 : 9;
     const int64_t rec_n = 4 * channels + 2 * hidden;
     const int64_t wg_n = 3 * channels * hidden + hidden + channels + channels * taps;
-    const int64_t chunks = (cells + kChunk - 1) / kChunk;
-    return (size_t)(cells * channels + cells * rec_n + chunks * wg_n);
+    const int64_t blocks = (cells + kChunk * kChunksPerBlock - 1) / (kChunk * kChunksPerBlock);
+    return (size_t)(cells * channels + cells * rec_n + blocks * wg_n);
 }
 
 hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,

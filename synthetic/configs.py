@@ -101,6 +101,18 @@ VIDEO_2DT = Workload(
 
 WORKLOADS = {w.name: w for w in (TINY_2D, MEDIUM_2D, PATHOLOGY_184MP, VOLUME_3D, VIDEO_2DT)}
 
+# Training workload (the fused training step): the paper trains the pathology
+# model on 320 x 320 patches (supplement S7, training details) with the
+# five-level octree of its level table; 20 steps per level as the inference
+# workloads, fp32 states.
+PATHOLOGY_TRAIN_320 = Workload(
+    name="pathology_train320", ndim=2, extent=(1, 320, 320), n_in=3, factors=_f2(4),
+    steps=(20,) * 5, image_kind="blobs",
+    description="RGB 320x320 training patch of smooth blobs + 5% noise, 5 levels "
+                "320^2 -> 20^2, 20 steps per level, fp32")
+
+TRAIN_WORKLOADS = {w.name: w for w in (PATHOLOGY_TRAIN_320,)}
+
 
 def scaled(base: Workload, extent: Extent, steps=None, name=None, **kw) -> Workload:
     """A smaller workload with the same structure (levels, factors, n_in, dtype)

@@ -143,3 +143,13 @@ def _ellipses(rng, t, h, w, n_in, n_ell=12):
             pos[hi, ax] = 2 * (lim - 1) - pos[hi, ax]
             vel[lo | hi, ax] = -vel[lo | hi, ax]
     return out
+
+
+def make_target(wl: Workload, image: np.ndarray) -> np.ndarray:
+    """Synthetic two-class segmentation target [D][H][W][2] (fp32 one-hot) for a
+    training workload: class 1 where the image's channel mean exceeds its
+    median, class 0 elsewhere.  A label map with the image's structure; no part
+    of the method is computed here."""
+    m = np.asarray(image, np.float32).mean(axis=-1)
+    fg = (m > np.median(m)).astype(np.float32)
+    return np.stack([1.0 - fg, fg], axis=-1).astype(np.float32)
