@@ -15,7 +15,7 @@
 //      [f | h | ga | gu | gP] for the weight gradients;
 //   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
 //      gP (halo tile of gP in LDS);
-//   3. wgrad_partials: per block of 64 consecutive cells, the sums of every
+//   3. wgrad_partials: per block of 32 consecutive cells, the sums of every
 //      weight-gradient entry (records staged in LDS 32 cells at a time, sums
 //      in registers), stored entry-major;
 //   4. wgrad_reduce: one wave per entry adds the block sums in fp64 (lane l
@@ -29,7 +29,7 @@ namespace {
 
 constexpr int kBwdThreads = 256;
 constexpr int kChunk = 32;          // cells staged in LDS at a time
-constexpr int kChunksPerBlock = 2;   // chunks summed by one block (64 cells)
+constexpr int kChunksPerBlock = 1;   // chunks summed by one block (32 cells)
 
 template <int NDIM> struct BwdTile;
 template <> struct BwdTile<2> { static constexpr int TZ = 1, TY = 8, TX = 32; };
@@ -215,31 +215,40 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
             float s = acc[q];
             if (o < G::W2) {                       // dW1[j][k] = sum ga[j] f[k]
                 const int j = o / (2 * C), k = o % (2 * C);
-                for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
+    #pragma unroll 8
+            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
             } else if (o < G::B1) {                // dW2[c][j] = sum gu[c] h[j]
                 const int c = (o - G::W2) / H, j = (o - G::W2) % H;
-                for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
+    #pragma unroll 8
+            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
             } else if (o < G::CB) {                // db1[j] = sum ga[j]
                 const int j = o - G::B1;
-                for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
+    #pragma unroll 8
+            for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
             } else if (o < G::CW) {                // dconv_b[c] = sum gP[c]
                 const int c = o - G::CB;
-                for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
+    #pragma unroll 8
+            for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
             } else if (o < G::N) {                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
                 const int c = (o - G::CW) / TAPS, t = (o - G::CW) % TAPS;
                 const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+                // neighbour loads without branches (clamped address, 0/1 weight),
+                // so that the loads of several cells are in flight together
                 int64_t p = first;
                 int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
+#pragma unroll 8
                 for (int i = 0; i < n; ++i) {
                     const int gx = x + dx, gy = y + dy, gz = z + dz;
-                    const float sv = (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
-                                         ? src[(((int64_t)gz * dh + gy) * dw + gx) * C + c]
-                                         : 0.f;
-                    s = fmaf(recs[R::GP + c][i], sv, s);
-                    if (++x == dw) {               // next cell in row-major order
-                        x = 0;
-                        if (++y == dh) { y = 0; ++z; }
-                    }
+                    const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+                    const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
+                              cz = min(max(gz, 0), dd - 1);
+                    const float sv = src[(((int64_t)cz * dh + cy) * dw + cx) * C + c];
+                    s = fmaf(recs[R::GP + c][i], in ? sv : 0.f, s);
+                    const bool wrap = ++x == dw;   // next cell in row-major order
+                    x = wrap ? 0 : x;
+                    const bool wrap_y = wrap && ++y == dh;
+                    y = wrap_y ? 0 : y;
+                    z += wrap_y ? 1 : 0;
                 }
             }
             acc[q] = s;
