@@ -1282,8 +1282,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
 }
 
 // ---------------------------------------------------------------------------
-// 3D: a work item is an 8 x 32 (y, x) column and a run of k3ZRun output
-// planes.  Input planes stream through a ring of three LDS plane slots
+// 3D: a work item is an 8 x 32 (y, x) column and a run of `zrun` output
+// planes (32, or fewer on levels with too few columns to fill the chip).  Input planes stream through a ring of three LDS plane slots
 // (planes p - 1 and p are in use while p + 1 is written).  Each input plane p
 // is read once: its 9 in-plane taps feed three rolling perception sums, for
 // outputs p + 1 (the dz = -1 weights), p (dz = 0) and p - 1 (dz = +1).  After
@@ -1293,7 +1293,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
 // read once per wave and applied to all 4 groups.
 // ---------------------------------------------------------------------------
 constexpr int k3TY = 8;
-constexpr int k3ZRun = 32;    // output planes per work item
+constexpr int k3ZRun = 32;    // output planes per work item (longest run)
 // Work item i of a 3D step is tile (tx, ty) of z run zr, with
 // i = (zr * tiles_y + ty) * tiles_x + tx.
 
@@ -1301,7 +1301,8 @@ constexpr int k3ZRun = 32;    // output planes per work item
 template <typename T, int NIN, class Mlp>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const T *__restrict__ src, T *__restrict__ dst, int dd, int dh, int dw, int tiles_x,
-    int tiles_y, int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
+    int tiles_y, int items, int zrun, const float *__restrict__ conv_w,
+    const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
     using Loader = RowLoader<T, k3TY + 2>;
@@ -1363,8 +1364,8 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         const int tx = rest % tiles_x;
         const int ty = rest / tiles_x;
         const int y0 = ty * k3TY, x0 = tx * kTileW;
-        const int z_begin = zr * k3ZRun;
-        const int z_end = min(dd, z_begin + k3ZRun);
+        const int z_begin = zr * zrun;
+        const int z_end = min(dd, z_begin + zrun);
 
         // rolling perception sums (bias included) of outputs p - 1, p, p + 1
         float acc_p[4][4], acc_c[4][4], acc_n[4][4];
@@ -1517,7 +1518,7 @@ constexpr int k3hBlocksPerCu = 3;
 template <int NIN, bool ALIGNED, bool UP>
 __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mfma_3d_f16(
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
-    int tiles_x, int tiles_y, int items, const float *__restrict__ conv_w,
+    int tiles_x, int tiles_y, int items, int zrun, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
     uint64_t threshold, const __half *__restrict__ up_img, int up_cdh, int up_cdw, int up_fz,
@@ -1593,8 +1594,8 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
         const int y0 = ty * k3TY, x0 = tx * kTileW;
         y0_cur = y0;
         x0_cur = x0;
-        const int z_begin = zr * k3ZRun;
-        const int z_end = min(dd, z_begin + k3ZRun);
+        const int z_begin = zr * zrun;
+        const int z_end = min(dd, z_begin + zrun);
         // store offsets of the lane's 4 cells within an output plane's tile rows
         uint32_t offs[4];
 #pragma unroll
@@ -1813,28 +1814,41 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     return hipGetLastError();
 }
 
+// Output planes per 3D work item: the longest run of 32, 16, 8 or 4 planes
+// that still gives at least two work items per block slot (on small levels
+// longer runs would leave CUs idle; a shorter run reads its two halo planes
+// once more per run).
+int pick_zrun(int64_t tiles, int64_t depth, int64_t slots) {
+    for (int r = k3ZRun; r > 4; r /= 2)
+        if (tiles * ((depth + r - 1) / r) >= 2 * slots) return r;
+    return 4;
+}
+
 template <typename T, int NIN, class Mlp>
 hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+    constexpr bool kF16 = std::is_same_v<T, __half> && std::is_same_v<Mlp, MlpF16>;
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
-    const int64_t zruns = (a.ext.d + k3ZRun - 1) / k3ZRun;
+    const int64_t slots = (int64_t)device_cus() * (kF16 ? k3hBlocksPerCu : kBlocksPerCu);
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots);
+    const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
     if (items > INT32_MAX) return hipErrorInvalidValue;
-    if constexpr (std::is_same_v<T, __half> && std::is_same_v<Mlp, MlpF16>) {
-        const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * k3hBlocksPerCu);
+    if constexpr (kF16) {
+        const int grid = (int)std::min<int64_t>(items, slots);
         auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, false>
                                      : nca_step_mfma_3d_f16<NIN, false, false>;
         kern<<<grid, kThreads, 0, stream>>>(
             (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
-            tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
-            a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1);
+            tiles_y, (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level,
+            a.step, a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1);
     } else {
-        const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * kBlocksPerCu);
+        const int grid = (int)std::min<int64_t>(items, slots);
         nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
-            (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
-            a.threshold);
+            (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
+            a.batch, a.seed, a.threshold);
     }
     return hipGetLastError();
 }
@@ -1846,17 +1860,19 @@ hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int 
                             int fy, int fx, const void *img, void *dst, hipStream_t stream) {
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
-    const int64_t zruns = (a.ext.d + k3ZRun - 1) / k3ZRun;
+    const int64_t slots = (int64_t)device_cus() * 2;
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots);
+    const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
     if (items > INT32_MAX) return hipErrorInvalidValue;
-    const int grid = (int)std::min<int64_t>(items, (int64_t)device_cus() * 2);
+    const int grid = (int)std::min<int64_t>(items, slots);
     auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, true>
                                  : nca_step_mfma_3d_f16<NIN, false, true>;
     kern<<<grid, kThreads, 0, stream>>>(
         (const __half *)coarse, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
-        tiles_y, (int)items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
-        a.batch, a.seed, a.threshold, (const __half *)img, cdh, cdw, fz, fy, fx);
+        tiles_y, (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level,
+        a.step, a.batch, a.seed, a.threshold, (const __half *)img, cdh, cdw, fz, fy, fx);
     return hipGetLastError();
 }
 
