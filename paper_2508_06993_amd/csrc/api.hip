@@ -119,17 +119,32 @@ StepArgs step_args(const octnca_model *m, const octnca_extent &e, const octnca_l
     return a;
 }
 
-// Enqueue steps t0 .. t1-1 of a level; step t reads bufs[(t - t0) % 2] and
-// writes bufs[(t - t0 + 1) % 2].
+// Launches that run steps t0 .. t1-1 of a level: one per step, or one per two
+// steps where the two-step kernel applies (a trailing odd step runs alone).
+int32_t level_launches(const StepArgs &a, int32_t t0, int32_t t1) {
+    if (t1 <= t0) return 0;
+    return step_pairs(a) ? (t1 - t0 + 1) / 2 : t1 - t0;
+}
+
+// Enqueue steps t0 .. t1-1 of a level; launch k reads bufs[k % 2] and writes
+// bufs[(k + 1) % 2], so the result is in bufs[level_launches(..) % 2].
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
               const octnca_level_weights *w, int32_t level, int32_t t0, int32_t t1,
               uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0) {
     StepArgs a = step_args(m, e, w, level, seed, threshold, batch);
     void *bufs[2] = {b0, b1};
-    for (int32_t t = t0; t < t1; ++t) {
+    const bool pairs = step_pairs(a);
+    int k = 0;
+    for (int32_t t = t0; t < t1; k ^= 1) {
         a.step = (uint32_t)t;
-        const int k = (t - t0) & 1;
-        const hipError_t err = launch_step(a, bufs[k], bufs[k ^ 1], stream);
+        hipError_t err;
+        if (pairs && t + 1 < t1) {
+            err = launch_step_pair(a, bufs[k], bufs[k ^ 1], stream);
+            t += 2;
+        } else {
+            err = launch_step(a, bufs[k], bufs[k ^ 1], stream);
+            t += 1;
+        }
         if (err != hipSuccess) return OCTNCA_EHIP;
     }
     return OCTNCA_OK;
@@ -242,7 +257,9 @@ int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octn
     st = run_steps(model, buf0, buf1, extent, weights, level, 0, steps, seed, threshold,
                    (hipStream_t)stream);
     if (st) return st;
-    if (result_in_buf1) *result_in_buf1 = steps & 1;
+    if (result_in_buf1)
+        *result_in_buf1 =
+            level_launches(step_args(model, extent, weights, level, seed, threshold, 0), 0, steps) & 1;
     return OCTNCA_OK;
 }
 
@@ -314,11 +331,8 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     if (image == nullptr || weights == nullptr || steps == nullptr || workspace == nullptr ||
         !fire_threshold(fire_rate, &threshold))
         return OCTNCA_EINVAL;
-    int64_t total_steps = 0;
-    for (int l = 0; l < levels; ++l) {
+    for (int l = 0; l < levels; ++l)
         if (!weights_ok(&weights[l]) || steps[l] < 0) return OCTNCA_EINVAL;
-        total_steps += steps[l];
-    }
     if (workspace_bytes < p.bytes) return OCTNCA_ESPACE;
     const size_t eb = elem_bytes(model);
     const size_t state_bytes = (size_t)(finest.d * finest.h * finest.w) * model->channels * eb;
@@ -346,13 +360,14 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     const Dtype dt = dtype_of(model);
     // Levels whose first step reads the next coarser state directly (upsample
     // + inject fused into the step): that transition flips no buffer.
+    // Buffer flips: one per unfused upsample and one per step launch.
     bool fused[kMaxLevels] = {};
-    int n_fused = 0;
-    for (int l = 0; l + 1 < levels; ++l) {
-        if (steps[l] < 1) continue;
+    int64_t flips = 0;
+    for (int l = 0; l < levels; ++l) {
         const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
-        fused[l] = step_fuses_upsample(a);
-        n_fused += fused[l] ? 1 : 0;
+        if (l + 1 < levels && steps[l] >= 1) fused[l] = step_fuses_upsample(a);
+        const int32_t t0 = fused[l] ? 1 : 0;
+        flips += (l + 1 < levels ? 1 : 0) + level_launches(a, t0, steps[l]);
     }
     for (int l = 1; l < levels; ++l) {
         const int32_t *f = factors + 3 * (l - 1);
@@ -360,7 +375,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
                         model->n_in, s) != hipSuccess)
             return OCTNCA_EHIP;
     }
-    int cur = (int)(((int64_t)(levels - 1) + total_steps - n_fused) & 1);
+    int cur = (int)(flips & 1);
     if (launch_upsample(dt, nullptr, ext3(p.ext[levels - 1]), 1, 1, 1, img[levels - 1], bufs[cur],
                         model->n_in, model->channels, s) != hipSuccess)
         return OCTNCA_EHIP;
@@ -388,7 +403,8 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
         st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, t0, steps[l],
                        seed, threshold, s, batch);
         if (st) return st;
-        cur ^= (steps[l] - t0) & 1;
+        cur ^= level_launches(step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch),
+                              t0, steps[l]) & 1;
         if (level_events && level_events[2 * l + 1] &&
             hipEventRecord((hipEvent_t)level_events[2 * l + 1], s) != hipSuccess)
             return OCTNCA_EHIP;
@@ -725,25 +741,39 @@ namespace octnca {
 //   "mfma_f16"      matrix-core kernel with fp16 operands (fp16 states only);
 //   "mfma_rows", "mfma_tiles"  the default kernel with the 2D work layout
 //                   forced to row streaming or to 16 x 32 tiles;
-//   "valu"          one thread per cell, fp32 FMAs on the vector ALUs.
+//   "mfma_1step"    the default kernel, one step per launch (no two-step
+//                   launches on large 2D fp32 levels);
+//   "valu"          one thread per cell, fp32 FMAs on the vector ALUs;
+// or a comma-separated combination of them (e.g. "mfma_rows,mfma_1step").
 struct Selection {
-    bool ok = true, valu = false;
+    bool ok = true, valu = false, pairs = true;
     MfmaMlp mlp = MfmaMlp::Default;
     Layout2d layout = Layout2d::Auto;
 };
 
 Selection select_step_kernel() {
     Selection r;
-    const char *sel = getenv("OCTREE_NCA_STEP_KERNEL");
-    if (sel == nullptr || sel[0] == 0 || strcmp(sel, "mfma") == 0) return r;
-    if (strcmp(sel, "valu") == 0) r.valu = true;
-    else if (strcmp(sel, "mfma_f32") == 0) r.mlp = MfmaMlp::F32;
-    else if (strcmp(sel, "mfma_bf16x3") == 0) r.mlp = MfmaMlp::Bf16x3;
-    else if (strcmp(sel, "mfma_f16") == 0) r.mlp = MfmaMlp::F16;
-    else if (strcmp(sel, "mfma_f16s") == 0) r.mlp = MfmaMlp::F16S;
-    else if (strcmp(sel, "mfma_rows") == 0) r.layout = Layout2d::Rows;
-    else if (strcmp(sel, "mfma_tiles") == 0) r.layout = Layout2d::Tiles;
-    else r.ok = false;
+    const char *env = getenv("OCTREE_NCA_STEP_KERNEL");
+    if (env == nullptr) return r;
+    // a comma-separated list of the names above, e.g. "mfma_rows,mfma_1step"
+    const char *p = env;
+    while (true) {
+        const char *e = strchr(p, ',');
+        const size_t len = e ? (size_t)(e - p) : strlen(p);
+        auto is = [&](const char *name) { return strlen(name) == len && strncmp(p, name, len) == 0; };
+        if (len == 0 || is("mfma")) {
+        } else if (is("valu")) r.valu = true;
+        else if (is("mfma_f32")) r.mlp = MfmaMlp::F32;
+        else if (is("mfma_bf16x3")) r.mlp = MfmaMlp::Bf16x3;
+        else if (is("mfma_f16")) r.mlp = MfmaMlp::F16;
+        else if (is("mfma_f16s")) r.mlp = MfmaMlp::F16S;
+        else if (is("mfma_rows")) r.layout = Layout2d::Rows;
+        else if (is("mfma_tiles")) r.layout = Layout2d::Tiles;
+        else if (is("mfma_1step")) r.pairs = false;
+        else r.ok = false;
+        if (e == nullptr) break;
+        p = e + 1;
+    }
     return r;
 }
 
@@ -755,6 +785,16 @@ hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_
     if (!sel.ok) return hipErrorInvalidValue;
     if (sel.valu) return launch_step_valu(a, src, dst, stream);
     return launch_step_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+}
+
+bool step_pairs(const StepArgs &a) {
+    const Selection sel = select_step_kernel();
+    return sel.ok && !sel.valu && sel.pairs && step_mfma_pairs(a, sel.mlp, sel.layout);
+}
+
+hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+    const Selection sel = select_step_kernel();
+    return launch_step2_mfma(a, sel.mlp, sel.layout, src, dst, stream);
 }
 
 bool step_fuses_upsample(const StepArgs &a) {

@@ -56,6 +56,10 @@ hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, i
                           int fz, int fy, int fx, const void *img, void *dst,
                           hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+// Whether launch_step_pair runs steps a.step and a.step + 1 in one launch, and
+// that launch (the state after step a.step is not written to memory).
+bool step_pairs(const StepArgs &a);
+hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 
 // Training (fp32 states): backward of one step (state `src` before the step,
 // gout = dL/dS'), writing gin = dL/dS (may alias gout) and adding the weight
@@ -87,6 +91,12 @@ hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, con
 // for `a`; launch_step_mfma_up then reads the coarse state (width coarse_w,
 // factors fy, fx) and the level's image instead of a state of the level.
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
+// Two steps, a.step and a.step + 1, in one launch (2D fp32 row layout, default
+// operand policy): step_mfma_pairs says whether that kernel exists for `a`;
+// launch_step2_mfma reads src and writes the state after both steps to dst.
+bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
+hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
+                             void *dst, hipStream_t stream);
 hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *coarse,
                                int coarse_h, int coarse_w, int fz, int fy, int fx,
                                const void *img, void *dst, hipStream_t stream);

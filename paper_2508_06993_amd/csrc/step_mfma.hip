@@ -992,7 +992,8 @@ struct RowStream {
 #pragma unroll
         for (int k = 0; k < kBody; ++k) {
             const int cx = x0 + k * kCellsPerBody + cell;
-            const uint32_t off = cx < dw ? (uint32_t)cx * kCellBytes + (uint32_t)chunk * 16 : kOut;
+            const uint32_t off =
+                cx >= 0 && cx < dw ? (uint32_t)cx * kCellBytes + (uint32_t)chunk * 16 : kOut;
             const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
             v[k] = make_uint4(x[0], x[1], x[2], x[3]);
         }
@@ -1277,6 +1278,252 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             __builtin_amdgcn_sched_barrier(0);
             commit(ra, ia, ring[(q + 2) & 3]);
             commit(rb, ib, ring[(q + 3) & 3]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// 2D, two steps per launch (temporal fusion).  The fire mask is a function of
+// (seed, level, step, cell) alone, so a wave can run step t + 1 on its own
+// copy of step t's result.  Same row streaming as nca_step_mfma_2d_rows, with
+// the strip narrowed to 30 output cells: the wave loads 34-cell halo rows
+// (cells x0 - 2 .. x0 + 31), runs step t on the 32 cells x0 - 1 .. x0 + 30 and
+// writes each finished row into a second LDS ring of two slots (cells and
+// rows outside the grid as 0: the zero padding of step t + 1's perception).
+// Step t + 1 folds those rows into its own rolling sums and finishes cells
+// x0 .. x0 + 31, of which x0 .. x0 + 29 are stored (the last two lack their
+// right neighbours).  Per input row q: step t folds q and finishes q - 1, then
+// step t + 1 folds q - 1 and finishes q - 2.  The state between the two steps
+// never reaches HBM, so HBM sees one read and one write of the state per two
+// steps, for 32/30 of the MLP work and 2 halo rows of step t per run; the
+// results equal two single-step launches bit for bit (the same operations in
+// the same order).
+// ---------------------------------------------------------------------------
+constexpr int k2PairW = kTileW - 2;   // output cells per strip
+
+template <typename T, int NIN, class Mlp>
+__global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
+    const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int run_rows,
+    int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
+    const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
+    static_assert(std::is_same_v<T, float>, "the intermediate ring holds fp32 states");
+    using RS = RowStream<T>;
+    // Row r of a work item (first input row `base`) lives in slot
+    // (r - base) % 3 of each ring: input rows, and step t's output rows.
+    __shared__ float4 ring[3][RS::kSlotWords];
+    __shared__ float4 mid[3][RS::kSlotWords];
+    __shared__ float4 tapw[9][4];                // [tap][quad] conv weights of channels 4q..4q+3
+    // fire ballots of the work item: [step t / t + 1][block of 12 rows][b]
+    constexpr int kOpr = 5, kEvalRows = 12;
+    constexpr int kEvalBlocks = (k2RunRows + 2 + kEvalRows - 1) / kEvalRows;
+    __shared__ uint64_t fire_words[2][kEvalBlocks][8];
+
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 15;
+    const int g = lane >> 4;
+
+    {
+        const int i = min(lane, 9 * 4 - 1);
+        const int t = i / 4, q = i % 4;
+        constexpr float ps = Mlp::kPerceptionScale;
+        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
+                                      ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
+        if (lane < 9 * 4) tapw[t][q] = tw;
+    }
+    // Slots 32 and 33 of the step-t ring are never written: the two cells
+    // per quad that step t + 1 computes but does not store read them.
+    if (lane < 24) mid[lane >> 3][((lane >> 1) & 3) * RS::PS + 32 + (lane & 1)] = make_float4(0.f, 0.f, 0.f, 0.f);
+    Mlp mlp;
+    mlp.load(w1, b1, w2, n, g, NIN);
+    float cb[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
+    mlp.pin_all();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) pin(cb[k]);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // Fire evaluations: a strip row spans at most 5 blocks of 8 cells (it may
+    // start anywhere within a block), so an evaluation gives 5 lanes to each of
+    // 12 rows of one step (lanes 60..63 repeat row 11).  All evaluations of a
+    // work item run at its start, where few registers are live, and leave
+    // their 8 ballots in LDS; a cell reads ballot (idx & 7) of its row's block.
+    const int ev_row = min(lane / kOpr, kEvalRows - 1), ev_blk = lane % kOpr;
+    auto evaluate = [&](int s, int blk, uint32_t st, int y_first, uint32_t xs) {
+        const int yy = min(max(y_first + ev_row, 0), dh - 1);
+        const uint64_t b0 = (((uint64_t)yy * dw + xs) >> 3) + ev_blk;
+        const FireBallots fb = fire_ballots(b0, st, level, batch, seed, threshold);
+        uint64_t word = fb.w[0];
+#pragma unroll
+        for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
+        fire_words[s][blk][lane & 7] = word;   // 8 lanes per address, same value
+    };
+    // Bit of cell idx in row `rel` (rows from the step's first row) of step s;
+    // 2D cell indices fit 32 bits (two fp32 states of 2^32 cells would need
+    // 512 GB).  Rows outside the step's range read some in-range word.
+    auto fire_bit = [&](int s, int rel, uint32_t idx, uint32_t row_b0) {
+        rel = min(max(rel, 0), kEvalBlocks * kEvalRows - 1);
+        const uint64_t fw = fire_words[s][rel / kEvalRows][idx & 7];
+        return (bool)((fw >> ((rel % kEvalRows) * kOpr + (int)((idx >> 3) - row_b0))) & 1);
+    };
+    constexpr int kCellBytes = RS::kCellBytes;
+    const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
+    int gq = g;
+    RS ra, rb;
+
+    for (int item = blockIdx.x; item < items; item += gridDim.x) {
+        const int sx = item % strips;
+        const int ry = item / strips;
+        const int x0 = sx * k2PairW;
+        const int x1 = x0 - 1;             // first cell of step t's strip
+        const uint32_t xs1 = (uint32_t)max(x1, 0);
+        const int y_begin = ry * run_rows;
+        const int y_end = min(dh, y_begin + run_rows);
+        const int x_stop = min(dw, x0 + k2PairW);
+        const int base = y_begin - 2;      // first input row
+
+        // Rolling perception sums (bias included): A[(r - base) % 3] holds
+        // step t's sum of output row r, B[(r - base) % 3] step t + 1's.  The
+        // loop body is unrolled three times, so the three sums of a step
+        // rotate roles without register moves.
+        float A[3][2][4], B[3][2][4];
+
+        ra.issue(src, base, dh, dw, x1);
+        rb.issue(src, base + 1, dh, dw, x1);
+        // step t's rows y_begin - 1 .. y_end, step t + 1's y_begin .. y_end - 1
+        for (int e = 0; e < 2 * kEvalBlocks; ++e) {
+            const int st = e >= kEvalBlocks ? 1 : 0;
+            const int blk = e - st * kEvalBlocks;
+            const int y_first = y_begin - 1 + st + blk * kEvalRows;
+            if (y_first <= y_end - st)
+                evaluate(st, blk, step + st, y_first, st ? (uint32_t)x0 : xs1);
+        }
+        ra.commit(ring[0]);
+        rb.commit(ring[1]);
+
+        // Row r of a plane set with its x taps: output r + 1 takes the dy = -1
+        // weights (its first contribution, started from the bias), r the
+        // dy = 0 ones and r - 1 the dy = +1 ones (its last).
+        auto fold = [&](const float4 *pl, float (&first)[2][4], float (&second)[2][4],
+                        float (&last)[2][4]) {
+            pin(gq);   // re-read the tap weights every row instead of keeping 36 registers
+#pragma unroll
+            for (int dx = 0; dx < 3; ++dx) {
+                const float4 wm = tapw[dx][gq];
+                const float4 w0 = tapw[3 + dx][gq];
+                const float4 wp = tapw[6 + dx][gq];
+                const float a_m[4] = {wm.x, wm.y, wm.z, wm.w};
+                const float a_0[4] = {w0.x, w0.y, w0.z, w0.w};
+                const float a_p[4] = {wp.x, wp.y, wp.z, wp.w};
+#pragma unroll
+                for (int grp = 0; grp < 2; ++grp) {
+                    const float4 v = pl[grp * 16 + n + dx];
+                    const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        first[grp][k] = fmaf(a_m[k], vv[k], dx == 0 ? cb[k] : first[grp][k]);
+                        second[grp][k] = fmaf(a_0[k], vv[k], second[grp][k]);
+                        last[grp][k] = fmaf(a_p[k], vv[k], last[grp][k]);
+                    }
+                }
+            }
+        };
+
+        // Step t, row yo (complete in p) -> mid ring.  Rows y_begin - 1 ..
+        // y_end are the ones step t + 1 reads; earlier rows are pipeline
+        // start-up whose values are never used.
+        auto finish_a = [&](int yo, int slot, const float (&p)[2][4]) {
+            const bool row_in = yo >= 0 && yo < dh;
+            const uint32_t rowc = (uint32_t)min(max(yo, 0), dh - 1) * (uint32_t)dw;
+            const uint32_t row_b0 = (rowc + xs1) >> 3;
+            const float4 *own = ring[slot] + g * RS::PS;
+            float4 *out = mid[slot] + g * RS::PS;
+            v4f acc[2][4];
+            float f[2][8];
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const float4 sv = own[1 + grp * 16 + n];
+                f[grp][0] = sv.x; f[grp][1] = sv.y; f[grp][2] = sv.z; f[grp][3] = sv.w;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[grp][4 + k] = p[grp][k];
+                mlp.layer1(f[grp], acc[grp]);
+            }
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const v4f u = mlp.layer2(acc[grp]);
+                const int x = x1 + grp * 16 + n;
+                const bool in = row_in && x >= 0 && x < dw;
+                const float m =
+                    fire_bit(0, yo - (y_begin - 1), rowc + (uint32_t)max(x, 0), row_b0) ? 1.f : 0.f;
+                float v[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) v[k] = in ? fmaf(m, u[k], f[grp][k]) : 0.f;
+                out[grp * 16 + n] = make_float4(v[0], v[1], v[2], v[3]);
+            }
+        };
+
+        // Step t + 1, row yo (complete in p): MLP, fire gate and store; rows
+        // outside [y_begin, y_end) are dropped by an empty descriptor.
+        auto finish_b = [&](int yo, int slot, const float (&p)[2][4]) {
+            const bool out_ok = yo >= y_begin && yo < y_end;
+            const int yc = min(max(yo, 0), dh - 1);
+            const uint32_t rowc = (uint32_t)yc * (uint32_t)dw;
+            const uint32_t row_b0 = (rowc + (uint32_t)x0) >> 3;
+            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
+            const float4 *own = mid[slot] + g * RS::PS;
+            v4f acc[2][4];
+            float f[2][8];
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const float4 sv = own[1 + grp * 16 + n];
+                f[grp][0] = sv.x; f[grp][1] = sv.y; f[grp][2] = sv.z; f[grp][3] = sv.w;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) f[grp][4 + k] = p[grp][k];
+                mlp.layer1(f[grp], acc[grp]);
+            }
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp) {
+                const v4f u = mlp.layer2(acc[grp]);
+                const int x = x0 + grp * 16 + n;
+                const uint32_t off = x < x_stop ? (uint32_t)x * kCellBytes : kOut;
+                update_store(dst, wr, off, g, f[grp], u,
+                             fire_bit(1, yo - y_begin, rowc + (uint32_t)x, row_b0));
+            }
+        };
+
+        // One input row q per body, from base through y_end + 1 (rounded up
+        // to whole groups of three): step t finishes row q - 1, step t + 1 row
+        // q - 2.  Row q + 2 is loaded during the body and written to the slot
+        // of row q - 1 at its end.
+        auto body = [&](int q, auto jc) {
+            constexpr int j = decltype(jc)::value;   // (q - base) % 3
+            constexpr int jm = (j + 2) % 3, jp = (j + 1) % 3;   // rows q - 1, q + 1 (= q - 2)
+            ra.issue(src, q + 2, dh, dw, x1);
+            // input row q: outputs q + 1, q, q - 1 of step t
+            fold(ring[j] + g * RS::PS, A[jp], A[j], A[jm]);
+            finish_a(q - 1, jm, A[jm]);
+            __builtin_amdgcn_sched_barrier(0);
+            // step t's row q - 1: outputs q, q - 1, q - 2 of step t + 1
+            fold(mid[jm] + g * RS::PS, B[j], B[jm], B[jp]);
+            finish_b(q - 2, jp, B[jp]);
+            __builtin_amdgcn_sched_barrier(0);
+            ra.commit(ring[jm]);
+        };
+        // The first bodies see sums that were never started (rows before
+        // base); they only feed rows that are not used.
+#pragma unroll
+        for (int i = 0; i < 3; ++i)
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) A[i][grp][k] = B[i][grp][k] = cb[k];
+        for (int q0 = base; q0 <= y_end + 1; q0 += 3) {
+            body(q0, std::integral_constant<int, 0>{});
+            body(q0 + 1, std::integral_constant<int, 1>{});
+            body(q0 + 2, std::integral_constant<int, 2>{});
         }
     }
 }
@@ -1797,6 +2044,38 @@ hipError_t launch_rows(const StepArgs &a, const void *src, void *dst, const void
     return hipGetLastError();
 }
 
+// Two-step row kernel: strips of 30 output cells; used where the single-step
+// kernel would use the row layout (fp32 states, default MLP).
+RowsPlan pair_plan(const StepArgs &a) {
+    RowsPlan r;
+    r.tiles_x = (int)((a.ext.w + k2PairW - 1) / k2PairW);
+    r.slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
+    r.runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
+    r.items = (int64_t)r.tiles_x * r.runs;
+    return r;
+}
+
+bool uses_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
+    return a.ndim == 2 && a.dtype == Dtype::F32 && a.channels == kC && a.hidden == kH &&
+           a.ext.h * a.ext.w < (int64_t(1) << 32) &&   // 32-bit cell indices in the kernel
+           (mlp == MfmaMlp::Default || mlp == MfmaMlp::F16S) &&
+           (layout == Layout2d::Rows ||
+            (layout == Layout2d::Auto && pair_plan(a).items >= pair_plan(a).slots));
+}
+
+template <int NIN>
+hipError_t launch_rows_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+    const RowsPlan r = pair_plan(a);
+    if (r.items == 0) return hipSuccess;
+    if (r.items > INT32_MAX) return hipErrorInvalidValue;
+    const int grid = (int)std::min<int64_t>(r.items, r.slots);
+    nca_step2_mfma_2d_rows<float, NIN, MlpF32State><<<grid, 64, 0, stream>>>(
+        (const float *)src, (float *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, k2RunRows,
+        (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
+        a.seed, a.threshold);
+    return hipGetLastError();
+}
+
 template <typename T, int NIN, class Mlp>
 hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *dst,
                      hipStream_t stream) {
@@ -1896,6 +2175,18 @@ bool mfma_fits(const StepArgs &a) {
     // more than (2^32 / 18 rows) bytes go to the vector kernel instead.
     const int64_t cell_bytes = (int64_t)kC * (a.dtype == Dtype::F32 ? 4 : 2);
     return (int64_t)(k2TY + 2) * a.ext.w * cell_bytes < (int64_t(1) << 32);
+}
+
+bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
+    return mfma_fits(a) && uses_pairs(a, mlp, layout);
+}
+
+hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
+                             void *dst, hipStream_t stream) {
+    if (!step_mfma_pairs(a, mlp, layout)) return hipErrorInvalidValue;
+    if (a.n_in == 1) return launch_rows_pair<1>(a, src, dst, stream);
+    if (a.n_in == 3) return launch_rows_pair<3>(a, src, dst, stream);
+    return hipErrorInvalidValue;
 }
 
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {

@@ -1,0 +1,88 @@
+"""Two steps per launch on large 2D fp32 levels (temporal fusion; legal because
+the fire mask is a function of seed, level, step and cell alone).
+
+The two-step row kernel keeps step t's state in LDS and runs step t + 1 on it,
+with the same operations in the same order as one launch per step, so its
+result must equal the single-step launches bit for bit: checked on ragged
+strips (widths around multiples of the 30-cell strip, widths not divisible by
+8), short and ragged runs of rows, one- and three-channel images, odd and even
+step counts and fire rates 0, 1/2 and 1.  Its parity with the oracle follows
+from that and from the single-step kernel's own parity tests (and is also
+tested directly by the "mfma_rows" step-kernel cases of the other suites and by
+the full-size pathology boxes, where the two-step launches are the default)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2508_06993_amd as octnca
+from paper_2508_06993_amd.runtime import upload_weights
+from synthetic import LevelWeights
+
+pytestmark = pytest.mark.gpu
+
+C, H = 16, 64
+
+
+def rand_weights(rng, scale=0.3):
+    return LevelWeights(
+        conv_w=rng.normal(0, scale, (C, 9)).astype(np.float32),
+        conv_b=rng.normal(0, scale, (C,)).astype(np.float32),
+        w1=rng.normal(0, scale, (H, 2 * C)).astype(np.float32),
+        b1=rng.normal(0, scale, (H,)).astype(np.float32),
+        w2=rng.normal(0, scale, (C, H)).astype(np.float32))
+
+
+def run(monkeypatch, kernel, state, w, n_in, steps, rate, level=1, seed=5):
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
+    b0 = state.clone()
+    b1 = torch.full_like(b0, float("nan"))
+    which = octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=n_in), b0, b1,
+                                        upload_weights([w])[0], level, steps, rate, seed)
+    torch.cuda.synchronize()
+    return (b1 if which else b0), which
+
+
+SHAPES = [(1, 1, 1), (1, 2, 29), (1, 3, 30), (1, 5, 31), (1, 9, 59), (1, 33, 61),
+          (1, 131, 95), (1, 257, 67), (1, 140, 600)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[1]}x{s[2]}")
+@pytest.mark.parametrize("n_in", [1, 3])
+def test_two_step_launches_equal_single_steps(gpu, monkeypatch, shape, n_in):
+    rng = np.random.default_rng(hash((shape, n_in)) % 2**32)
+    w = rand_weights(rng)
+    s = torch.from_numpy(rng.normal(0, 1, shape + (C,)).astype(np.float32)).cuda()
+    for steps in (1, 2, 5):
+        print(f"two-step shape={shape} n_in={n_in} steps={steps}", flush=True)
+        got, which = run(monkeypatch, "mfma_rows", s, w, n_in, steps, 0.5)
+        want, which1 = run(monkeypatch, "mfma_rows,mfma_1step", s, w, n_in, steps, 0.5)
+        assert which1 == steps % 2
+        assert which == ((steps + 1) // 2) % 2
+        assert torch.equal(got, want), (shape, n_in, steps)
+        # the input channels are never written
+        assert torch.equal(got[..., :n_in], s[..., :n_in])
+
+
+@pytest.mark.parametrize("rate", [0.0, 1.0])
+def test_two_step_fire_rate_extremes(gpu, monkeypatch, rate):
+    rng = np.random.default_rng(7)
+    w = rand_weights(rng)
+    s = torch.from_numpy(rng.normal(0, 1, (1, 70, 97, C)).astype(np.float32)).cuda()
+    got, _ = run(monkeypatch, "mfma_rows", s, w, 3, 4, rate)
+    want, _ = run(monkeypatch, "mfma_rows,mfma_1step", s, w, 3, 4, rate)
+    assert torch.equal(got, want)
+    if rate == 0.0:
+        assert torch.equal(got, s)
+
+
+def test_two_step_default_on_a_large_level(gpu, monkeypatch):
+    """A level large enough for the default layout to pick the row kernel (and
+    with it the two-step launches): 4096 x 1920 cells, strips x runs = 2048."""
+    rng = np.random.default_rng(8)
+    w = rand_weights(rng, scale=0.2)
+    g = torch.Generator(device="cuda").manual_seed(3)
+    s = torch.randn((1, 4096, 1920, C), generator=g, device="cuda", dtype=torch.float32)
+    got, which = run(monkeypatch, "mfma", s, w, 3, 3, 0.5, level=0)
+    want, which1 = run(monkeypatch, "mfma_1step", s, w, 3, 3, 0.5, level=0)
+    assert (which, which1) == (0, 1)   # 2 launches against 3
+    assert torch.equal(got, want)
