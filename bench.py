@@ -372,7 +372,10 @@ def main(argv=None):
         for l in range(L):
             if wl.steps[l] > 0:
                 step_ms += row[2 * l].elapsed_time(row[2 * l + 1])
-    launches = args.steps * sum(wl.steps)
+    # step-kernel launches of a pass as the library enqueues them (a launch
+    # runs one step, or two on large 2D fp32 levels)
+    launches = args.steps * sum(octnca.octree_nca_infer_launches(model, wl.extent, wl.factors,
+                                                                 wl.steps))
     avg_launch_ms = step_ms / launches
     flop = algorithmic_flop_per_cell_step(wl) * cell_steps * args.steps
     byts = algorithmic_bytes_per_cell_step(wl) * cell_steps * args.steps

@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define OCTNCA_ABI_VERSION 3
+#define OCTNCA_ABI_VERSION 4
 
 typedef enum {
     OCTNCA_OK = 0,
@@ -136,16 +136,19 @@ int octree_nca_upsample(const octnca_model *model, const void *coarse_state,
                         void *fine_state, void *stream);
 
 /* Run `steps` NCA steps t = 0 .. steps-1 of one level (Sec. 3.1; supplement
- * S3, Listing 1), out of place, alternating between two buffers:
- * step t reads bufs[t % 2] and writes bufs[(t+1) % 2].
+ * S3, Listing 1), out of place, alternating between two buffers: launch k
+ * reads bufs[k % 2] and writes bufs[(k+1) % 2].  A launch runs one step, or
+ * two (t, t+1) on large 2D fp32 levels, where the state after step t stays
+ * on chip; the results are the same.
  *   buf0     [extent][C], the level's state on entry.
  *   buf1     [extent][C], scratch of the same size; must not overlap buf0.
  *   weights  host pointer to one octnca_level_weights (device arrays).
  *   level    the level index, used only by the fire mask (0 = finest).
  *   steps    >= 0; 0 leaves buf0 as it is.
  *   fire_rate in [0, 1]; seed: fire-mask key.
- *   result_in_buf1  host, may be NULL: set to steps % 2, i.e. 1 when the
- *            final state is in buf1, 0 when it is in buf0.
+ *   result_in_buf1  host, may be NULL: set to the parity of the number of
+ *            launches, i.e. 1 when the final state is in buf1, 0 when it is
+ *            in buf0 (steps % 2 with one step per launch).
  * Errors: EINVAL, ESHAPE, EUNSUPPORTED, EHIP. */
 int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1,
                          octnca_extent extent, const octnca_level_weights *weights,
@@ -202,6 +205,15 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
                      const octnca_level_weights *weights, const int32_t *steps,
                      float fire_rate, uint64_t seed, void *workspace, size_t workspace_bytes,
                      void *final_state, uint8_t *seg, void *const *level_events, void *stream);
+
+/* Step-kernel launches that octree_nca_infer enqueues for each level with the
+ * step kernel selected at the time of the call (a measurement aid: the
+ * launches of a level add up to its steps, one or two steps per launch).
+ *   launches  host, [L], written: launches[l] for level l (index 0 = finest).
+ * Host only: enqueues nothing.  Errors: EINVAL (null pointer, a negative
+ * step count), ESHAPE, EUNSUPPORTED. */
+int octree_nca_infer_launches(const octnca_model *model, octnca_extent finest, int32_t levels,
+                              const int32_t *factors, const int32_t *steps, int32_t *launches);
 
 /* Inference of a batch of images of the same extent (the paper's kernel
  * works on one image and notes that a batch is an extra dimension to iterate

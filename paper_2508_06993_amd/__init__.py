@@ -22,7 +22,8 @@ __all__ = [
     "OctreeNCAError", "Model", "lib", "library_path", "level_weights_struct",
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
-    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_infer_launches",
+    "octree_nca_first_level_steps",
     "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
     "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
     "octree_nca_upsample_backward", "octree_nca_readout_mse_workspace_bytes",
@@ -39,7 +40,8 @@ OCTNCA_F32, OCTNCA_F16 = 0, 1
 EXPORTED_SYMBOLS = (
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
-    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_first_level_steps",
+    "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_infer_launches",
+    "octree_nca_first_level_steps",
     "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
     "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
     "octree_nca_upsample_backward", "octree_nca_readout_mse_workspace_bytes",
@@ -87,6 +89,9 @@ _SIGS = {
     "octree_nca_readout_classes": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32, _P, _P]),
     "octree_nca_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(_Model), _Extent, _I32,
                                                      ctypes.POINTER(_I32), _I32]),
+    "octree_nca_infer_launches": (_I32, [ctypes.POINTER(_Model), _Extent, _I32,
+                                         ctypes.POINTER(_I32), ctypes.POINTER(_I32),
+                                         ctypes.POINTER(_I32)]),
     "octree_nca_infer": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32, ctypes.POINTER(_I32),
                                 ctypes.POINTER(_LevelWeights), ctypes.POINTER(_I32),
                                 ctypes.c_float, ctypes.c_uint64, _P, ctypes.c_size_t, _P, _P,
@@ -290,6 +295,17 @@ def octree_nca_workspace_bytes(model: Model, finest, factors, with_final_state=T
     if n == 0:
         raise OctreeNCAError("octree_nca_workspace_bytes: invalid arguments", OCTNCA_EINVAL)
     return int(n)
+
+
+def octree_nca_infer_launches(model: Model, finest, factors, steps) -> list:
+    """Step-kernel launches per level (index 0 = finest) that octree_nca_infer
+    enqueues with the step kernel selected now."""
+    levels = len(factors) + 1
+    out = (_I32 * levels)()
+    st = lib().octree_nca_infer_launches(ctypes.byref(model.struct()), _extent(finest), levels,
+                                         _factors(factors), (_I32 * levels)(*steps), out)
+    _check(st, "octree_nca_infer_launches")
+    return [int(v) for v in out]
 
 
 def octree_nca_infer(model: Model, image, factors, weights, steps, fire_rate: float, seed: int,

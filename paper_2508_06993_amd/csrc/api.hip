@@ -315,6 +315,23 @@ size_t octree_nca_workspace_bytes(const octnca_model *model, octnca_extent fines
     return p.bytes;
 }
 
+int octree_nca_infer_launches(const octnca_model *model, octnca_extent finest, int32_t levels,
+                              const int32_t *factors, const int32_t *steps, int32_t *launches) {
+    Plan p;
+    const int st = make_plan(model, finest, levels, factors, true, &p);
+    if (st) return st;
+    if (steps == nullptr || launches == nullptr) return OCTNCA_EINVAL;
+    for (int l = 0; l < levels; ++l)
+        if (steps[l] < 0) return OCTNCA_EINVAL;
+    const octnca_level_weights none{};
+    for (int l = 0; l < levels; ++l) {
+        const StepArgs a = step_args(model, p.ext[l], &none, l, 0, 0, 0);
+        const bool fused = l + 1 < levels && steps[l] >= 1 && step_fuses_upsample(a);
+        launches[l] = (fused ? 1 : 0) + level_launches(a, fused ? 1 : 0, steps[l]);
+    }
+    return OCTNCA_OK;
+}
+
 }  // extern "C"
 
 namespace {

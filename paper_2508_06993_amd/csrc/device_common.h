@@ -26,10 +26,17 @@ struct Philox4x64Out {
     uint64_t w[4];
 };
 
-// 64 x 64 -> 128-bit product as (hi, lo).
+// 64 x 64 -> 128-bit product as (hi, lo), from four 32 x 32 -> 64-bit
+// products with 64-bit addends (one multiply-add each; no partial sum
+// overflows: (2^32 - 1)^2 + 2 (2^32 - 1) < 2^64).
 __device__ __forceinline__ void mul_wide_u64(uint64_t a, uint64_t b, uint64_t &hi, uint64_t &lo) {
-    lo = a * b;
-    hi = __umul64hi(a, b);
+    const uint32_t a0 = (uint32_t)a, a1 = (uint32_t)(a >> 32);
+    const uint32_t b0 = (uint32_t)b, b1 = (uint32_t)(b >> 32);
+    const uint64_t p0 = (uint64_t)a0 * b0;
+    const uint64_t t1 = (uint64_t)a0 * b1 + (p0 >> 32);
+    const uint64_t t2 = (uint64_t)a1 * b0 + (uint32_t)t1;
+    lo = (t2 << 32) | (uint32_t)p0;
+    hi = (uint64_t)a1 * b1 + (t1 >> 32) + (t2 >> 32);
 }
 
 __device__ __forceinline__ Philox4x64Out philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,

@@ -1310,14 +1310,18 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     static_assert(std::is_same_v<T, float>, "the intermediate ring holds fp32 states");
     using RS = RowStream<T>;
     // Row r of a work item (first input row `base`) lives in slot
-    // (r - base) % 3 of each ring: input rows, and step t's output rows.
+    // (r - base) % 3 of the input ring and (r - base) % 2 of the ring of step
+    // t's output rows.
     __shared__ float4 ring[3][RS::kSlotWords];
-    __shared__ float4 mid[3][RS::kSlotWords];
+    __shared__ float4 mid[2][RS::kSlotWords];
     __shared__ float4 tapw[9][4];                // [tap][quad] conv weights of channels 4q..4q+3
-    // fire ballots of the work item: [step t / t + 1][block of 12 rows][b]
+    // Fire bits of the work item, [step t / t + 1][row]: byte o of a row's
+    // word holds the 8 draws of the o-th block of 8 cells from the block that
+    // contains the row's first strip cell.
     constexpr int kOpr = 5, kEvalRows = 12;
     constexpr int kEvalBlocks = (k2RunRows + 2 + kEvalRows - 1) / kEvalRows;
-    __shared__ uint64_t fire_words[2][kEvalBlocks][8];
+    constexpr int kMaskRows = kEvalBlocks * kEvalRows;
+    __shared__ uint64_t fire_rows[2][kMaskRows];
 
     const int lane = threadIdx.x & 63;
     const int n = lane & 15;
@@ -1333,7 +1337,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     }
     // Slots 32 and 33 of the step-t ring are never written: the two cells
     // per quad that step t + 1 computes but does not store read them.
-    if (lane < 24) mid[lane >> 3][((lane >> 1) & 3) * RS::PS + 32 + (lane & 1)] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (lane < 16) mid[lane >> 3][((lane >> 1) & 3) * RS::PS + 32 + (lane & 1)] = make_float4(0.f, 0.f, 0.f, 0.f);
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
@@ -1349,25 +1353,25 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     // Fire evaluations: a strip row spans at most 5 blocks of 8 cells (it may
     // start anywhere within a block), so an evaluation gives 5 lanes to each of
     // 12 rows of one step (lanes 60..63 repeat row 11).  All evaluations of a
-    // work item run at its start, where few registers are live, and leave
-    // their 8 ballots in LDS; a cell reads ballot (idx & 7) of its row's block.
+    // work item run at its start, where few registers are live; each lane
+    // writes the 8 fire bits of its block as one byte of its row's word.
     const int ev_row = min(lane / kOpr, kEvalRows - 1), ev_blk = lane % kOpr;
     auto evaluate = [&](int s, int blk, uint32_t st, int y_first, uint32_t xs) {
         const int yy = min(max(y_first + ev_row, 0), dh - 1);
         const uint64_t b0 = (((uint64_t)yy * dw + xs) >> 3) + ev_blk;
-        const FireBallots fb = fire_ballots(b0, st, level, batch, seed, threshold);
-        uint64_t word = fb.w[0];
+        const Philox4x64Out r = philox4x64_10(b0, st, level, batch, seed, 0);
+        uint32_t bits = 0;
 #pragma unroll
-        for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
-        fire_words[s][blk][lane & 7] = word;   // 8 lanes per address, same value
+        for (int c = 0; c < 8; ++c) bits |= ((uint64_t)draw_of(r, (uint32_t)c) < threshold ? 1u : 0u) << c;
+        reinterpret_cast<uint8_t *>(&fire_rows[s][blk * kEvalRows + ev_row])[ev_blk] = (uint8_t)bits;
     };
-    // Bit of cell idx in row `rel` (rows from the step's first row) of step s;
-    // 2D cell indices fit 32 bits (two fp32 states of 2^32 cells would need
-    // 512 GB).  Rows outside the step's range read some in-range word.
-    auto fire_bit = [&](int s, int rel, uint32_t idx, uint32_t row_b0) {
-        rel = min(max(rel, 0), kEvalBlocks * kEvalRows - 1);
-        const uint64_t fw = fire_words[s][rel / kEvalRows][idx & 7];
-        return (bool)((fw >> ((rel % kEvalRows) * kOpr + (int)((idx >> 3) - row_b0))) & 1);
+    // Fire bit of strip cell c (c = x - xs >= 0) in row `rel` (rows from the
+    // step's first row) of step s, whose row starts at canonical index rowc:
+    // bit c + ((rowc + xs) & 7) of the row's word.  2D cell indices fit 32
+    // bits (two fp32 states of 2^32 cells would need 512 GB).  Rows outside
+    // the step's range read some in-range word.
+    auto row_word = [&](int s, int rel) {
+        return fire_rows[s][min(max(rel, 0), kMaskRows - 1)];
     };
     constexpr int kCellBytes = RS::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
@@ -1438,9 +1442,10 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
         auto finish_a = [&](int yo, int slot, const float (&p)[2][4]) {
             const bool row_in = yo >= 0 && yo < dh;
             const uint32_t rowc = (uint32_t)min(max(yo, 0), dh - 1) * (uint32_t)dw;
-            const uint32_t row_b0 = (rowc + xs1) >> 3;
+            const int sh = (int)((rowc + xs1) & 7u) + (x1 - (int)xs1);   // bit of cell x1
+            const uint64_t fw = row_word(0, yo - (y_begin - 1));
             const float4 *own = ring[slot] + g * RS::PS;
-            float4 *out = mid[slot] + g * RS::PS;
+            float4 *out = mid[(yo - base) & 1] + g * RS::PS;
             v4f acc[2][4];
             float f[2][8];
 #pragma unroll
@@ -1456,8 +1461,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x1 + grp * 16 + n;
                 const bool in = row_in && x >= 0 && x < dw;
-                const float m =
-                    fire_bit(0, yo - (y_begin - 1), rowc + (uint32_t)max(x, 0), row_b0) ? 1.f : 0.f;
+                const float m = (fw >> max(sh + grp * 16 + n, 0)) & 1 ? 1.f : 0.f;
                 float v[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) v[k] = in ? fmaf(m, u[k], f[grp][k]) : 0.f;
@@ -1467,13 +1471,14 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
 
         // Step t + 1, row yo (complete in p): MLP, fire gate and store; rows
         // outside [y_begin, y_end) are dropped by an empty descriptor.
-        auto finish_b = [&](int yo, int slot, const float (&p)[2][4]) {
+        auto finish_b = [&](int yo, const float (&p)[2][4]) {
             const bool out_ok = yo >= y_begin && yo < y_end;
             const int yc = min(max(yo, 0), dh - 1);
             const uint32_t rowc = (uint32_t)yc * (uint32_t)dw;
-            const uint32_t row_b0 = (rowc + (uint32_t)x0) >> 3;
+            const int sh = (int)((rowc + (uint32_t)x0) & 7u);
+            const uint64_t fw = row_word(1, yo - y_begin);
             const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
-            const float4 *own = mid[slot] + g * RS::PS;
+            const float4 *own = mid[(yo - base) & 1] + g * RS::PS;
             v4f acc[2][4];
             float f[2][8];
 #pragma unroll
@@ -1489,8 +1494,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
                 const uint32_t off = x < x_stop ? (uint32_t)x * kCellBytes : kOut;
-                update_store(dst, wr, off, g, f[grp], u,
-                             fire_bit(1, yo - y_begin, rowc + (uint32_t)x, row_b0));
+                update_store(dst, wr, off, g, f[grp], u, (fw >> (sh + grp * 16 + n)) & 1);
             }
         };
 
@@ -1507,8 +1511,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             finish_a(q - 1, jm, A[jm]);
             __builtin_amdgcn_sched_barrier(0);
             // step t's row q - 1: outputs q, q - 1, q - 2 of step t + 1
-            fold(mid[jm] + g * RS::PS, B[j], B[jm], B[jp]);
-            finish_b(q - 2, jp, B[jp]);
+            fold(mid[(q - 1 - base) & 1] + g * RS::PS, B[j], B[jm], B[jp]);
+            finish_b(q - 2, B[jp]);
             __builtin_amdgcn_sched_barrier(0);
             ra.commit(ring[jm]);
         };

@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib, library_path):
 
 def test_version_and_strerror(lib):
     declared = int(re.search(r"#define OCTNCA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.octree_nca_abi_version() == declared == 3
+    assert lib.octree_nca_abi_version() == declared == 4
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.octree_nca_strerror(st).decode() not in ("", "unknown status")
     assert lib.octree_nca_strerror(17).decode() == "unknown status"
@@ -336,3 +336,25 @@ def test_train_workspace_and_step_validation(lib):
     assert lib.octree_nca_train_step(*args(n - 1)) == ESPACE
     assert lib.octree_nca_train_step(model(), FAKE, _Extent(1, 8, 8), 2, f, ws, steps, 0.5, 0,
                                      FAKE2, big, n, gs, None, None, None) == EINVAL
+
+
+def test_infer_launches_counts_two_step_launches(monkeypatch):
+    """Host query of the launches octree_nca_infer enqueues: on the 184.5 MP
+    pyramid the three large levels run their first step fused with the
+    upsample and the other 19 in 9 two-step launches and one single one; the
+    smaller levels and the one-step selection run one launch per step."""
+    m = octnca.Model(ndim=2, n_in=3)
+    f = [(1, 2, 2)] * 5
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma")
+    assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == \
+        [11, 11, 11, 20, 20, 20]
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_1step")
+    assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == [20] * 6
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
+    assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 0]) == \
+        [3, 3, 0]
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "valu")
+    assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 3]) == \
+        [5, 4, 3]
+    with pytest.raises(octnca.OctreeNCAError):
+        octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, -1, 3])
