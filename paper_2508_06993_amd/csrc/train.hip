@@ -15,9 +15,9 @@
 //      [f | h | ga | gu | gP] for the weight gradients;
 //   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
 //      gP (halo tile of gP in LDS);
-//   3. wgrad_partials: per block of 32 consecutive cells, the sums of every
-//      weight-gradient entry (records staged in LDS 32 cells at a time, sums
-//      in registers), stored entry-major;
+//   3. wgrad_partials: per block of 64 consecutive cells, the sums of every
+//      weight-gradient entry (records staged in LDS cell-major, 4 x 4 register
+//      blocks of the outer-product sums), stored entry-major;
 //   4. wgrad_reduce: one wave per entry adds the block sums in fp64 (lane l
 //      takes blocks l, l + 64, ... in order, then a fixed shuffle tree) to
 //      the caller's gradients (accumulated, so the steps of a level sum up).
@@ -28,8 +28,7 @@ namespace octnca {
 namespace {
 
 constexpr int kBwdThreads = 256;
-constexpr int kChunk = 32;          // cells staged in LDS at a time
-constexpr int kChunksPerBlock = 1;   // chunks summed by one block (32 cells)
+constexpr int kWgCells = 64;   // cells per block of the weight-gradient partial sums
 
 template <int NDIM> struct BwdTile;
 template <> struct BwdTile<2> { static constexpr int TZ = 1, TY = 8, TX = 32; };
@@ -49,6 +48,29 @@ template <int C, int H, int TAPS> struct WG {
     static constexpr int W1 = 0, W2 = 2 * C * H, B1 = 3 * C * H, CB = 3 * C * H + H,
                          CW = 3 * C * H + H + C, N = 3 * C * H + H + C + C * TAPS;
 };
+
+// LDS staging of TOTAL words by the block: word i = load(i), stored by
+// store(i, value).  The loads go out in batches of BATCH per thread before
+// their stores, so that a thread's loads are in flight together (a plain
+// strided loop waits for each load before the next).
+template <int TOTAL, int BATCH, class Load, class Store>
+__device__ __forceinline__ void stage(Load load, Store store) {
+    constexpr int ITERS = (TOTAL + kBwdThreads - 1) / kBwdThreads;
+#pragma unroll 1
+    for (int it0 = 0; it0 < ITERS; it0 += BATCH) {
+        float v[BATCH];
+#pragma unroll
+        for (int j = 0; j < BATCH; ++j) {
+            const int i = (int)threadIdx.x + (it0 + j) * kBwdThreads;
+            v[j] = load(min(i, TOTAL - 1));
+        }
+#pragma unroll
+        for (int j = 0; j < BATCH; ++j) {
+            const int i = (int)threadIdx.x + (it0 + j) * kBwdThreads;
+            if (it0 + j < ITERS && i < TOTAL) store(i, v[j]);
+        }
+    }
+}
 
 template <int NDIM, int NIN, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
@@ -71,15 +93,18 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     const int by = b % tiles_y;
     const int bz = b / tiles_y;
     const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
-    for (int i = threadIdx.x; i < NCELL * C; i += kBwdThreads) {
-        const int c = i / NCELL, cell = i % NCELL;
-        const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
-        const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
-        float v = 0.f;
-        if (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
-            v = src[(((int64_t)gz * dh + gy) * dw + gx) * C + c];
-        tile[c][cell] = v;
-    }
+    stage<NCELL * C, 8>(
+        [&](int i) {
+            const int c = i / NCELL, cell = i % NCELL;
+            const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+            const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+            const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+            const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
+                      cz = min(max(gz, 0), dd - 1);
+            const float v = src[(((int64_t)cz * dh + cy) * dw + cx) * C + c];
+            return in ? v : 0.f;
+        },
+        [&](int i, float v) { tile[i / NCELL][i % NCELL] = v; });
     __syncthreads();
 
     const int tx = threadIdx.x % T::TX, ty = (threadIdx.x / T::TX) % T::TY,
@@ -154,15 +179,18 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
     const int by = b % tiles_y;
     const int bz = b / tiles_y;
     const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
-    for (int i = threadIdx.x; i < NCELL * C; i += kBwdThreads) {
-        const int c = i / NCELL, cell = i % NCELL;
-        const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
-        const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
-        float v = 0.f;
-        if (gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd)
-            v = rec[(R::GP + c) * cells + ((int64_t)gz * dh + gy) * dw + gx];
-        tile[c][cell] = v;
-    }
+    stage<NCELL * C, 8>(
+        [&](int i) {
+            const int c = i / NCELL, cell = i % NCELL;
+            const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+            const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+            const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+            const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
+                      cz = min(max(gz, 0), dd - 1);
+            const float v = rec[(R::GP + c) * cells + ((int64_t)cz * dh + cy) * dw + cx];
+            return in ? v : 0.f;
+        },
+        [&](int i, float v) { tile[i / NCELL][i % NCELL] = v; });
     __syncthreads();
 
     const int tx = threadIdx.x % T::TX, ty = (threadIdx.x / T::TX) % T::TY,
@@ -184,9 +212,13 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
     }
 }
 
-// Sums over a block's cells (kChunksPerBlock chunks of kChunk cells, staged
-// in LDS one chunk at a time) of every weight-gradient entry; thread t owns
-// entries t, t + 256, ... and keeps their sums in registers.
+// Sums over a block's kWgCells consecutive cells of every weight-gradient
+// entry.  The block stages its cells' records in LDS cell by cell (a row of
+// R::N words per cell), and each thread takes jobs of entries that share
+// operands: a 4 x 4 block of dW1 (ga[j..j+3] x f[k..k+3]) or of dW2
+// (gu[c..c+3] x h[j..j+3]), four entries of db1 or dconv_b, or one tap of
+// dconv_w for four channels; per cell a job reads two 16-byte words and does
+// up to 16 FMAs, in cell order.  Sums are stored entry-major.
 template <int NDIM, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     const float *__restrict__ src, const float *__restrict__ rec, int dd, int dh, int dw,
@@ -194,70 +226,99 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     using R = Rec<C, H>;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
     using G = WG<C, H, TAPS>;
-    constexpr int KO = (G::N + kBwdThreads - 1) / kBwdThreads;   // entries per thread
-    __shared__ float recs[R::N][kChunk + 1];   // [entry][cell]
-    float acc[KO];
-#pragma unroll
-    for (int q = 0; q < KO; ++q) acc[q] = 0.f;
-    for (int ch = 0; ch < kChunksPerBlock; ++ch) {
-        const int64_t first = ((int64_t)blockIdx.x * kChunksPerBlock + ch) * kChunk;
-        if (first >= cells) break;                       // uniform over the block
-        const int n = (int)min<int64_t>(kChunk, cells - first);
-        __syncthreads();                                 // previous chunk consumed
-        for (int i = threadIdx.x; i < kChunk * R::N; i += kBwdThreads) {
-            const int k = i / kChunk, cell = i % kChunk;
-            recs[k][cell] = cell < n ? rec[k * cells + first + cell] : 0.f;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < KO; ++q) {
-            const int o = threadIdx.x + q * kBwdThreads;
-            float s = acc[q];
-            if (o < G::W2) {                       // dW1[j][k] = sum ga[j] f[k]
-                const int j = o / (2 * C), k = o % (2 * C);
-    #pragma unroll 8
-            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GA + j][i], recs[R::F + k][i], s);
-            } else if (o < G::B1) {                // dW2[c][j] = sum gu[c] h[j]
-                const int c = (o - G::W2) / H, j = (o - G::W2) % H;
-    #pragma unroll 8
-            for (int i = 0; i < n; ++i) s = fmaf(recs[R::GU + c][i], recs[R::Hh + j][i], s);
-            } else if (o < G::CB) {                // db1[j] = sum ga[j]
-                const int j = o - G::B1;
-    #pragma unroll 8
-            for (int i = 0; i < n; ++i) s += recs[R::GA + j][i];
-            } else if (o < G::CW) {                // dconv_b[c] = sum gP[c]
-                const int c = o - G::CB;
-    #pragma unroll 8
-            for (int i = 0; i < n; ++i) s += recs[R::GP + c][i];
-            } else if (o < G::N) {                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
-                const int c = (o - G::CW) / TAPS, t = (o - G::CW) % TAPS;
-                const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
-                // neighbour loads without branches (clamped address, 0/1 weight),
-                // so that the loads of several cells are in flight together
-                int64_t p = first;
-                int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
-#pragma unroll 8
-                for (int i = 0; i < n; ++i) {
-                    const int gx = x + dx, gy = y + dy, gz = z + dz;
-                    const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
-                    const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
-                              cz = min(max(gz, 0), dd - 1);
-                    const float sv = src[(((int64_t)cz * dh + cy) * dw + cx) * C + c];
-                    s = fmaf(recs[R::GP + c][i], in ? sv : 0.f, s);
-                    const bool wrap = ++x == dw;   // next cell in row-major order
-                    x = wrap ? 0 : x;
-                    const bool wrap_y = wrap && ++y == dh;
-                    y = wrap_y ? 0 : y;
-                    z += wrap_y ? 1 : 0;
-                }
+    static_assert(C % 4 == 0 && H % 4 == 0, "entries in blocks of 4");
+    constexpr int RS = R::N + 4;   // words per staged record (16-byte aligned rows)
+    __shared__ __align__(16) float recs[kWgCells * RS];   // [cell][entry]
+    const int64_t first = (int64_t)blockIdx.x * kWgCells;
+    const int n = (int)min<int64_t>(kWgCells, cells - first);
+    stage<kWgCells * R::N, 8>(
+        [&](int i) {
+            const int k = i / kWgCells, cell = i % kWgCells;
+            const float v = rec[k * cells + first + min(cell, n - 1)];
+            return cell < n ? v : 0.f;
+        },
+        [&](int i, float v) { recs[(i % kWgCells) * RS + i / kWgCells] = v; });
+    __syncthreads();
+    auto quad = [&](int cell, int e) {
+        const float4 v = *reinterpret_cast<const float4 *>(&recs[cell * RS + e]);
+        return v;
+    };
+    const int64_t nb = gridDim.x;
+    auto put = [&](int o, float v) { partial[(int64_t)o * nb + blockIdx.x] = v; };
+    constexpr int J1 = (H / 4) * (2 * C / 4);    // dW1 blocks
+    constexpr int J2 = (C / 4) * (H / 4);        // dW2 blocks
+    constexpr int JB = H / 4, JC = C / 4;        // db1, dconv_b quads
+    constexpr int JK = (C / 4) * TAPS;           // dconv_w (channel quad, tap)
+    constexpr int NJ = J1 + J2 + JB + JC + JK;
+    for (int job = threadIdx.x; job < NJ; job += kBwdThreads) {
+        if (job < J1 + J2) {
+            int ea, eb, o0, os;
+            if (job < J1) {                      // dW1[j][k] = sum ga[j] f[k]
+                const int jb = job / (2 * C / 4), kb = job % (2 * C / 4);
+                ea = R::GA + 4 * jb; eb = R::F + 4 * kb;
+                o0 = G::W1 + 4 * jb * 2 * C + 4 * kb; os = 2 * C;
+            } else {                             // dW2[c][j] = sum gu[c] h[j]
+                const int jj = job - J1, cb = jj / (H / 4), jb = jj % (H / 4);
+                ea = R::GU + 4 * cb; eb = R::Hh + 4 * jb;
+                o0 = G::W2 + 4 * cb * H + 4 * jb; os = H;
             }
-            acc[q] = s;
-        }
-    }
+            float acc[4][4] = {};
+#pragma unroll 4
+            for (int i = 0; i < n; ++i) {
+                const float4 av = quad(i, ea), bv = quad(i, eb);
+                const float ar[4] = {av.x, av.y, av.z, av.w}, br[4] = {bv.x, bv.y, bv.z, bv.w};
 #pragma unroll
-    for (int q = 0; q < KO; ++q) {
-        const int o = threadIdx.x + q * kBwdThreads;
-        if (o < G::N) partial[(int64_t)o * gridDim.x + blockIdx.x] = acc[q];   // [entry][block]
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(ar[r], br[c], acc[r][c]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) put(o0 + r * os + c, acc[r][c]);
+        } else if (job < J1 + J2 + JB + JC) {    // db1[j] = sum ga[j]; dconv_b[c] = sum gP[c]
+            const int jj = job - J1 - J2;
+            const int e = jj < JB ? R::GA + 4 * jj : R::GP + 4 * (jj - JB);
+            const int o0 = jj < JB ? G::B1 + 4 * jj : G::CB + 4 * (jj - JB);
+            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < n; ++i) {
+                const float4 v = quad(i, e);
+                sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) put(o0 + r, sum[r]);
+        } else {                                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
+            const int jj = job - J1 - J2 - JB - JC;
+            const int cq = jj / TAPS, t = jj % TAPS;
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            int64_t p = first;
+            int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
+            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            // neighbour loads without branches (clamped address, 0/1 weight),
+            // so that the loads of several cells are in flight together
+#pragma unroll 8
+            for (int i = 0; i < n; ++i) {
+                const int gx = x + dx, gy = y + dy, gz = z + dz;
+                const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+                const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
+                          cz = min(max(gz, 0), dd - 1);
+                const float4 sv = *reinterpret_cast<const float4 *>(
+                    &src[(((int64_t)cz * dh + cy) * dw + cx) * C + 4 * cq]);
+                const float w = in ? 1.f : 0.f;
+                const float4 gp = quad(i, R::GP + 4 * cq);
+                sum[0] = fmaf(gp.x, w * sv.x, sum[0]);
+                sum[1] = fmaf(gp.y, w * sv.y, sum[1]);
+                sum[2] = fmaf(gp.z, w * sv.z, sum[2]);
+                sum[3] = fmaf(gp.w, w * sv.w, sum[3]);
+                const bool wrap = ++x == dw;   // next cell in row-major order
+                x = wrap ? 0 : x;
+                const bool wrap_y = wrap && ++y == dh;
+                y = wrap_y ? 0 : y;
+                z += wrap_y ? 1 : 0;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) put(G::CW + (4 * cq + r) * TAPS + t, sum[r]);
+        }
     }
 }
 
@@ -297,7 +358,7 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
     const int tiles_y = (int)((a.ext.h + T::TY - 1) / T::TY);
     const int tiles_z = (int)((a.ext.d + T::TZ - 1) / T::TZ);
     const int64_t blocks = (int64_t)tiles_x * tiles_y * tiles_z;
-    const int64_t chunks = (cells + kChunk * kChunksPerBlock - 1) / (kChunk * kChunksPerBlock);
+    const int64_t chunks = (cells + kWgCells - 1) / kWgCells;
     if (cells == 0) return hipSuccess;
     float *gpart = ws;
     float *rec = gpart + cells * C;
@@ -403,7 +464,7 @@ size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_
     const int taps = ndim == 3 ? 27 : 9;
     const int64_t rec_n = 4 * channels + 2 * hidden;
     const int64_t wg_n = 3 * channels * hidden + hidden + channels + channels * taps;
-    const int64_t blocks = (cells + kChunk * kChunksPerBlock - 1) / (kChunk * kChunksPerBlock);
+    const int64_t blocks = (cells + kWgCells - 1) / kWgCells;
     return (size_t)(cells * channels + cells * rec_n + blocks * wg_n);
 }
 

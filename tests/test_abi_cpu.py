@@ -261,7 +261,7 @@ def grads():
 
 
 def bwd_ws_floats(cells, c=16, h=64, taps=9):
-    chunks = (cells + 31) // 32
+    chunks = (cells + 63) // 64
     return cells * c + cells * (4 * c + 2 * h) + chunks * (3 * c * h + h + c + c * taps)
 
 
