@@ -9,9 +9,9 @@
 //   dW1 += ga f^T, db1 += ga, [gS, gP] = W1^T ga, dconv_b += gP,
 //   dK[c][t] += gP[p][c] S[p + o_t][c], dL/dS = G' + gS + conv^T(gP).
 // Four launches:
-//   1. bwd_cell: one thread per cell (halo tile of S in LDS, as the vector
-//      step kernel): perception, then the 64 hidden units streamed once,
-//      each giving a, h, gh and ga; writes G' + gS and the cell's record
+//   1. bwd_cell: four lanes per cell (halo tile of S in LDS): perception,
+//      then the hidden units streamed once, a quarter per lane, each giving
+//      a, h, gh and ga; writes G' + gS and the cell's record
 //      [f | h | ga | gu | gP] for the weight gradients;
 //   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
 //      gP (halo tile of gP in LDS);
@@ -72,6 +72,16 @@ __device__ __forceinline__ void stage(Load load, Store store) {
     }
 }
 
+// bwd_cell: a quad of lanes per cell (lane = 4 * cell + part); part p takes
+// hidden units j = 4 i + p, and the four partial feature gradients W1^T ga
+// are summed across the quad.  Blocks of 64 cells.  W1 and W2^T sit in LDS
+// with rows padded by 4 words, so the quad's four rows fall in different
+// banks.
+constexpr int kParts = 4;
+template <int NDIM> struct BwdCellTile;
+template <> struct BwdCellTile<2> { static constexpr int TZ = 1, TY = 2, TX = 32; };
+template <> struct BwdCellTile<3> { static constexpr int TZ = 2, TY = 4, TX = 8; };
+
 template <int NDIM, int NIN, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     const float *__restrict__ src, const float *__restrict__ gout, int dd, int dh, int dw,
@@ -79,13 +89,18 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
     float *__restrict__ gpart, float *__restrict__ rec, int64_t cells) {
-    using T = BwdTile<NDIM>;
+    using T = BwdCellTile<NDIM>;
     using R = Rec<C, H>;
     constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
     constexpr int NCELL = HZ * HY * HX;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
-    static_assert(T::TZ * T::TY * T::TX == kBwdThreads, "one thread per tile cell");
-    __shared__ float tile[C][NCELL];   // channel-major: neighbouring threads, neighbouring words
+    constexpr int HP = H / kParts;   // hidden units per lane
+    static_assert(T::TZ * T::TY * T::TX * kParts == kBwdThreads, "a quad of lanes per tile cell");
+    static_assert(H % kParts == 0 && C % kParts == 0, "parts of equal size");
+    __shared__ float tile[C][NCELL];   // channel-major: neighbouring cells, neighbouring words
+    __shared__ __align__(16) float sw1[H][2 * C + 4];   // W1
+    __shared__ __align__(16) float sw2[H][C + 4];       // W2^T
+    __shared__ float sb1[H];
 
     int b = blockIdx.x;
     const int bx = b % tiles_x;
@@ -105,14 +120,22 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
             return in ? v : 0.f;
         },
         [&](int i, float v) { tile[i / NCELL][i % NCELL] = v; });
+    stage<H * 2 * C, 8>([&](int i) { return w1[i]; },
+                        [&](int i, float v) { sw1[i / (2 * C)][i % (2 * C)] = v; });
+    stage<C * H, 8>([&](int i) { return w2[i]; },
+                    [&](int i, float v) { sw2[i % H][i / H] = v; });
+    for (int i = threadIdx.x; i < H; i += kBwdThreads) sb1[i] = b1[i];
     __syncthreads();
 
-    const int tx = threadIdx.x % T::TX, ty = (threadIdx.x / T::TX) % T::TY,
-              tz = threadIdx.x / (T::TX * T::TY);
+    const int part = threadIdx.x % kParts, cl = threadIdx.x / kParts;
+    const int tx = cl % T::TX, ty = (cl / T::TX) % T::TY, tz = cl / (T::TX * T::TY);
     const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
-    if (x >= dw || y >= dh || z >= dd) return;
+    // a quad outside the grid computes on a clamped cell and stores nothing
+    // (no early return: the quad's lanes exchange values below)
+    const bool valid = x < dw && y < dh && z < dd;
     const int centre = ((tz + (NDIM == 3 ? 1 : 0)) * HY + ty + 1) * HX + tx + 1;
-    const int64_t idx = ((int64_t)z * dh + y) * dw + x;
+    const int64_t idx =
+        ((int64_t)min(z, dd - 1) * dh + min(y, dh - 1)) * dw + min(x, dw - 1);
 
     float f[2 * C];
 #pragma unroll
@@ -138,27 +161,40 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
 #pragma unroll
     for (int k = 0; k < 2 * C; ++k) gf[k] = 0.f;
 #pragma unroll 2
-    for (int j = 0; j < H; ++j) {
-        float a = b1[j];
+    for (int jj = 0; jj < HP; ++jj) {
+        const int j = jj * kParts + part;
+        float a = sb1[j];
 #pragma unroll
-        for (int k = 0; k < 2 * C; ++k) a = fmaf(w1[j * 2 * C + k], f[k], a);
+        for (int k = 0; k < 2 * C; ++k) a = fmaf(sw1[j][k], f[k], a);
         float gh = 0.f;
 #pragma unroll
-        for (int c = NIN; c < C; ++c) gh = fmaf(w2[c * H + j], gu[c], gh);
+        for (int c = NIN; c < C; ++c) gh = fmaf(sw2[j][c], gu[c], gh);
         const float ga = a > 0.f ? gh : 0.f;
 #pragma unroll
-        for (int k = 0; k < 2 * C; ++k) gf[k] = fmaf(w1[j * 2 * C + k], ga, gf[k]);
-        r[(R::Hh + j) * cells] = fmaxf(a, 0.f);
-        r[(R::GA + j) * cells] = ga;
+        for (int k = 0; k < 2 * C; ++k) gf[k] = fmaf(sw1[j][k], ga, gf[k]);
+        if (valid) {
+            r[(R::Hh + j) * cells] = fmaxf(a, 0.f);
+            r[(R::GA + j) * cells] = ga;
+        }
     }
+    // sum of the quad's four partial W1^T ga (the same order in every lane)
 #pragma unroll
-    for (int k = 0; k < 2 * C; ++k) r[(R::F + k) * cells] = f[k];
-#pragma unroll
-    for (int c = 0; c < C; ++c) {
-        r[(R::GU + c) * cells] = gu[c];
-        r[(R::GP + c) * cells] = gf[C + c];
-        gpart[idx * C + c] = g[c] + gf[c];
+    for (int k = 0; k < 2 * C; ++k) {
+        gf[k] += __shfl_xor(gf[k], 1);
+        gf[k] += __shfl_xor(gf[k], 2);
     }
+    if (!valid) return;
+    constexpr int FP = 2 * C / kParts, CP = C / kParts;
+#pragma unroll
+    for (int k = 0; k < 2 * C; ++k)
+        if (k / FP == part) r[(R::F + k) * cells] = f[k];
+#pragma unroll
+    for (int c = 0; c < C; ++c)
+        if (c / CP == part) {
+            r[(R::GU + c) * cells] = gu[c];
+            r[(R::GP + c) * cells] = gf[C + c];
+            gpart[idx * C + c] = g[c] + gf[c];
+        }
 }
 
 template <int NDIM, int C, int H>
@@ -363,8 +399,12 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
     float *gpart = ws;
     float *rec = gpart + cells * C;
     float *partial = rec + cells * R::N;
-    bwd_cell<NDIM, NIN, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
-        src, gout, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w,
+    using TC = BwdCellTile<NDIM>;
+    const int ctiles_x = (int)((a.ext.w + TC::TX - 1) / TC::TX);
+    const int ctiles_y = (int)((a.ext.h + TC::TY - 1) / TC::TY);
+    const int64_t cblocks = (int64_t)ctiles_x * ctiles_y * ((a.ext.d + TC::TZ - 1) / TC::TZ);
+    bwd_cell<NDIM, NIN, C, H><<<(unsigned)cblocks, kBwdThreads, 0, stream>>>(
+        src, gout, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, ctiles_x, ctiles_y, a.w.conv_w,
         a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold, gpart,
         rec, cells);
     bwd_conv_t<NDIM, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
