@@ -267,7 +267,7 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     __shared__ __align__(16) float recs[kWgCells * RS];   // [cell][entry]
     const int64_t first = (int64_t)blockIdx.x * kWgCells;
     const int n = (int)min<int64_t>(kWgCells, cells - first);
-    stage<kWgCells * R::N, 8>(
+    stage<kWgCells * R::N, 16>(
         [&](int i) {
             const int k = i / kWgCells, cell = i % kWgCells;
             const float v = rec[k * cells + first + min(cell, n - 1)];
@@ -332,7 +332,7 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
             float sum[4] = {0.f, 0.f, 0.f, 0.f};
             // neighbour loads without branches (clamped address, 0/1 weight),
             // so that the loads of several cells are in flight together
-#pragma unroll 8
+#pragma unroll 16
             for (int i = 0; i < n; ++i) {
                 const int gx = x + dx, gy = y + dy, gz = z + dz;
                 const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
