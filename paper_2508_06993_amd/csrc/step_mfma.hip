@@ -2097,14 +2097,24 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     return hipGetLastError();
 }
 
-// Output planes per 3D work item: the longest run of 32, 16, 8 or 4 planes
-// that still gives at least two work items per block slot (on small levels
-// longer runs would leave CUs idle; a shorter run reads its two halo planes
-// once more per run).
+// Output planes per 3D work item, chosen per launch: the run length r in
+// 1 .. 32 that minimises ceil(items(r) / slots) * (planes(r) + 2), the work
+// of the most loaded block slot (grid-stride rounds times the planes a work
+// item streams, its two halo planes included); ties go to the longer run.
+// Short runs spread small levels over the chip at the cost of reading their
+// halo planes again; long runs stream large levels with little re-reading.
 int pick_zrun(int64_t tiles, int64_t depth, int64_t slots) {
-    for (int r = k3ZRun; r > 4; r /= 2)
-        if (tiles * ((depth + r - 1) / r) >= 2 * slots) return r;
-    return 4;
+    int best = 1;
+    int64_t best_cost = INT64_MAX;
+    for (int r = 1; r <= k3ZRun; ++r) {
+        const int64_t items = tiles * ((depth + r - 1) / r);
+        const int64_t cost = (items + slots - 1) / slots * (std::min<int64_t>(r, depth) + 2);
+        if (cost <= best_cost) {
+            best_cost = cost;
+            best = r;
+        }
+    }
+    return best;
 }
 
 template <typename T, int NIN, class Mlp>
