@@ -126,6 +126,14 @@ int32_t level_launches(const StepArgs &a, int32_t t0, int32_t t1) {
     return step_pairs(a) ? (t1 - t0 + 1) / 2 : t1 - t0;
 }
 
+// Steps run by a level's first launch when it is fused with the upsample: two
+// where the two-step kernel applies and the level has two steps, else one; 0
+// when the first step is not fused.
+int32_t fused_up_steps(const StepArgs &a, bool fused, int32_t steps) {
+    if (!fused) return 0;
+    return steps >= 2 && step_pairs(a) ? 2 : 1;
+}
+
 // Enqueue steps t0 .. t1-1 of a level; launch k reads bufs[k % 2] and writes
 // bufs[(k + 1) % 2], so the result is in bufs[level_launches(..) % 2].
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
@@ -327,7 +335,8 @@ int octree_nca_infer_launches(const octnca_model *model, octnca_extent finest, i
     for (int l = 0; l < levels; ++l) {
         const StepArgs a = step_args(model, p.ext[l], &none, l, 0, 0, 0);
         const bool fused = l + 1 < levels && steps[l] >= 1 && step_fuses_upsample(a);
-        launches[l] = (fused ? 1 : 0) + level_launches(a, fused ? 1 : 0, steps[l]);
+        launches[l] = (fused ? 1 : 0) + level_launches(a, fused_up_steps(a, fused, steps[l]),
+                                                       steps[l]);
     }
     return OCTNCA_OK;
 }
@@ -383,7 +392,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     for (int l = 0; l < levels; ++l) {
         const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
         if (l + 1 < levels && steps[l] >= 1) fused[l] = step_fuses_upsample(a);
-        const int32_t t0 = fused[l] ? 1 : 0;
+        const int32_t t0 = fused_up_steps(a, fused[l], steps[l]);
         flips += (l + 1 < levels ? 1 : 0) + level_launches(a, t0, steps[l]);
     }
     for (int l = 1; l < levels; ++l) {
@@ -409,13 +418,17 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
             return OCTNCA_EHIP;
         int32_t t0 = 0;
         if (fused[l]) {
-            // step 0 from the coarse state bufs[cur] (level l + 1) and image l
+            // step 0 (or steps 0 and 1) from the coarse state bufs[cur] (level
+            // l + 1) and image l
             const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
-            if (launch_step_up(a, bufs[cur], (int)p.ext[l + 1].h, (int)p.ext[l + 1].w, f[0],
-                               f[1], f[2], img[l], bufs[cur ^ 1], s) != hipSuccess)
-                return OCTNCA_EHIP;
+            t0 = fused_up_steps(a, true, steps[l]);
+            const hipError_t err =
+                t0 == 2 ? launch_step_pair_up(a, bufs[cur], (int)p.ext[l + 1].w, f[0], f[1], f[2],
+                                              img[l], bufs[cur ^ 1], s)
+                        : launch_step_up(a, bufs[cur], (int)p.ext[l + 1].h, (int)p.ext[l + 1].w,
+                                         f[0], f[1], f[2], img[l], bufs[cur ^ 1], s);
+            if (err != hipSuccess) return OCTNCA_EHIP;
             cur ^= 1;
-            t0 = 1;
         }
         st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, t0, steps[l],
                        seed, threshold, s, batch);
@@ -812,6 +825,14 @@ bool step_pairs(const StepArgs &a) {
 hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
     const Selection sel = select_step_kernel();
     return launch_step2_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+}
+
+hipError_t launch_step_pair_up(const StepArgs &a, const void *coarse, int coarse_w, int fz,
+                               int fy, int fx, const void *img, void *dst, hipStream_t stream) {
+    if (fz != 1 || !step_fuses_upsample(a)) return hipErrorInvalidValue;
+    const Selection sel = select_step_kernel();
+    return launch_step2_mfma_up(a, sel.mlp, sel.layout, coarse, coarse_w, fy, fx, img, dst,
+                                stream);
 }
 
 bool step_fuses_upsample(const StepArgs &a) {

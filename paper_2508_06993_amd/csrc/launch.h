@@ -60,6 +60,10 @@ hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipSt
 // that launch (the state after step a.step is not written to memory).
 bool step_pairs(const StepArgs &a);
 hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+// The first two steps of a level, the first fused with the upsample (when
+// step_pairs and step_fuses_upsample both hold).
+hipError_t launch_step_pair_up(const StepArgs &a, const void *coarse, int coarse_w, int fz,
+                               int fy, int fx, const void *img, void *dst, hipStream_t stream);
 
 // Training (fp32 states): backward of one step (state `src` before the step,
 // gout = dL/dS'), writing gin = dL/dS (may alias gout) and adding the weight
@@ -97,6 +101,11 @@ bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
 bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
 hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                              void *dst, hipStream_t stream);
+// The same two steps with step a.step fused with the upsample + inject from
+// the coarse state (width coarse_w, factors fy, fx) and the level's image.
+hipError_t launch_step2_mfma_up(const StepArgs &a, MfmaMlp mlp, Layout2d layout,
+                                const void *coarse, int coarse_w, int fy, int fx, const void *img,
+                                void *dst, hipStream_t stream);
 hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *coarse,
                                int coarse_h, int coarse_w, int fz, int fy, int fx,
                                const void *img, void *dst, hipStream_t stream);

@@ -1052,8 +1052,9 @@ struct RowStream {
 #pragma unroll
         for (int k = 0; k < kBody; ++k) {
             const int cx = x0 + k * kCellsPerBody + cell;
-            const uint32_t off =
-                cx < dw ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)chunk * 16 : kOut;
+            const uint32_t off = cx >= 0 && cx < dw
+                                     ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)chunk * 16
+                                     : kOut;
             const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
             v[k] = make_uint4(x[0], x[1], x[2], x[3]);
         }
@@ -1301,12 +1302,16 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
 // ---------------------------------------------------------------------------
 constexpr int k2PairW = kTileW - 2;   // output cells per strip
 
-template <typename T, int NIN, class Mlp>
+// UP: step t is a level's first step, fused with the upsample + inject as in
+// nca_step_mfma_2d_rows (src is the next coarser state, width up_cdw, factors
+// up_fy, up_fx; the input channels come from up_img).
+template <typename T, int NIN, class Mlp, bool UP>
 __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int run_rows,
     int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
-    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
+    const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx) {
     static_assert(std::is_same_v<T, float>, "the intermediate ring holds fp32 states");
     using RS = RowStream<T>;
     // Row r of a work item (first input row `base`) lives in slot
@@ -1377,6 +1382,63 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     int gq = g;
     RS ra, rb;
+    using Img = typename RS::template Image<NIN>;
+    Img ia, ib;   // used by UP only
+    // UP: the lane's byte offsets within a coarse row and an image row, the
+    // same for every row of a work item (computed once per item).
+    struct UpCols {
+        uint32_t body[RS::kBody], side, img[Img::kImg];
+    } uc;
+    auto up_cols = [&](int x) {
+        const int lane = threadIdx.x & 63;
+        const int cell = lane % RS::kCellsPerBody, chunk = lane / RS::kCellsPerBody;
+#pragma unroll
+        for (int kk = 0; kk < RS::kBody; ++kk) {
+            const int cx = x + kk * RS::kCellsPerBody + cell;
+            uc.body[kk] = cx >= 0 && cx < dw
+                              ? (uint32_t)(cx / up_fx) * kCellBytes + (uint32_t)chunk * 16 : kOut;
+        }
+        const int cx = lane < RS::NQ ? x - 1 : x + kTileW;
+        uc.side = lane < 2 * RS::NQ && cx >= 0 && cx < dw
+                      ? (uint32_t)(cx / up_fx) * kCellBytes + (uint32_t)(lane % RS::NQ) * 16 : kOut;
+#pragma unroll
+        for (int j = 0; j < Img::kImg; ++j) {
+            const int e = lane + 64 * j;
+            const int fc = x - 1 + e / NIN;
+            uc.img[j] = e < Img::kElems && fc >= 0 && fc < dw
+                            ? (uint32_t)(fc * NIN + e % NIN) * (uint32_t)sizeof(T) : kOut;
+        }
+    };
+    // Fine row y of the upsampled state: coarse row cy = y / fy, image row y.
+    // The loop passes cy kept by counting (a division per row in the unrolled
+    // loop made the compiler spill).
+    auto issue = [&](RS &rs, Img &im, int y, int cy, int x) {
+        if constexpr (UP) {
+            const bool row_ok = y >= 0 && y < dh;
+            const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? cy : 0) * up_cdw * kC,
+                                     row_ok ? (uint32_t)up_cdw * kCellBytes : 0u);
+#pragma unroll
+            for (int kk = 0; kk < RS::kBody; ++kk) {
+                const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, uc.body[kk], 0, 0);
+                rs.v[kk] = make_uint4(v[0], v[1], v[2], v[3]);
+            }
+            const v4u v = __builtin_amdgcn_raw_buffer_load_b128(r, uc.side, 0, 0);
+            rs.v[RS::kBody] = make_uint4(v[0], v[1], v[2], v[3]);
+            const Rsrc ri = make_rsrc(up_img + (int64_t)(row_ok ? y : 0) * dw * NIN,
+                                      row_ok ? (uint32_t)dw * NIN * (uint32_t)sizeof(T) : 0u);
+#pragma unroll
+            for (int j = 0; j < Img::kImg; ++j)
+                im.e[j] = __builtin_amdgcn_raw_buffer_load_b32(ri, uc.img[j], 0, 0);
+        } else {
+            rs.issue(src, y, dh, dw, x);
+        }
+    };
+    auto commit = [&](const RS &rs, const Img &im, float4 *slot) {
+        if constexpr (UP)
+            rs.template commit_up<NIN>(slot, im);
+        else
+            rs.commit(slot);
+    };
 
     for (int item = blockIdx.x; item < items; item += gridDim.x) {
         const int sx = item % strips;
@@ -1395,8 +1457,11 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
         // rotate roles without register moves.
         float A[3][2][4], B[3][2][4];
 
-        ra.issue(src, base, dh, dw, x1);
-        rb.issue(src, base + 1, dh, dw, x1);
+        if constexpr (UP) up_cols(x1);
+        issue(ra, ia, base, base >= 0 ? base / up_fy : 0, x1);
+        issue(rb, ib, base + 1, base + 1 >= 0 ? (base + 1) / up_fy : 0, x1);
+        // coarse row and remainder of the next row the loop loads (y_begin >= 0)
+        int up_cy = y_begin / up_fy, up_ry = y_begin - up_cy * up_fy;
         // step t's rows y_begin - 1 .. y_end, step t + 1's y_begin .. y_end - 1
         for (int e = 0; e < 2 * kEvalBlocks; ++e) {
             const int st = e >= kEvalBlocks ? 1 : 0;
@@ -1405,8 +1470,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             if (y_first <= y_end - st)
                 evaluate(st, blk, step + st, y_first, st ? (uint32_t)x0 : xs1);
         }
-        ra.commit(ring[0]);
-        rb.commit(ring[1]);
+        commit(ra, ia, ring[0]);
+        commit(rb, ib, ring[1]);
 
         // Row r of a plane set with its x taps: output r + 1 takes the dy = -1
         // weights (its first contribution, started from the bias), r the
@@ -1505,7 +1570,11 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
         auto body = [&](int q, auto jc) {
             constexpr int j = decltype(jc)::value;   // (q - base) % 3
             constexpr int jm = (j + 2) % 3, jp = (j + 1) % 3;   // rows q - 1, q + 1 (= q - 2)
-            ra.issue(src, q + 2, dh, dw, x1);
+            issue(ra, ia, q + 2, up_cy, x1);
+            if constexpr (UP) {
+                up_cy += ++up_ry == up_fy ? 1 : 0;
+                up_ry = up_ry == up_fy ? 0 : up_ry;
+            }
             // input row q: outputs q + 1, q, q - 1 of step t
             fold(ring[j] + g * RS::PS, A[jp], A[j], A[jm]);
             finish_a(q - 1, jm, A[jm]);
@@ -1514,7 +1583,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             fold(mid[(q - 1 - base) & 1] + g * RS::PS, B[j], B[jm], B[jp]);
             finish_b(q - 2, B[jp]);
             __builtin_amdgcn_sched_barrier(0);
-            ra.commit(ring[jm]);
+            commit(ra, ia, ring[jm]);
         };
         // The first bodies see sums that were never started (rows before
         // base); they only feed rows that are not used.
@@ -2067,16 +2136,19 @@ bool uses_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
             (layout == Layout2d::Auto && pair_plan(a).items >= pair_plan(a).slots));
 }
 
-template <int NIN>
-hipError_t launch_rows_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
+// UP: src is the coarse state (width cdw) upsampled by (fy, fx), img the
+// level's image; steps a.step and a.step + 1.
+template <int NIN, bool UP>
+hipError_t launch_rows_pair(const StepArgs &a, const void *src, void *dst, const void *img,
+                            int cdw, int fy, int fx, hipStream_t stream) {
     const RowsPlan r = pair_plan(a);
     if (r.items == 0) return hipSuccess;
     if (r.items > INT32_MAX) return hipErrorInvalidValue;
     const int grid = (int)std::min<int64_t>(r.items, r.slots);
-    nca_step2_mfma_2d_rows<float, NIN, MlpF32State><<<grid, 64, 0, stream>>>(
+    nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP><<<grid, 64, 0, stream>>>(
         (const float *)src, (float *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, k2RunRows,
         (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
-        a.seed, a.threshold);
+        a.seed, a.threshold, (const float *)img, cdw, fy, fx);
     return hipGetLastError();
 }
 
@@ -2198,8 +2270,19 @@ bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
 hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                              void *dst, hipStream_t stream) {
     if (!step_mfma_pairs(a, mlp, layout)) return hipErrorInvalidValue;
-    if (a.n_in == 1) return launch_rows_pair<1>(a, src, dst, stream);
-    if (a.n_in == 3) return launch_rows_pair<3>(a, src, dst, stream);
+    if (a.n_in == 1) return launch_rows_pair<1, false>(a, src, dst, nullptr, 0, 1, 1, stream);
+    if (a.n_in == 3) return launch_rows_pair<3, false>(a, src, dst, nullptr, 0, 1, 1, stream);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_step2_mfma_up(const StepArgs &a, MfmaMlp mlp, Layout2d layout,
+                                const void *coarse, int coarse_w, int fy, int fx, const void *img,
+                                void *dst, hipStream_t stream) {
+    if (!step_mfma_pairs(a, mlp, layout)) return hipErrorInvalidValue;
+    if (a.n_in == 1)
+        return launch_rows_pair<1, true>(a, coarse, dst, img, coarse_w, fy, fx, stream);
+    if (a.n_in == 3)
+        return launch_rows_pair<3, true>(a, coarse, dst, img, coarse_w, fy, fx, stream);
     return hipErrorInvalidValue;
 }
 

@@ -340,19 +340,21 @@ def test_train_workspace_and_step_validation(lib):
 
 def test_infer_launches_counts_two_step_launches(monkeypatch):
     """Host query of the launches octree_nca_infer enqueues: on the 184.5 MP
-    pyramid the three large levels run their first step fused with the
-    upsample and the other 19 in 9 two-step launches and one single one; the
+    pyramid the three large levels run their 20 steps in 10 two-step launches,
+    the first fused with the upsample; an odd count adds one single step; the
     smaller levels and the one-step selection run one launch per step."""
     m = octnca.Model(ndim=2, n_in=3)
     f = [(1, 2, 2)] * 5
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma")
     assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == \
-        [11, 11, 11, 20, 20, 20]
+        [10, 10, 10, 20, 20, 20]
+    assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [19, 1, 2, 20, 20, 20]) == \
+        [10, 1, 1, 20, 20, 20]
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_1step")
     assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == [20] * 6
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
     assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 0]) == \
-        [3, 3, 0]
+        [3, 2, 0]
     monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "valu")
     assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 3]) == \
         [5, 4, 3]

@@ -86,3 +86,30 @@ def test_two_step_default_on_a_large_level(gpu, monkeypatch):
     want, which1 = run(monkeypatch, "mfma_1step", s, w, 3, 3, 0.5, level=0)
     assert (which, which1) == (0, 1)   # 2 launches against 3
     assert torch.equal(got, want)
+
+
+@pytest.mark.parametrize("steps", [(2, 3, 1), (5, 4, 2), (1, 2, 3), (6, 0, 4)],
+                         ids=lambda s: "s" + "-".join(map(str, s)))
+@pytest.mark.parametrize("factors", [((1, 2, 2), (1, 2, 2)), ((1, 3, 2), (1, 1, 3))],
+                         ids=["f22", "f32-13"])
+def test_two_step_inference_equals_single_steps(gpu, monkeypatch, steps, factors):
+    """Whole inference with two-step launches (the first of a level fused with
+    the upsample when the level has two or more steps) against one step per
+    launch: the final state and the readout are equal bit for bit."""
+    from synthetic import Workload, make_image, make_weights
+    from paper_2508_06993_amd.runtime import Inference, to_device_image
+    wl = Workload(name="two_step_infer", ndim=2, extent=(1, 72, 96), n_in=3, factors=factors,
+                  steps=steps, image_kind="uniform")
+    model = octnca.Model(ndim=2, n_in=3)
+    image = to_device_image(make_image(wl), model)
+    weights = upload_weights(make_weights(wl))
+    out = {}
+    for kernel in ("mfma_rows", "mfma_rows,mfma_1step"):
+        monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
+        print(f"two-step inference steps={steps} factors={factors} kernel={kernel}", flush=True)
+        run = Inference(model, wl.extent, wl.factors)
+        state, seg = run(image, weights, wl.steps, wl.fire_rate, wl.seed)
+        torch.cuda.synchronize()
+        out[kernel] = (state.clone(), seg.clone())
+    assert torch.equal(out["mfma_rows"][0], out["mfma_rows,mfma_1step"][0])
+    assert torch.equal(out["mfma_rows"][1], out["mfma_rows,mfma_1step"][1])
