@@ -17,10 +17,11 @@
 //      gP (halo tile of gP in LDS);
 //   3. wgrad_partials: per block of 64 consecutive cells, the sums of every
 //      weight-gradient entry (records staged in LDS cell-major, 4 x 4 register
-//      blocks of the outer-product sums), stored entry-major;
-//   4. wgrad_reduce: one wave per entry adds the block sums in fp64 (lane l
-//      takes blocks l, l + 64, ... in order, then a fixed shuffle tree) to
-//      the caller's gradients (accumulated, so the steps of a level sum up).
+//      blocks of the outer-product sums), stored block-major;
+//   4. wgrad_reduce: per 64 entries, 16 waves add the block sums in fp64
+//      (wave w takes blocks w, w + 16, ... in order, then the waves' sums in
+//      wave order) to the caller's gradients (accumulated, so the steps of a
+//      level sum up).
 #include "launch.h"
 
 namespace octnca {
@@ -254,7 +255,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
 // operands: a 4 x 4 block of dW1 (ga[j..j+3] x f[k..k+3]) or of dW2
 // (gu[c..c+3] x h[j..j+3]), four entries of db1 or dconv_b, or one tap of
 // dconv_w for four channels; per cell a job reads two 16-byte words and does
-// up to 16 FMAs, in cell order.  Sums are stored entry-major.
+// up to 16 FMAs, in cell order.  Sums are stored block-major (each block
+// writes one contiguous row; entry-major rows scattered every write).
 template <int NDIM, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     const float *__restrict__ src, const float *__restrict__ rec, int dd, int dh, int dw,
@@ -279,8 +281,8 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
         const float4 v = *reinterpret_cast<const float4 *>(&recs[cell * RS + e]);
         return v;
     };
-    const int64_t nb = gridDim.x;
-    auto put = [&](int o, float v) { partial[(int64_t)o * nb + blockIdx.x] = v; };
+    // block-major partial sums: one contiguous row of G::N words per block
+    auto put = [&](int o, float v) { partial[(int64_t)blockIdx.x * G::N + o] = v; };
     constexpr int J1 = (H / 4) * (2 * C / 4);    // dW1 blocks
     constexpr int J2 = (C / 4) * (H / 4);        // dW2 blocks
     constexpr int JB = H / 4, JC = C / 4;        // db1, dconv_b quads
@@ -358,28 +360,36 @@ __global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
     }
 }
 
-// grads += the sum of the block partial sums of each entry: one wave per
-// entry, lane l summing blocks l, l + 64, ... in order in fp64, then a fixed
-// butterfly over the lanes (deterministic).
+// grads += the sum of the block partial sums of each entry.  A block of
+// kRedWaves waves takes 64 consecutive entries; wave w sums block rows w,
+// w + kRedWaves, ... in order in fp64 (lane = entry, so each row read is one
+// coalesced 256-byte segment), and the waves' sums are added in wave order
+// (deterministic).
+constexpr int kRedWaves = 16;
 template <int C, int H, int TAPS>
-__global__ __launch_bounds__(kBwdThreads) void wgrad_reduce(const float *__restrict__ partial,
-                                                            int64_t blocks, LevelGradsDev g) {
+__global__ __launch_bounds__(64 * kRedWaves) void wgrad_reduce(const float *__restrict__ partial,
+                                                               int64_t blocks, LevelGradsDev g) {
     using G = WG<C, H, TAPS>;
-    const int o = blockIdx.x * (kBwdThreads / 64) + (int)(threadIdx.x >> 6);
-    const int lane = threadIdx.x & 63;
-    if (o >= G::N) return;                               // uniform over the wave
+    __shared__ double red[kRedWaves][64];
+    const int lane = threadIdx.x & 63, w = (int)(threadIdx.x >> 6);
+    const int o = blockIdx.x * 64 + lane;
+    const int oc = min(o, G::N - 1);
     double s = 0.0;
-    for (int64_t b = lane; b < blocks; b += 64) s += (double)partial[(int64_t)o * blocks + b];
+#pragma unroll 8
+    for (int64_t b = w; b < blocks; b += kRedWaves) s += (double)partial[b * G::N + oc];
+    red[w][lane] = s;
+    __syncthreads();
+    if (w != 0 || o >= G::N) return;
+    double t = red[0][lane];
 #pragma unroll
-    for (int m = 32; m > 0; m >>= 1) s += __shfl_xor(s, m);
-    if (lane != 0) return;
+    for (int k = 1; k < kRedWaves; ++k) t += red[k][lane];
     float *dst;
     if (o < G::W2) dst = g.w1 + o;
     else if (o < G::B1) dst = g.w2 + (o - G::W2);
     else if (o < G::CB) dst = g.b1 + (o - G::B1);
     else if (o < G::CW) dst = g.conv_b + (o - G::CB);
     else dst = g.conv_w + (o - G::CW);
-    *dst = (float)((double)*dst + s);
+    *dst = (float)((double)*dst + t);
 }
 
 template <int NDIM, int NIN, int C, int H>
@@ -412,9 +422,7 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
         cells);
     wgrad_partials<NDIM, C, H><<<(unsigned)chunks, kBwdThreads, 0, stream>>>(
         src, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, cells, partial);
-    constexpr int kWavesPerBlock = kBwdThreads / 64;
-    wgrad_reduce<C, H, TAPS><<<(G::N + kWavesPerBlock - 1) / kWavesPerBlock, kBwdThreads, 0,
-                               stream>>>(partial, chunks, g);
+    wgrad_reduce<C, H, TAPS><<<(G::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(partial, chunks, g);
     return hipGetLastError();
 }
 
