@@ -518,7 +518,7 @@ int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_
 size_t octree_nca_step_backward_workspace_bytes(const octnca_model *model, octnca_extent extent) {
     if (check_model(model) || check_extent(model, extent)) return 0;
     return step_backward_workspace_floats(model->ndim, model->channels, model->hidden,
-                                          extent.d * extent.h * extent.w) *
+                                          ext3(extent)) *
            sizeof(float);
 }
 
@@ -637,7 +637,9 @@ int make_train_plan(const octnca_model *m, octnca_extent finest, int32_t levels,
     p->grad_off[1] = off;
     off += gb;
     p->bwd_off = off;
-    off += align_up(step_backward_workspace_floats(m->ndim, m->channels, m->hidden, cells) * 4);
+    // the finest level needs the most (every level's extent is at most the finest's)
+    off += align_up(step_backward_workspace_floats(m->ndim, m->channels, m->hidden, ext3(finest)) *
+                    4);
     p->mse_off = off;
     off += align_up(mse_workspace_doubles(cells) * sizeof(double));
     p->bytes = off;

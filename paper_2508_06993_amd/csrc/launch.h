@@ -68,7 +68,7 @@ hipError_t launch_step_pair_up(const StepArgs &a, const void *coarse, int coarse
 // Training (fp32 states): backward of one step (state `src` before the step,
 // gout = dL/dS'), writing gin = dL/dS (may alias gout) and adding the weight
 // gradients to g; ws holds step_backward_workspace_floats floats.
-size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_t cells);
+size_t step_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 extent);
 hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,
                                 float *gin, LevelGradsDev g, float *ws, hipStream_t stream);
 // Adjoint of the upsample + inject from `coarse` (extent of the coarse level).

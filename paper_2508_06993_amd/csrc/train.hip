@@ -73,11 +73,91 @@ __device__ __forceinline__ void stage(Load load, Store store) {
     }
 }
 
+// Sums over kWgCells cells of every weight-gradient entry, from the cells'
+// records in LDS (a row of RS = R::N + 4 words per cell, zero rows for cells
+// outside the grid).  Each thread takes jobs of entries that share operands:
+// a 4 x 4 block of dW1 (ga[j..j+3] x f[k..k+3]) or of dW2 (gu[c..c+3] x
+// h[j..j+3]), four entries of db1 or dconv_b, or one tap of dconv_w for four
+// channels (state(p, t, c) gives channel c of the tap-t neighbour of cell p);
+// per cell a job reads two 16-byte words and does up to 16 FMAs, in cell
+// order.  out receives the G::N sums (one block-major row).
+template <int NDIM, int C, int H, class State>
+__device__ __forceinline__ void wgrad_block(const float *recs, State state, float *out) {
+    using R = Rec<C, H>;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    using G = WG<C, H, TAPS>;
+    static_assert(C % 4 == 0 && H % 4 == 0, "entries in blocks of 4");
+    constexpr int RS = R::N + 4;
+    auto quad = [&](int cell, int e) {
+        return *reinterpret_cast<const float4 *>(&recs[cell * RS + e]);
+    };
+    constexpr int J1 = (H / 4) * (2 * C / 4);    // dW1 blocks
+    constexpr int J2 = (C / 4) * (H / 4);        // dW2 blocks
+    constexpr int JB = H / 4, JC = C / 4;        // db1, dconv_b quads
+    constexpr int JK = (C / 4) * TAPS;           // dconv_w (channel quad, tap)
+    constexpr int NJ = J1 + J2 + JB + JC + JK;
+    for (int job = threadIdx.x; job < NJ; job += kBwdThreads) {
+        if (job < J1 + J2) {
+            int ea, eb, o0, os;
+            if (job < J1) {                      // dW1[j][k] = sum ga[j] f[k]
+                const int jb = job / (2 * C / 4), kb = job % (2 * C / 4);
+                ea = R::GA + 4 * jb; eb = R::F + 4 * kb;
+                o0 = G::W1 + 4 * jb * 2 * C + 4 * kb; os = 2 * C;
+            } else {                             // dW2[c][j] = sum gu[c] h[j]
+                const int jj = job - J1, cb = jj / (H / 4), jb = jj % (H / 4);
+                ea = R::GU + 4 * cb; eb = R::Hh + 4 * jb;
+                o0 = G::W2 + 4 * cb * H + 4 * jb; os = H;
+            }
+            float acc[4][4] = {};
+#pragma unroll 4
+            for (int i = 0; i < kWgCells; ++i) {
+                const float4 av = quad(i, ea), bv = quad(i, eb);
+                const float ar[4] = {av.x, av.y, av.z, av.w}, br[4] = {bv.x, bv.y, bv.z, bv.w};
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(ar[r], br[c], acc[r][c]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) out[o0 + r * os + c] = acc[r][c];
+        } else if (job < J1 + J2 + JB + JC) {    // db1[j] = sum ga[j]; dconv_b[c] = sum gP[c]
+            const int jj = job - J1 - J2;
+            const int e = jj < JB ? R::GA + 4 * jj : R::GP + 4 * (jj - JB);
+            const int o0 = jj < JB ? G::B1 + 4 * jj : G::CB + 4 * (jj - JB);
+            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            for (int i = 0; i < kWgCells; ++i) {
+                const float4 v = quad(i, e);
+                sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[o0 + r] = sum[r];
+        } else {                                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
+            const int jj = job - J1 - J2 - JB - JC;
+            const int cq = jj / TAPS, t = jj % TAPS;
+            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+            for (int i = 0; i < kWgCells; ++i) {
+                const float4 gpv = quad(i, R::GP + 4 * cq);
+                sum[0] = fmaf(gpv.x, state(i, t, 4 * cq + 0), sum[0]);
+                sum[1] = fmaf(gpv.y, state(i, t, 4 * cq + 1), sum[1]);
+                sum[2] = fmaf(gpv.z, state(i, t, 4 * cq + 2), sum[2]);
+                sum[3] = fmaf(gpv.w, state(i, t, 4 * cq + 3), sum[3]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[G::CW + (4 * cq + r) * TAPS + t] = sum[r];
+        }
+    }
+}
+
 // bwd_cell: a quad of lanes per cell (lane = 4 * cell + part); part p takes
 // hidden units j = 4 i + p, and the four partial feature gradients W1^T ga
 // are summed across the quad.  Blocks of 64 cells.  W1 and W2^T sit in LDS
 // with rows padded by 4 words, so the quad's four rows fall in different
-// banks.
+// banks.  The cells' records stay in LDS, and the block then forms its sums of
+// every weight-gradient entry from them (see wgrad_block) and stores one
+// block-major row of partial sums; only G' + gS and gP go to memory.
 constexpr int kParts = 4;
 template <int NDIM> struct BwdCellTile;
 template <> struct BwdCellTile<2> { static constexpr int TZ = 1, TY = 2, TX = 32; };
@@ -89,7 +169,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     int tiles_x, int tiles_y, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
-    float *__restrict__ gpart, float *__restrict__ rec, int64_t cells) {
+    float *__restrict__ gpart, float *__restrict__ gp, float *__restrict__ partial,
+    int64_t cells) {
     using T = BwdCellTile<NDIM>;
     using R = Rec<C, H>;
     constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
@@ -102,6 +183,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     __shared__ __align__(16) float sw1[H][2 * C + 4];   // W1
     __shared__ __align__(16) float sw2[H][C + 4];       // W2^T
     __shared__ float sb1[H];
+    constexpr int RS = R::N + 4;   // words per record row (16-byte aligned rows)
+    __shared__ __align__(16) float recs[kWgCells * RS];   // [cell][entry]
 
     int b = blockIdx.x;
     const int bx = b % tiles_x;
@@ -157,7 +240,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
 #pragma unroll
     for (int c = 0; c < C; ++c) gu[c] = (c >= NIN && fire) ? g[c] : 0.f;
 
-    float *r = rec + idx;   // entry k at r[k * cells]
+    float *r = recs + cl * RS;   // this cell's record row
     float gf[2 * C];
 #pragma unroll
     for (int k = 0; k < 2 * C; ++k) gf[k] = 0.f;
@@ -173,10 +256,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
         const float ga = a > 0.f ? gh : 0.f;
 #pragma unroll
         for (int k = 0; k < 2 * C; ++k) gf[k] = fmaf(sw1[j][k], ga, gf[k]);
-        if (valid) {
-            r[(R::Hh + j) * cells] = fmaxf(a, 0.f);
-            r[(R::GA + j) * cells] = ga;
-        }
+        r[R::Hh + j] = valid ? fmaxf(a, 0.f) : 0.f;   // a cell outside the grid adds 0
+        r[R::GA + j] = valid ? ga : 0.f;
     }
     // sum of the quad's four partial W1^T ga (the same order in every lane)
 #pragma unroll
@@ -184,27 +265,37 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
         gf[k] += __shfl_xor(gf[k], 1);
         gf[k] += __shfl_xor(gf[k], 2);
     }
-    if (!valid) return;
     constexpr int FP = 2 * C / kParts, CP = C / kParts;
 #pragma unroll
     for (int k = 0; k < 2 * C; ++k)
-        if (k / FP == part) r[(R::F + k) * cells] = f[k];
+        if (k / FP == part) r[R::F + k] = valid ? f[k] : 0.f;
 #pragma unroll
     for (int c = 0; c < C; ++c)
         if (c / CP == part) {
-            r[(R::GU + c) * cells] = gu[c];
-            r[(R::GP + c) * cells] = gf[C + c];
-            gpart[idx * C + c] = g[c] + gf[c];
+            r[R::GU + c] = valid ? gu[c] : 0.f;
+            r[R::GP + c] = valid ? gf[C + c] : 0.f;
+            if (valid) {
+                gp[c * cells + idx] = gf[C + c];
+                gpart[idx * C + c] = g[c] + gf[c];
+            }
         }
+    __syncthreads();
+    // dconv_w needs S at the neighbours of cell p: tile word of p's centre
+    // plus the tap's offset (zero outside the grid, as staged)
+    wgrad_block<NDIM, C, H>(recs, [&](int p, int t, int c) {
+        const int px = p % T::TX, py = (p / T::TX) % T::TY, pz = p / (T::TX * T::TY);
+        const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+        const int nb = ((pz + (NDIM == 3 ? 1 : 0) + dz) * HY + py + 1 + dy) * HX + px + 1 + dx;
+        return tile[c][nb];
+    }, partial + (int64_t)blockIdx.x * WG<C, H, TAPS>::N);
 }
 
 template <int NDIM, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
-    const float *__restrict__ gpart, const float *__restrict__ rec, int dd, int dh, int dw,
+    const float *__restrict__ gpart, const float *__restrict__ gp, int dd, int dh, int dw,
     int tiles_x, int tiles_y, const float *__restrict__ conv_w, float *__restrict__ gin,
     int64_t cells) {
     using T = BwdTile<NDIM>;
-    using R = Rec<C, H>;
     constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
     constexpr int NCELL = HZ * HY * HX;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
@@ -224,7 +315,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
             const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
             const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
                       cz = min(max(gz, 0), dd - 1);
-            const float v = rec[(R::GP + c) * cells + ((int64_t)cz * dh + cy) * dw + cx];
+            const float v = gp[c * cells + ((int64_t)cz * dh + cy) * dw + cx];
             return in ? v : 0.f;
         },
         [&](int i, float v) { tile[i / NCELL][i % NCELL] = v; });
@@ -246,117 +337,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
             v = fmaf(conv_w[c * TAPS + t], tile[c][centre - (dz * HY + dy) * HX - dx], v);
         }
         gin[idx * C + c] = v;
-    }
-}
-
-// Sums over a block's kWgCells consecutive cells of every weight-gradient
-// entry.  The block stages its cells' records in LDS cell by cell (a row of
-// R::N words per cell), and each thread takes jobs of entries that share
-// operands: a 4 x 4 block of dW1 (ga[j..j+3] x f[k..k+3]) or of dW2
-// (gu[c..c+3] x h[j..j+3]), four entries of db1 or dconv_b, or one tap of
-// dconv_w for four channels; per cell a job reads two 16-byte words and does
-// up to 16 FMAs, in cell order.  Sums are stored block-major (each block
-// writes one contiguous row; entry-major rows scattered every write).
-template <int NDIM, int C, int H>
-__global__ __launch_bounds__(kBwdThreads) void wgrad_partials(
-    const float *__restrict__ src, const float *__restrict__ rec, int dd, int dh, int dw,
-    int64_t cells, float *__restrict__ partial) {
-    using R = Rec<C, H>;
-    constexpr int TAPS = NDIM == 3 ? 27 : 9;
-    using G = WG<C, H, TAPS>;
-    static_assert(C % 4 == 0 && H % 4 == 0, "entries in blocks of 4");
-    constexpr int RS = R::N + 4;   // words per staged record (16-byte aligned rows)
-    __shared__ __align__(16) float recs[kWgCells * RS];   // [cell][entry]
-    const int64_t first = (int64_t)blockIdx.x * kWgCells;
-    const int n = (int)min<int64_t>(kWgCells, cells - first);
-    stage<kWgCells * R::N, 16>(
-        [&](int i) {
-            const int k = i / kWgCells, cell = i % kWgCells;
-            const float v = rec[k * cells + first + min(cell, n - 1)];
-            return cell < n ? v : 0.f;
-        },
-        [&](int i, float v) { recs[(i % kWgCells) * RS + i / kWgCells] = v; });
-    __syncthreads();
-    auto quad = [&](int cell, int e) {
-        const float4 v = *reinterpret_cast<const float4 *>(&recs[cell * RS + e]);
-        return v;
-    };
-    // block-major partial sums: one contiguous row of G::N words per block
-    auto put = [&](int o, float v) { partial[(int64_t)blockIdx.x * G::N + o] = v; };
-    constexpr int J1 = (H / 4) * (2 * C / 4);    // dW1 blocks
-    constexpr int J2 = (C / 4) * (H / 4);        // dW2 blocks
-    constexpr int JB = H / 4, JC = C / 4;        // db1, dconv_b quads
-    constexpr int JK = (C / 4) * TAPS;           // dconv_w (channel quad, tap)
-    constexpr int NJ = J1 + J2 + JB + JC + JK;
-    for (int job = threadIdx.x; job < NJ; job += kBwdThreads) {
-        if (job < J1 + J2) {
-            int ea, eb, o0, os;
-            if (job < J1) {                      // dW1[j][k] = sum ga[j] f[k]
-                const int jb = job / (2 * C / 4), kb = job % (2 * C / 4);
-                ea = R::GA + 4 * jb; eb = R::F + 4 * kb;
-                o0 = G::W1 + 4 * jb * 2 * C + 4 * kb; os = 2 * C;
-            } else {                             // dW2[c][j] = sum gu[c] h[j]
-                const int jj = job - J1, cb = jj / (H / 4), jb = jj % (H / 4);
-                ea = R::GU + 4 * cb; eb = R::Hh + 4 * jb;
-                o0 = G::W2 + 4 * cb * H + 4 * jb; os = H;
-            }
-            float acc[4][4] = {};
-#pragma unroll 4
-            for (int i = 0; i < n; ++i) {
-                const float4 av = quad(i, ea), bv = quad(i, eb);
-                const float ar[4] = {av.x, av.y, av.z, av.w}, br[4] = {bv.x, bv.y, bv.z, bv.w};
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-#pragma unroll
-                    for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(ar[r], br[c], acc[r][c]);
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-                for (int c = 0; c < 4; ++c) put(o0 + r * os + c, acc[r][c]);
-        } else if (job < J1 + J2 + JB + JC) {    // db1[j] = sum ga[j]; dconv_b[c] = sum gP[c]
-            const int jj = job - J1 - J2;
-            const int e = jj < JB ? R::GA + 4 * jj : R::GP + 4 * (jj - JB);
-            const int o0 = jj < JB ? G::B1 + 4 * jj : G::CB + 4 * (jj - JB);
-            float sum[4] = {0.f, 0.f, 0.f, 0.f};
-            for (int i = 0; i < n; ++i) {
-                const float4 v = quad(i, e);
-                sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) put(o0 + r, sum[r]);
-        } else {                                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
-            const int jj = job - J1 - J2 - JB - JC;
-            const int cq = jj / TAPS, t = jj % TAPS;
-            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
-            int64_t p = first;
-            int x = (int)(p % dw), y = (int)((p / dw) % dh), z = (int)(p / ((int64_t)dw * dh));
-            float sum[4] = {0.f, 0.f, 0.f, 0.f};
-            // neighbour loads without branches (clamped address, 0/1 weight),
-            // so that the loads of several cells are in flight together
-#pragma unroll 16
-            for (int i = 0; i < n; ++i) {
-                const int gx = x + dx, gy = y + dy, gz = z + dz;
-                const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
-                const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
-                          cz = min(max(gz, 0), dd - 1);
-                const float4 sv = *reinterpret_cast<const float4 *>(
-                    &src[(((int64_t)cz * dh + cy) * dw + cx) * C + 4 * cq]);
-                const float w = in ? 1.f : 0.f;
-                const float4 gp = quad(i, R::GP + 4 * cq);
-                sum[0] = fmaf(gp.x, w * sv.x, sum[0]);
-                sum[1] = fmaf(gp.y, w * sv.y, sum[1]);
-                sum[2] = fmaf(gp.z, w * sv.z, sum[2]);
-                sum[3] = fmaf(gp.w, w * sv.w, sum[3]);
-                const bool wrap = ++x == dw;   // next cell in row-major order
-                x = wrap ? 0 : x;
-                const bool wrap_y = wrap && ++y == dh;
-                y = wrap_y ? 0 : y;
-                z += wrap_y ? 1 : 0;
-            }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) put(G::CW + (4 * cq + r) * TAPS + t, sum[r]);
-        }
     }
 }
 
@@ -396,33 +376,29 @@ template <int NDIM, int NIN, int C, int H>
 hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, float *gin,
                       LevelGradsDev g, float *ws, hipStream_t stream) {
     using T = BwdTile<NDIM>;
-    using R = Rec<C, H>;
+    using TC = BwdCellTile<NDIM>;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
-    using G = WG<C, H, TAPS>;
     const int64_t cells = a.ext.cells();
+    if (cells == 0) return hipSuccess;
     const int tiles_x = (int)((a.ext.w + T::TX - 1) / T::TX);
     const int tiles_y = (int)((a.ext.h + T::TY - 1) / T::TY);
     const int tiles_z = (int)((a.ext.d + T::TZ - 1) / T::TZ);
     const int64_t blocks = (int64_t)tiles_x * tiles_y * tiles_z;
-    const int64_t chunks = (cells + kWgCells - 1) / kWgCells;
-    if (cells == 0) return hipSuccess;
-    float *gpart = ws;
-    float *rec = gpart + cells * C;
-    float *partial = rec + cells * R::N;
-    using TC = BwdCellTile<NDIM>;
     const int ctiles_x = (int)((a.ext.w + TC::TX - 1) / TC::TX);
     const int ctiles_y = (int)((a.ext.h + TC::TY - 1) / TC::TY);
     const int64_t cblocks = (int64_t)ctiles_x * ctiles_y * ((a.ext.d + TC::TZ - 1) / TC::TZ);
+    float *gpart = ws;                 // G' + gS
+    float *gp = gpart + cells * C;     // gP, [C][cells]
+    float *partial = gp + cells * C;   // [cblocks][entries]
     bwd_cell<NDIM, NIN, C, H><<<(unsigned)cblocks, kBwdThreads, 0, stream>>>(
         src, gout, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, ctiles_x, ctiles_y, a.w.conv_w,
         a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold, gpart,
-        rec, cells);
+        gp, partial, cells);
     bwd_conv_t<NDIM, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
-        gpart, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w, gin,
+        gpart, gp, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w, gin,
         cells);
-    wgrad_partials<NDIM, C, H><<<(unsigned)chunks, kBwdThreads, 0, stream>>>(
-        src, rec, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, cells, partial);
-    wgrad_reduce<C, H, TAPS><<<(G::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(partial, chunks, g);
+    wgrad_reduce<C, H, TAPS><<<(WG<C, H, TAPS>::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(
+        partial, cblocks, g);
     return hipGetLastError();
 }
 
@@ -508,12 +484,15 @@ __global__ __launch_bounds__(256) void fill_zero(float *__restrict__ p, int64_t 
 
 }  // namespace
 
-size_t step_backward_workspace_floats(int ndim, int channels, int hidden, int64_t cells) {
+size_t step_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 e) {
     const int taps = ndim == 3 ? 27 : 9;
-    const int64_t rec_n = 4 * channels + 2 * hidden;
+    const int64_t cells = e.cells();
     const int64_t wg_n = 3 * channels * hidden + hidden + channels + channels * taps;
-    const int64_t blocks = (cells + kWgCells - 1) / kWgCells;
-    return (size_t)(cells * channels + cells * rec_n + blocks * wg_n);
+    // bwd_cell blocks: 2 x 32 cells (2D), 2 x 4 x 8 (3D)
+    const int64_t tz = ndim == 3 ? 2 : 1, ty = ndim == 3 ? 4 : 2, tx = ndim == 3 ? 8 : 32;
+    const int64_t cblocks =
+        ((e.d + tz - 1) / tz) * ((e.h + ty - 1) / ty) * ((e.w + tx - 1) / tx);
+    return (size_t)(2 * cells * channels + cblocks * wg_n);
 }
 
 hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,

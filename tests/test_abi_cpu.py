@@ -260,16 +260,23 @@ def grads():
     return ctypes.byref(_LevelGrads(FAKE, FAKE, FAKE, FAKE, FAKE))
 
 
-def bwd_ws_floats(cells, c=16, h=64, taps=9):
-    chunks = (cells + 63) // 64
-    return cells * c + cells * (4 * c + 2 * h) + chunks * (3 * c * h + h + c + c * taps)
+def bwd_ws_floats(ext, c=16, h=64, ndim=2):
+    """G' + gS and gP (C floats per cell each), and one row of weight-gradient
+    sums per block of the per-cell backward (2 x 32 cells in 2D, 2 x 4 x 8 in
+    3D)."""
+    d, hh, w = ext
+    cells = d * hh * w
+    taps = 27 if ndim == 3 else 9
+    tz, ty, tx = (2, 4, 8) if ndim == 3 else (1, 2, 32)
+    blocks = -(-d // tz) * -(-hh // ty) * -(-w // tx)
+    return 2 * cells * c + blocks * (3 * c * h + h + c + c * taps)
 
 
 def test_step_backward_workspace_bytes(lib):
     assert lib.octree_nca_step_backward_workspace_bytes(model(), _Extent(1, 8, 10)) == \
-        4 * bwd_ws_floats(80)
+        4 * bwd_ws_floats((1, 8, 10))
     assert lib.octree_nca_step_backward_workspace_bytes(model(ndim=3, n_in=1), _Extent(3, 5, 7)) \
-        == 4 * bwd_ws_floats(105, taps=27)
+        == 4 * bwd_ws_floats((3, 5, 7), ndim=3)
     assert lib.octree_nca_step_backward_workspace_bytes(model(ndim=4), _Extent(1, 8, 8)) == 0
 
 
