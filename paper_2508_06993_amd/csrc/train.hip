@@ -8,18 +8,17 @@
 //   gu = m G' (hidden channels), dW2 += gu h^T, ga = (W2^T gu) * [a > 0],
 //   dW1 += ga f^T, db1 += ga, [gS, gP] = W1^T ga, dconv_b += gP,
 //   dK[c][t] += gP[p][c] S[p + o_t][c], dL/dS = G' + gS + conv^T(gP).
-// Four launches:
-//   1. bwd_cell: four lanes per cell (halo tile of S in LDS): perception,
-//      then the hidden units streamed once, a quarter per lane, each giving
-//      a, h, gh and ga; writes G' + gS and the cell's record
-//      [f | h | ga | gu | gP] for the weight gradients;
+// Three launches:
+//   1. bwd_cell: four lanes per cell, blocks of 64 cells (halo tile of S in
+//      LDS): perception, then the hidden units streamed once, a quarter per
+//      lane, each giving a, h, gh and ga; writes G' + gS and gP to memory and
+//      keeps the cells' records [f | h | ga | gu | gP] in LDS, from which the
+//      block forms its sums of every weight-gradient entry (4 x 4 register
+//      blocks of the outer-product sums) and stores them as one row;
 //   2. bwd_conv_t: dL/dS = (G' + gS) + the transposed depthwise convolution of
 //      gP (halo tile of gP in LDS);
-//   3. wgrad_partials: per block of 64 consecutive cells, the sums of every
-//      weight-gradient entry (records staged in LDS cell-major, 4 x 4 register
-//      blocks of the outer-product sums), stored block-major;
-//   4. wgrad_reduce: per 64 entries, 16 waves add the block sums in fp64
-//      (wave w takes blocks w, w + 16, ... in order, then the waves' sums in
+//   3. wgrad_reduce: per 64 entries, 16 waves add the block rows in fp64
+//      (wave w takes rows w, w + 16, ... in order, then the waves' sums in
 //      wave order) to the caller's gradients (accumulated, so the steps of a
 //      level sum up).
 #include "launch.h"
