@@ -1926,17 +1926,19 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                                : kOut;
         }
 
-        // rolling perception sums (bias included) of outputs p - 1, p, p + 1,
-        // channels (4g, 4g+1) in [.][0] and (4g+2, 4g+3) in [.][1]
-        h2 acc_p[4][2], acc_c[4][2], acc_n[4][2];
+        // Rolling perception sums (bias included), channels (4g, 4g+1) in
+        // [.][0] and (4g+2, 4g+3) in [.][1]: A[(r - z_begin + 1) % 3] holds the
+        // sum of output plane r.  The plane loop is unrolled three times, so
+        // the three sums rotate roles instead of being moved; a run is padded
+        // to whole groups of three planes (the padding planes load nothing and
+        // store nothing).
+        h2 A[3][4][2];
 #pragma unroll
-        for (int grp = 0; grp < 4; ++grp)
+        for (int i = 0; i < 3; ++i)
 #pragma unroll
-            for (int k = 0; k < 2; ++k) {
-                acc_p[grp][k] = cb[k];
-                acc_c[grp][k] = cb[k];
-                acc_n[grp][k] = cb[k];
-            }
+            for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                for (int k = 0; k < 2; ++k) A[i][grp][k] = cb[k];
 
         __syncthreads();
         issue(z_begin - 1, true);
@@ -1944,9 +1946,15 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
         issue(z_begin, true);
         __syncthreads();
 
-        int slot = 0, slot_prev = 2;
-        for (int p = z_begin - 1; p <= z_end; ++p) {
-            const uint2 *pl = ring[slot];
+        // Plane p (j = (p - z_begin + 1) % 3) is in ring slot j, plane p - 1 in
+        // slot (j + 2) % 3, and plane p + 1 goes to slot (j + 1) % 3.
+        auto body = [&](int p, auto jc) {
+            constexpr int j = decltype(jc)::value;
+            constexpr int jm = (j + 2) % 3, jp = (j + 1) % 3;
+            h2 (&first)[4][2] = A[jp];    // output p + 1 (dz = -1 weights)
+            h2 (&second)[4][2] = A[j];    // output p (dz = 0)
+            h2 (&last)[4][2] = A[jm];     // output p - 1 (dz = +1), complete after
+            const uint2 *pl = ring[j];
             int gq = g;
             pin(gq);
             uint2 sv[2][4], wv[2][3];
@@ -1971,18 +1979,19 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                     const h2 v[2] = {as_h2(sv[t & 1][grp].x), as_h2(sv[t & 1][grp].y)};
 #pragma unroll
                     for (int k = 0; k < 2; ++k) {
-                        acc_n[grp][k] = __builtin_elementwise_fma(a_m[k], v[k], acc_n[grp][k]);
-                        acc_c[grp][k] = __builtin_elementwise_fma(a_0[k], v[k], acc_c[grp][k]);
-                        acc_p[grp][k] = __builtin_elementwise_fma(a_p[k], v[k], acc_p[grp][k]);
+                        first[grp][k] = __builtin_elementwise_fma(a_m[k], v[k],
+                                                                  t == 0 ? cb[k] : first[grp][k]);
+                        second[grp][k] = __builtin_elementwise_fma(a_0[k], v[k], second[grp][k]);
+                        last[grp][k] = __builtin_elementwise_fma(a_p[k], v[k], last[grp][k]);
                     }
                 }
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp)
 #pragma unroll
                     for (int k = 0; k < 2; ++k) {
-                        pin(acc_n[grp][k]);
-                        pin(acc_c[grp][k]);
-                        pin(acc_p[grp][k]);
+                        pin(first[grp][k]);
+                        pin(second[grp][k]);
+                        pin(last[grp][k]);
                     }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -2004,15 +2013,15 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
             const int slot0 = 2 * phase;
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
-            const uint2 *own = ring[slot_prev];
+            const uint2 *own = ring[jm];
             uint64_t fw_lane = 0;
             if constexpr (ALIGNED) fw_lane = fire_words[wave][n & 7];
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const uint2 sp = own[centre[grp]];
                 const h2 s01 = as_h2(sp.x), s23 = as_h2(sp.y);
-                const v8h fh = {s01[0], s01[1], s23[0], s23[1], acc_p[grp][0][0], acc_p[grp][0][1],
-                                acc_p[grp][1][0], acc_p[grp][1][1]};
+                const v8h fh = {s01[0], s01[1], s23[0], s23[1], last[grp][0][0], last[grp][0][1],
+                                last[grp][1][0], last[grp][1][1]};
                 v4f acc[4];
                 mlp.layer1_h(fh, acc);
                 const v4f u = mlp.layer2(acc);
@@ -2041,21 +2050,14 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                 __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
             }
 
-#pragma unroll
-            for (int grp = 0; grp < 4; ++grp)
-#pragma unroll
-                for (int k = 0; k < 2; ++k) {
-                    acc_p[grp][k] = acc_c[grp][k];
-                    acc_c[grp][k] = acc_n[grp][k];
-                    acc_n[grp][k] = cb[k];
-                }
-
-            const int slot_next = 3 - slot - slot_prev;
-            commit(ring[slot_next]);
+            commit(ring[jp]);
             issue(p + 2, p + 2 <= z_end);
             __syncthreads();
-            slot_prev = slot;
-            slot = slot_next;
+        };
+        for (int p0 = z_begin - 1; p0 <= z_end; p0 += 3) {
+            body(p0, std::integral_constant<int, 0>{});
+            body(p0 + 1, std::integral_constant<int, 1>{});
+            body(p0 + 2, std::integral_constant<int, 2>{});
         }
     }
 }
@@ -2175,12 +2177,16 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
 // item streams, its two halo planes included); ties go to the longer run.
 // Short runs spread small levels over the chip at the cost of reading their
 // halo planes again; long runs stream large levels with little re-reading.
-int pick_zrun(int64_t tiles, int64_t depth, int64_t slots) {
+// With groups of 3 (the fp16 kernel's plane loop is unrolled three times),
+// a work item streams its planes in whole groups of three.
+int pick_zrun(int64_t tiles, int64_t depth, int64_t slots, bool groups_of_3 = false) {
     int best = 1;
     int64_t best_cost = INT64_MAX;
     for (int r = 1; r <= k3ZRun; ++r) {
         const int64_t items = tiles * ((depth + r - 1) / r);
-        const int64_t cost = (items + slots - 1) / slots * (std::min<int64_t>(r, depth) + 2);
+        int64_t planes = std::min<int64_t>(r, depth) + 2;
+        if (groups_of_3) planes = (planes + 2) / 3 * 3;
+        const int64_t cost = (items + slots - 1) / slots * planes;
         if (cost <= best_cost) {
             best_cost = cost;
             best = r;
@@ -2195,7 +2201,7 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t slots = (int64_t)device_cus() * (kF16 ? k3hBlocksPerCu : kBlocksPerCu);
-    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots);
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, kF16);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
@@ -2226,7 +2232,7 @@ hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int 
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t slots = (int64_t)device_cus() * 2;
-    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots);
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
