@@ -1846,7 +1846,9 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     using Loader = RowLoader<__half, k3TY + 2>;
     __shared__ uint2 ring[3][4 * Loader::PS16];
     __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
-    __shared__ uint64_t fire_words[4][8];   // [wave][b]: ballot b of the last evaluation
+    // [wave][evaluation of the work item][b]: ballot b (k3ZRun / 4 evaluations
+    // at most: one per 4 or 8 planes)
+    __shared__ uint64_t fire_words[4][k3ZRun / 4][8];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1942,6 +1944,21 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
 
         __syncthreads();
         issue(z_begin - 1, true);
+        // All fire evaluations of the work item, before the plane loop (inside
+        // it they cost the loop registers): evaluation e covers output planes
+        // z_begin + e * planes_per_eval onwards.
+        for (int e = 0; z_begin + e * planes_per_eval < z_end; ++e) {
+            const int zo = z_begin + e * planes_per_eval;
+            const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
+            const uint64_t row =
+                (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
+            const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)), step,
+                                                level, batch, seed, threshold);
+            uint64_t word = fb.w[0];
+#pragma unroll
+            for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
+            fire_words[wave][e][lane & 7] = word;
+        }
         commit(ring[0]);
         issue(z_begin, true);
         __syncthreads();
@@ -1998,24 +2015,15 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
 
             const int zo = p - 1;
             const bool out_ok = zo >= z_begin && zo < z_end;
-            const int phase = (zo - z_begin) & (planes_per_eval - 1);
-            if (out_ok && phase == 0) {
-                const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
-                const uint64_t row =
-                    (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
-                const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
-                                                    step, level, batch, seed, threshold);
-                uint64_t word = fb.w[0];
-#pragma unroll
-                for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
-                fire_words[wave][lane & 7] = word;
-            }
+            const int zrel = min(max(zo - z_begin, 0), k3ZRun - 1);   // in range for any plane
+            const int phase = zrel & (planes_per_eval - 1);
+            const uint64_t *fwe = fire_words[wave][zrel / planes_per_eval];
             const int slot0 = 2 * phase;
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
             const uint2 *own = ring[jm];
             uint64_t fw_lane = 0;
-            if constexpr (ALIGNED) fw_lane = fire_words[wave][n & 7];
+            if constexpr (ALIGNED) fw_lane = fwe[n & 7];
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const uint2 sp = own[centre[grp]];
@@ -2034,7 +2042,7 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                     const int y = y0 + 2 * wave + r, x = x0 + (grp & 1) * 16 + n;
                     const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
                     const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
-                    const uint64_t fw = fire_words[wave][idx & 7];
+                    const uint64_t fw = fwe[idx & 7];
                     fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
                 }
                 const uint32_t off = offs[grp];
