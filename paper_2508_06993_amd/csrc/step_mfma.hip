@@ -1628,7 +1628,9 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     using Loader = RowLoader<T, k3TY + 2>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
-    __shared__ uint64_t fire_words[4][8];   // [wave][b]: ballot b of the last evaluation
+    // [wave][evaluation of the work item][b]: ballot b (k3ZRun / 4 evaluations
+    // at most: one per 4 or 8 planes)
+    __shared__ uint64_t fire_words[4][k3ZRun / 4][8];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1687,27 +1689,48 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         const int z_begin = zr * zrun;
         const int z_end = min(dd, z_begin + zrun);
 
-        // rolling perception sums (bias included) of outputs p - 1, p, p + 1
-        float acc_p[4][4], acc_c[4][4], acc_n[4][4];
+        // Rolling perception sums (bias included): A[(r - z_begin + 1) % 3]
+        // holds the sum of output plane r.  The plane loop is unrolled three
+        // times, so the sums rotate roles instead of being moved; a run is
+        // padded to whole groups of three planes (padding planes load and
+        // store nothing).
+        float A[3][4][4];
 #pragma unroll
-        for (int grp = 0; grp < 4; ++grp)
+        for (int i = 0; i < 3; ++i)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                acc_p[grp][k] = cb[k];
-                acc_c[grp][k] = cb[k];
-                acc_n[grp][k] = cb[k];
-            }
+            for (int grp = 0; grp < 4; ++grp)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) A[i][grp][k] = cb[k];
 
         __syncthreads();   // the previous item's readers are done with the ring
         ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
+        // All fire evaluations of the work item, before the plane loop:
+        // evaluation e covers output planes z_begin + e * planes_per_eval onwards.
+        for (int e = 0; z_begin + e * planes_per_eval < z_end; ++e) {
+            const int zo = z_begin + e * planes_per_eval;
+            const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
+            const uint64_t row =
+                (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
+            const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)), step,
+                                                level, batch, seed, threshold);
+            uint64_t word = fb.w[0];
+#pragma unroll
+            for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
+            fire_words[wave][e][lane & 7] = word;   // 8 lanes per address, same value
+        }
         ld.commit(ring[0]);
         ld.issue(src, z_begin, dd, dh, dw, y0, x0);
         __syncthreads();
 
-        int slot = 0;        // ring slot of plane p
-        int slot_prev = 2;   // ring slot of plane p - 1
-        for (int p = z_begin - 1; p <= z_end; ++p) {
-            const float4 *pl = ring[slot];
+        // Plane p (j = (p - z_begin + 1) % 3) is in ring slot j, plane p - 1 in
+        // slot (j + 2) % 3, and plane p + 1 goes to slot (j + 1) % 3.
+        auto body = [&](int p, auto jc) {
+            constexpr int j = decltype(jc)::value;
+            constexpr int jm = (j + 2) % 3, jp = (j + 1) % 3;
+            float (&first)[4][4] = A[jp];    // output p + 1 (dz = -1 weights)
+            float (&second)[4][4] = A[j];    // output p (dz = 0)
+            float (&last)[4][4] = A[jm];     // output p - 1 (dz = +1), complete after
+            const float4 *pl = ring[j];
             // Taps are software-pipelined: the LDS reads of tap t + 1 are issued
             // before the FMAs of tap t, and pinning the sums after each tap keeps
             // the compiler from hoisting every read of the plane at once.
@@ -1736,18 +1759,18 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                     const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        acc_n[grp][k] = fmaf(a_m[k], vv[k], acc_n[grp][k]);
-                        acc_c[grp][k] = fmaf(a_0[k], vv[k], acc_c[grp][k]);
-                        acc_p[grp][k] = fmaf(a_p[k], vv[k], acc_p[grp][k]);
+                        first[grp][k] = fmaf(a_m[k], vv[k], t == 0 ? cb[k] : first[grp][k]);
+                        second[grp][k] = fmaf(a_0[k], vv[k], second[grp][k]);
+                        last[grp][k] = fmaf(a_p[k], vv[k], last[grp][k]);
                     }
                 }
 #pragma unroll
                 for (int grp = 0; grp < 4; ++grp)
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        pin(acc_n[grp][k]);
-                        pin(acc_c[grp][k]);
-                        pin(acc_p[grp][k]);
+                        pin(first[grp][k]);
+                        pin(second[grp][k]);
+                        pin(last[grp][k]);
                     }
             }
             __builtin_amdgcn_sched_barrier(0);
@@ -1756,28 +1779,19 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
             // outside [z_begin, z_end) are dropped by an empty descriptor)
             const int zo = p - 1;
             const bool out_ok = zo >= z_begin && zo < z_end;
-            const int phase = (zo - z_begin) & (planes_per_eval - 1);
-            if (out_ok && phase == 0) {
-                const int zz = min(zo + (lane >> (lg_opr + 1)), dd - 1);
-                const uint64_t row =
-                    (uint64_t)zz * dh + (uint64_t)(y0 + 2 * wave + ((lane >> lg_opr) & 1));
-                const FireBallots fb = fire_ballots(((row * dw + x0) >> 3) + (lane & (opr - 1)),
-                                                    step, level, batch, seed, threshold);
-                uint64_t word = fb.w[0];
-#pragma unroll
-                for (int b = 1; b < 8; ++b) word = (lane & 7) == b ? fb.w[b] : word;
-                fire_words[wave][lane & 7] = word;   // 8 lanes per address, same value
-            }
+            const int zrel = min(max(zo - z_begin, 0), k3ZRun - 1);   // in range for any plane
+            const int phase = zrel & (planes_per_eval - 1);
+            const uint64_t *fwe = fire_words[wave][zrel / planes_per_eval];
             const int slot0 = 2 * phase;
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
-            const float4 *own = ring[slot_prev];
+            const float4 *own = ring[jm];
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const float4 sp = own[centre[grp]];
                 float f[8] = {sp.x, sp.y, sp.z, sp.w};
 #pragma unroll
-                for (int k = 0; k < 4; ++k) f[4 + k] = acc_p[grp][k];
+                for (int k = 0; k < 4; ++k) f[4 + k] = last[grp][k];
                 v4f acc[4];
                 mlp.layer1(f, acc);
                 const v4f u = mlp.layer2(acc);
@@ -1788,28 +1802,21 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
                 const uint32_t off =
                     x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-                const uint64_t fw = fire_words[wave][idx & 7];
+                const uint64_t fw = fwe[idx & 7];
                 const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
                 update_store(dst, wr, off, g, f, u, fires);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
-#pragma unroll
-            for (int grp = 0; grp < 4; ++grp)
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    acc_p[grp][k] = acc_c[grp][k];
-                    acc_c[grp][k] = acc_n[grp][k];
-                    acc_n[grp][k] = cb[k];
-                }
-
             // plane p + 1 into the free slot, then start loading p + 2
-            const int slot_next = 3 - slot - slot_prev;
-            ld.commit(ring[slot_next]);
+            ld.commit(ring[jp]);
             ld.issue(src, p + 2, dd, dh, dw, y0, x0, p + 2 <= z_end);
             __syncthreads();
-            slot_prev = slot;
-            slot = slot_next;
+        };
+        for (int p0 = z_begin - 1; p0 <= z_end; p0 += 3) {
+            body(p0, std::integral_constant<int, 0>{});
+            body(p0 + 1, std::integral_constant<int, 1>{});
+            body(p0 + 2, std::integral_constant<int, 2>{});
         }
     }
 }
@@ -2209,7 +2216,7 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t slots = (int64_t)device_cus() * (kF16 ? k3hBlocksPerCu : kBlocksPerCu);
-    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, kF16);
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
