@@ -136,9 +136,12 @@ int32_t fused_up_steps(const StepArgs &a, bool fused, int32_t steps) {
 
 // Enqueue steps t0 .. t1-1 of a level; launch k reads bufs[k % 2] and writes
 // bufs[(k + 1) % 2], so the result is in bufs[level_launches(..) % 2].
+// seg_last: when the last launch is a two-step launch, it also writes the
+// readout of its result there (null: no readout).
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
               const octnca_level_weights *w, int32_t level, int32_t t0, int32_t t1,
-              uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0) {
+              uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0,
+              uint8_t *seg_last = nullptr) {
     StepArgs a = step_args(m, e, w, level, seed, threshold, batch);
     void *bufs[2] = {b0, b1};
     const bool pairs = step_pairs(a);
@@ -147,7 +150,9 @@ int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
         a.step = (uint32_t)t;
         hipError_t err;
         if (pairs && t + 1 < t1) {
+            a.seg = t + 2 == t1 ? seg_last : nullptr;
             err = launch_step_pair(a, bufs[k], bufs[k ^ 1], stream);
+            a.seg = nullptr;
             t += 2;
         } else {
             err = launch_step(a, bufs[k], bufs[k ^ 1], stream);
@@ -405,6 +410,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
     if (launch_upsample(dt, nullptr, ext3(p.ext[levels - 1]), 1, 1, 1, img[levels - 1], bufs[cur],
                         model->n_in, model->channels, s) != hipSuccess)
         return OCTNCA_EHIP;
+    bool seg_fused = false;
     for (int l = levels - 1; l >= 0; --l) {
         const int32_t *f = factors + 3 * l;
         if (l < levels - 1 && !fused[l]) {
@@ -416,12 +422,22 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
         if (level_events && level_events[2 * l] &&
             hipEventRecord((hipEvent_t)level_events[2 * l], s) != hipSuccess)
             return OCTNCA_EHIP;
+        // The finest level's last launch writes the readout too when it is a
+        // two-step launch; otherwise the readout kernel runs at the end.
+        uint8_t *seg_last = nullptr;
+        if (l == 0 && seg != nullptr && steps[0] >= 2) {
+            const StepArgs a = step_args(model, p.ext[0], &weights[0], 0, seed, threshold, batch);
+            const int32_t first = fused_up_steps(a, fused[0], steps[0]);
+            if (step_pairs(a) && (steps[0] - first) % 2 == 0) seg_last = seg;
+            seg_fused = seg_last != nullptr;
+        }
         int32_t t0 = 0;
         if (fused[l]) {
             // step 0 (or steps 0 and 1) from the coarse state bufs[cur] (level
             // l + 1) and image l
-            const StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
+            StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch);
             t0 = fused_up_steps(a, true, steps[l]);
+            if (t0 == steps[l]) a.seg = seg_last;   // this launch is the level's last
             const hipError_t err =
                 t0 == 2 ? launch_step_pair_up(a, bufs[cur], (int)p.ext[l + 1].w, f[0], f[1], f[2],
                                               img[l], bufs[cur ^ 1], s)
@@ -431,7 +447,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
             cur ^= 1;
         }
         st = run_steps(model, bufs[cur], bufs[cur ^ 1], p.ext[l], &weights[l], l, t0, steps[l],
-                       seed, threshold, s, batch);
+                       seed, threshold, s, batch, seg_last);
         if (st) return st;
         cur ^= level_launches(step_args(model, p.ext[l], &weights[l], l, seed, threshold, batch),
                               t0, steps[l]) & 1;
@@ -440,7 +456,7 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
             return OCTNCA_EHIP;
     }
     // cur == 0 here by construction of the seed buffer
-    if (seg != nullptr &&
+    if (seg != nullptr && !seg_fused &&
         launch_readout(dt, bufs[cur], finest.d * finest.h * finest.w, model->channels, seg, s) !=
             hipSuccess)
         return OCTNCA_EHIP;

@@ -47,6 +47,9 @@ struct StepArgs {
     int hidden = kH;
     uint64_t seed;
     uint64_t threshold;
+    // Device [cells] uint8 or null: a two-step launch also writes the two-class
+    // readout of the state it stores (see step_pairs).
+    uint8_t *seg = nullptr;
 };
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 // Whether launch_step would fuse a level's first step with the upsample from

@@ -1304,14 +1304,18 @@ constexpr int k2PairW = kTileW - 2;   // output cells per strip
 
 // UP: step t is a level's first step, fused with the upsample + inject as in
 // nca_step_mfma_2d_rows (src is the next coarser state, width up_cdw, factors
-// up_fy, up_fx; the input channels come from up_img).
-template <typename T, int NIN, class Mlp, bool UP>
+// up_fy, up_fx; the input channels come from up_img).  SEG: the launch also
+// writes the two-class readout of its result (Sec. 3.2) to seg: the lanes of
+// channel quad 3 hold channels 12..15 of their cell, and its byte is 1 iff
+// channel C - 1 > channel C - 2 (ties and NaNs give 0), the readout kernel's
+// rule; the finest level's last launch uses it.
+template <typename T, int NIN, class Mlp, bool UP, bool SEG>
 __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     const T *__restrict__ src, T *__restrict__ dst, int dh, int dw, int strips, int run_rows,
     int items, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
-    const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx) {
+    const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx, uint8_t *__restrict__ seg) {
     static_assert(std::is_same_v<T, float>, "the intermediate ring holds fp32 states");
     using RS = RowStream<T>;
     // Row r of a work item (first input row `base`) lives in slot
@@ -1559,7 +1563,20 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
                 const uint32_t off = x < x_stop ? (uint32_t)x * kCellBytes : kOut;
-                update_store(dst, wr, off, g, f[grp], u, (fw >> (sh + grp * 16 + n)) & 1);
+                if constexpr (SEG) {
+                    const bool fires = (fw >> (sh + grp * 16 + n)) & 1;
+                    const float m = fires ? 1.f : 0.f;
+                    v4f o;
+#pragma unroll
+                    for (int kk = 0; kk < 4; ++kk) o[kk] = fmaf(m, u[kk], f[grp][kk]);
+                    store_quad(dst, wr, off, g, o);
+                    const Rsrc sr = make_rsrc(seg + (int64_t)yc * dw, out_ok ? (uint32_t)dw : 0u);
+                    const uint32_t so = g == 3 && x < x_stop ? (uint32_t)x : kOut;
+                    __builtin_amdgcn_raw_buffer_store_b8((unsigned char)(o[3] > o[2] ? 1 : 0), sr,
+                                                         so, 0, 0);
+                } else {
+                    update_store(dst, wr, off, g, f[grp], u, (fw >> (sh + grp * 16 + n)) & 1);
+                }
             }
         };
 
@@ -2162,10 +2179,12 @@ hipError_t launch_rows_pair(const StepArgs &a, const void *src, void *dst, const
     if (r.items == 0) return hipSuccess;
     if (r.items > INT32_MAX) return hipErrorInvalidValue;
     const int grid = (int)std::min<int64_t>(r.items, r.slots);
-    nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP><<<grid, 64, 0, stream>>>(
+    auto kern = a.seg != nullptr ? nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP, true>
+                                 : nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP, false>;
+    kern<<<grid, 64, 0, stream>>>(
         (const float *)src, (float *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, k2RunRows,
         (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
-        a.seed, a.threshold, (const float *)img, cdw, fy, fx);
+        a.seed, a.threshold, (const float *)img, cdw, fy, fx, a.seg);
     return hipGetLastError();
 }
 

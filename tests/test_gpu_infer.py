@@ -252,3 +252,28 @@ def test_full_size_sampled_boxes(gpu, wl):
                          what=f"{wl.name} box {box}")
     del state, seg
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# readout fused into the finest level's last two-step launch
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kernel", ["mfma_rows", "mfma_rows,mfma_1step", "mfma_tiles"])
+@pytest.mark.parametrize("steps", [(4, 2, 3), (5, 2, 3), (2, 2, 3), (0, 2, 3)],
+                         ids=lambda s: "s" + "-".join(map(str, s)))
+def test_fused_readout_equals_readout_of_final_state(gpu, monkeypatch, kernel, steps):
+    """Where the finest level's last launch runs two steps (with the upsample
+    fused into it or not), that launch writes the readout; it must equal the
+    readout kernel applied to the final state, byte for byte.  Elsewhere the
+    readout kernel runs."""
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
+    wl = Workload(name="fused_readout", ndim=2, extent=(1, 72, 100), n_in=3,
+                  factors=((1, 2, 2), (1, 2, 2)), steps=steps, image_kind="uniform")
+    print(f"fused readout kernel={kernel} steps={steps}", flush=True)
+    state, seg = gpu_infer(wl, make_image(wl), make_weights(wl))
+    model = octnca.Model(ndim=2, n_in=3)
+    want = torch.empty_like(seg)
+    octnca.octree_nca_readout(model, state, want)
+    torch.cuda.synchronize()
+    assert torch.equal(seg, want)
+    np.testing.assert_array_equal(to_np(seg), oracle.readout(to_np(state)))
