@@ -136,8 +136,8 @@ int32_t fused_up_steps(const StepArgs &a, bool fused, int32_t steps) {
 
 // Enqueue steps t0 .. t1-1 of a level; launch k reads bufs[k % 2] and writes
 // bufs[(k + 1) % 2], so the result is in bufs[level_launches(..) % 2].
-// seg_last: when the last launch is a two-step launch, it also writes the
-// readout of its result there (null: no readout).
+// seg_last: the last launch also writes the readout of its result there (null:
+// no readout); the caller passes it only where that launch's kernel can.
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
               const octnca_level_weights *w, int32_t level, int32_t t0, int32_t t1,
               uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0,
@@ -155,7 +155,9 @@ int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
             a.seg = nullptr;
             t += 2;
         } else {
+            a.seg = t + 1 == t1 ? seg_last : nullptr;
             err = launch_step(a, bufs[k], bufs[k ^ 1], stream);
+            a.seg = nullptr;
             t += 1;
         }
         if (err != hipSuccess) return OCTNCA_EHIP;
@@ -425,11 +427,17 @@ int infer_impl(const octnca_model *model, const void *image, octnca_extent fines
         // The finest level's last launch writes the readout too when it is a
         // two-step launch; otherwise the readout kernel runs at the end.
         uint8_t *seg_last = nullptr;
-        if (l == 0 && seg != nullptr && steps[0] >= 2) {
+        if (l == 0 && seg != nullptr) {
             const StepArgs a = step_args(model, p.ext[0], &weights[0], 0, seed, threshold, batch);
             const int32_t first = fused_up_steps(a, fused[0], steps[0]);
-            if (step_pairs(a) && (steps[0] - first) % 2 == 0) seg_last = seg;
-            seg_fused = seg_last != nullptr;
+            const int32_t rest = steps[0] - first;
+            bool ok;
+            if (step_pairs(a))   // the last launch runs two steps
+                ok = rest % 2 == 0 && (rest > 0 || first == 2);
+            else                 // the last launch is a single step after the first
+                ok = rest >= 1 && step_single_fuses_readout(a);
+            if (ok) seg_last = seg;
+            seg_fused = ok;
         }
         int32_t t0 = 0;
         if (fused[l]) {
@@ -833,6 +841,11 @@ hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_
     if (!sel.ok) return hipErrorInvalidValue;
     if (sel.valu) return launch_step_valu(a, src, dst, stream);
     return launch_step_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+}
+
+bool step_single_fuses_readout(const StepArgs &a) {
+    const Selection sel = select_step_kernel();
+    return sel.ok && !sel.valu && step_mfma_single_readout(a, sel.mlp);
 }
 
 bool step_pairs(const StepArgs &a) {

@@ -47,8 +47,9 @@ struct StepArgs {
     int hidden = kH;
     uint64_t seed;
     uint64_t threshold;
-    // Device [cells] uint8 or null: a two-step launch also writes the two-class
-    // readout of the state it stores (see step_pairs).
+    // Device [cells] uint8 or null: a two-step launch, or a single step of the
+    // fp16 3D kernel (see step_single_fuses_readout), also writes the
+    // two-class readout of the state it stores.
     uint8_t *seg = nullptr;
 };
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
@@ -62,6 +63,8 @@ hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipSt
 // Whether launch_step_pair runs steps a.step and a.step + 1 in one launch, and
 // that launch (the state after step a.step is not written to memory).
 bool step_pairs(const StepArgs &a);
+// Whether the single-step launch that launch_step makes for `a` writes StepArgs::seg.
+bool step_single_fuses_readout(const StepArgs &a);
 hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 // The first two steps of a level, the first fused with the upsample (when
 // step_pairs and step_fuses_upsample both hold).
@@ -102,6 +105,8 @@ bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
 // operand policy): step_mfma_pairs says whether that kernel exists for `a`;
 // launch_step2_mfma reads src and writes the state after both steps to dst.
 bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout);
+// Whether a single-step launch of launch_step_mfma for `a` writes StepArgs::seg.
+bool step_mfma_single_readout(const StepArgs &a, MfmaMlp mlp);
 hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                              void *dst, hipStream_t stream);
 // The same two steps with step a.step fused with the upsample + inject from

@@ -1859,14 +1859,17 @@ constexpr int k3hBlocksPerCu = 3;
 // (up_fz, up_fy, up_fx), with the input channels from up_img.
 // (The UP variant runs one step per level and needs more registers for its
 // extra loads: it is built for 2 blocks per CU, the plain one for 3.)
-template <int NIN, bool ALIGNED, bool UP>
+// SEG: the launch also writes the two-class readout of the state it stores
+// (channel C - 1 > channel C - 2 in the stored fp16 values, ties and NaNs 0)
+// to seg; the finest level's last launch uses it.
+template <int NIN, bool ALIGNED, bool UP, bool SEG = false>
 __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mfma_3d_f16(
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
     int tiles_x, int tiles_y, int items, int zrun, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
     uint64_t threshold, const __half *__restrict__ up_img, int up_cdh, int up_cdw, int up_fz,
-    int up_fy, int up_fx) {
+    int up_fy, int up_fx, uint8_t *__restrict__ seg) {
     using Loader = RowLoader<__half, k3TY + 2>;
     __shared__ uint2 ring[3][4 * Loader::PS16];
     __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
@@ -2080,6 +2083,17 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                                 (_Float16)fmaf(one, u[3], (float)s23[1])};
                 const v2u out = {fires ? as_u32(n01) : sp.x, fires ? as_u32(n23) : sp.y};
                 __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
+                if constexpr (SEG) {
+                    // lanes of quad 3: out[1] holds channels 14 (low) and 15 (high)
+                    const h2 c1415 = as_h2(out[1]);
+                    const int x = x0 + (grp & 1) * 16 + n;
+                    const Rsrc sr = make_rsrc(seg + ((int64_t)max(zo, 0) * dh + y0) * dw,
+                                              out_ok ? (uint32_t)min(k3TY, dh - y0) * dw : 0u);
+                    const uint32_t so =
+                        g == 3 && x < dw ? (uint32_t)(2 * wave + (grp >> 1)) * dw + x : kOut;
+                    __builtin_amdgcn_raw_buffer_store_b8(
+                        (unsigned char)((float)c1415[1] > (float)c1415[0] ? 1 : 0), sr, so, 0, 0);
+                }
             }
 
             commit(ring[jp]);
@@ -2242,12 +2256,15 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     if (items > INT32_MAX) return hipErrorInvalidValue;
     if constexpr (kF16) {
         const int grid = (int)std::min<int64_t>(items, slots);
-        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, false>
-                                     : nca_step_mfma_3d_f16<NIN, false, false>;
+        auto kern = a.seg != nullptr
+                        ? (a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, false, true>
+                                            : nca_step_mfma_3d_f16<NIN, false, false, true>)
+                        : (a.ext.w % 8 == 0 ? nca_step_mfma_3d_f16<NIN, true, false>
+                                            : nca_step_mfma_3d_f16<NIN, false, false>);
         kern<<<grid, kThreads, 0, stream>>>(
             (const __half *)src, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
             tiles_y, (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level,
-            a.step, a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1);
+            a.step, a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1, a.seg);
     } else {
         const int grid = (int)std::min<int64_t>(items, slots);
         nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
@@ -2277,7 +2294,7 @@ hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int 
     kern<<<grid, kThreads, 0, stream>>>(
         (const __half *)coarse, (__half *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x,
         tiles_y, (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level,
-        a.step, a.batch, a.seed, a.threshold, (const __half *)img, cdh, cdw, fz, fy, fx);
+        a.step, a.batch, a.seed, a.threshold, (const __half *)img, cdh, cdw, fz, fy, fx, nullptr);
     return hipGetLastError();
 }
 
@@ -2301,6 +2318,11 @@ bool mfma_fits(const StepArgs &a) {
     // more than (2^32 / 18 rows) bytes go to the vector kernel instead.
     const int64_t cell_bytes = (int64_t)kC * (a.dtype == Dtype::F32 ? 4 : 2);
     return (int64_t)(k2TY + 2) * a.ext.w * cell_bytes < (int64_t(1) << 32);
+}
+
+bool step_mfma_single_readout(const StepArgs &a, MfmaMlp mlp) {
+    return a.ndim == 3 && a.dtype == Dtype::F16 && a.channels == kC && a.hidden == kH &&
+           (mlp == MfmaMlp::Default || mlp == MfmaMlp::F16) && mfma_fits(a);
 }
 
 bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {

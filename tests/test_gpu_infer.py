@@ -277,3 +277,20 @@ def test_fused_readout_equals_readout_of_final_state(gpu, monkeypatch, kernel, s
     torch.cuda.synchronize()
     assert torch.equal(seg, want)
     np.testing.assert_array_equal(to_np(seg), oracle.readout(to_np(state)))
+
+
+@pytest.mark.parametrize("steps", [(3, 2), (1, 2), (2, 3)], ids=lambda s: "s" + "-".join(map(str, s)))
+def test_fused_readout_fp16_3d(gpu, monkeypatch, steps):
+    """fp16 3D (2D+t): the finest level's last single-step launch writes the
+    readout (when it is not the level's first, upsample-fused step); it must
+    equal the readout kernel applied to the final state, byte for byte."""
+    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma")
+    wl = Workload(name="fused_readout_f16", ndim=3, extent=(12, 24, 40), n_in=3,
+                  factors=((1, 2, 2),), steps=steps, dtype="f16", image_kind="uniform")
+    print(f"fused readout fp16 3D steps={steps}", flush=True)
+    state, seg = gpu_infer(wl, make_image(wl), make_weights(wl))
+    model = octnca.Model(ndim=3, n_in=3, dtype="f16")
+    want = torch.empty_like(seg)
+    octnca.octree_nca_readout(model, state, want)
+    torch.cuda.synchronize()
+    assert torch.equal(seg, want)
