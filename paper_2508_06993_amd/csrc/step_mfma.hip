@@ -33,6 +33,7 @@
 // reads).  3D: a block owns an 8 x 32 column of the (y, x) plane and a run
 // of z planes, keeping three halo planes in an LDS ring (each plane is read
 // from HBM once per run).
+#include <atomic>
 #include <algorithm>
 #include <type_traits>
 
@@ -2108,18 +2109,20 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     }
 }
 
+// Compute units of the current device, cached per device.  Host threads may
+// call this concurrently: racing first calls store the same value.
 int device_cus() {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int n = 0;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             n <= 0)
             n = 256;
-        cached[dev] = n;
+        cached[dev].store(n, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return n;
 }
 
 constexpr int kBlocksPerCu = 2;
