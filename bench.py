@@ -15,7 +15,10 @@ Prints one JSON line with
   timed with HIP events on the launch stream, against the peak of the
   arithmetic the kernel runs on;
 * cpu_baseline: the CPU oracle timed on a bounded sample of the same workload;
-* peak device memory.
+* peak device memory;
+* under "workloads", the same record (value, ms per pass, roofline, peak
+  memory) for further workloads timed in the same run (default: the one-minute
+  2D+t video, 1800 x 240 x 432 RGB, fp16 states, 5 levels, 16 steps each).
 """
 from __future__ import annotations
 
@@ -74,17 +77,17 @@ def algorithmic_bytes_per_cell_step(wl) -> int:
     return (wl.channels + wl.channels - wl.n_in) * eb
 
 
-def step_kernel_arithmetic(wl):
+def step_kernel_arithmetic(wl, kernel: str):
     """(kernel name, arithmetic of its MLP contraction, that arithmetic's
-    MI355X peak in TFLOP/s) for the step kernel OCTREE_NCA_STEP_KERNEL selects."""
-    sel = os.environ.get("OCTREE_NCA_STEP_KERNEL", "mfma")
-    if sel == "valu":
+    MI355X peak in TFLOP/s) for a step-kernel name of ``Model(kernel=...)``."""
+    names = set(kernel.split(","))
+    if "valu" in names:
         return "nca_step_valu", "fp32 vector FMA", FP32_SCALAR_FMA_PEAK_TFLOPS
-    if sel == "mfma_f32":
+    if "mfma_f32" in names:
         return "nca_step_mfma / fp32 MFMA", "fp32 MFMA", FP32_MFMA_PEAK_TFLOPS
-    if sel == "mfma_f16" or (sel == "mfma" and wl.dtype == "f16"):
+    if "mfma_f16" in names or (wl.dtype == "f16" and "mfma_bf16x3" not in names):
         return "nca_step_mfma / fp16 MFMA", "fp16 MFMA", FP16_MFMA_PEAK_TFLOPS
-    if sel == "mfma_bf16x3":
+    if "mfma_bf16x3" in names:
         return "nca_step_mfma / split-bf16 MFMA", "bf16 MFMA (3 products per fp32 product)", \
             BF16_MFMA_PEAK_TFLOPS
     return "nca_step_mfma / scaled-fp16 MFMA", \
@@ -92,15 +95,37 @@ def step_kernel_arithmetic(wl):
         FP16_MFMA_PEAK_TFLOPS
 
 
+def arithmetic_label(wl, kernel: str) -> str:
+    """What the step computes in, beside the storage type ``dtype``."""
+    names = set(kernel.split(","))
+    store = "fp16 state" if wl.dtype == "f16" else "fp32 state"
+    if "valu" in names:
+        return f"{store}; perception and MLP fp32 FMA on the vector ALUs"
+    if "mfma_f32" in names:
+        return f"{store}; perception fp32 FMA; MLP fp32 MFMA, fp32 accumulate"
+    if "mfma_bf16x3" in names:
+        return f"{store}; perception fp32 FMA; MLP split-bf16 MFMA (3 products), fp32 accumulate"
+    if wl.dtype == "f16":
+        pk = "packed fp16 FMA" if wl.ndim == 3 else "fp32 FMA"
+        return f"{store}; perception {pk}; MLP fp16 MFMA, fp32 accumulate"
+    return (f"{store}; perception fp32 FMA; MLP fp16 MFMA on activations scaled by 2^-8 and "
+            "rounded to fp16 x weights split into fp16 hi + lo, fp32 accumulate")
+
+
 STEP_SOURCES = ("paper_2508_06993_amd/csrc/step_mfma.hip", "paper_2508_06993_amd/csrc/device_common.h")
+HOST_MARKER = "// ==== host side"
 
 
 def step_source_sha256() -> str:
+    """Hash of the step kernels' device code: device_common.h and the part of
+    step_mfma.hip before its host-side launch code."""
     import hashlib
     h = hashlib.sha256()
     for rel in STEP_SOURCES:
         with open(os.path.join(ROOT, rel), "rb") as f:
-            h.update(f.read())
+            text = f.read()
+        cut = text.find(HOST_MARKER.encode())
+        h.update(text if cut < 0 else text[:cut])
     return h.hexdigest()
 
 
@@ -122,18 +147,30 @@ def measured_traffic(wl, selector: str):
     return float(rec["traffic_bytes_per_launch"])
 
 
+def blas_info():
+    """(numpy version, BLAS library and version, BLAS threads) of this process."""
+    import numpy as np
+    libs, threads = [], 1
+    try:
+        from threadpoolctl import threadpool_info
+        for p in threadpool_info():
+            if p.get("user_api") == "blas":
+                libs.append(f"{p.get('internal_api')} {p.get('version')}")
+                threads = max(threads, int(p.get("num_threads", 1)))
+    except Exception:   # pragma: no cover
+        pass
+    return np.__version__, ", ".join(libs) or "unknown", threads
+
+
 def cpu_baseline(wl, seconds_hint=10.0, max_steps=200):
     """Time the CPU oracle on a crop of the finest level (random state, the
-    workload's level-0 weights): consecutive NCA steps until about
-    `seconds_hint` seconds of CPU work (at least 4 steps, at most max_steps)."""
+    workload's level-0 weights): consecutive NCA steps in one process (no
+    band-parallel driver) until about `seconds_hint` seconds of CPU work (at
+    least 4 steps, at most max_steps)."""
     import numpy as np
     import oracle
     from synthetic import make_weights, storage_dtype
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:   # pragma: no cover
-        threads = 1
+    npver, blas, threads = blas_info()
     rng = np.random.default_rng(0)
     if wl.ndim == 2:
         shape = (1, 512, 1024)
@@ -154,7 +191,9 @@ def cpu_baseline(wl, seconds_hint=10.0, max_steps=200):
             "sample": f"{steps} NCA steps of the finest level on a {shape[0]}x{shape[1]}x"
                       f"{shape[2]} crop ({cells * steps} cell-steps, {dt_s:.1f} s), "
                       f"numpy float64 arithmetic, BLAS threads={threads}, "
-                      f"affinity={len(os.sched_getaffinity(0))} cpus"}
+                      f"affinity={len(os.sched_getaffinity(0))} cpus",
+            "numpy": npver, "blas": blas, "blas_threads": int(threads),
+            "affinity_cpus": len(os.sched_getaffinity(0)), "band_parallel": False}
 
 
 def cpu_train_baseline(wl, seconds_hint=10.0):
@@ -164,11 +203,7 @@ def cpu_train_baseline(wl, seconds_hint=10.0):
     import numpy as np
     import oracle
     from synthetic import make_image, make_target, make_weights, scaled
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:   # pragma: no cover
-        threads = 1
+    npver, blas, threads = blas_info()
     small = scaled(wl, (1, 160, 160)) if wl.ndim == 2 else scaled(wl, wl.extent)
     image = make_image(small)
     target = make_target(small, image)
@@ -190,7 +225,9 @@ def cpu_train_baseline(wl, seconds_hint=10.0):
             "sample": f"{runs} training step(s) (forward + backward) of the workload's structure "
                       f"at {small.extent[1]}x{small.extent[2]} ({cs} cell-steps each, "
                       f"{dt_s:.1f} s), numpy float64, BLAS threads={threads}, "
-                      f"affinity={len(os.sched_getaffinity(0))} cpus"}
+                      f"affinity={len(os.sched_getaffinity(0))} cpus",
+            "numpy": npver, "blas": blas, "blas_threads": int(threads),
+            "affinity_cpus": len(os.sched_getaffinity(0)), "band_parallel": False}
 
 
 def train_bench(args):
@@ -290,6 +327,12 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="pathology184mp")
+    ap.add_argument("--extra", default="video2dt",
+                    help="comma-separated further workloads timed in the same run and reported "
+                         "under 'workloads' in the same JSON line ('' for none)")
+    ap.add_argument("--kernel", default="mfma",
+                    help="step kernel, a name accepted by Model(kernel=...), e.g. mfma, "
+                         "mfma_1step, mfma_f32, valu")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--train", action="store_true",
                     help="time the fused training step instead of the inference")
@@ -321,22 +364,42 @@ def main(argv=None):
         print(json.dumps({"copy_probe_bytes": n, "copies": 3}))
         return 0
 
+    from synthetic import WORKLOADS
+    import paper_2508_06993_amd as octnca
+    octnca.lib()   # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    wl = WORKLOADS[args.workload]
+    out = inference_record(wl, args.kernel, args.steps, args.warmup)
+    extras = [w for w in (args.extra.split(",") if args.extra else []) if w and w != wl.name]
+    if extras:
+        out["workloads"] = {}
+        for name in extras:
+            out["workloads"][name] = inference_record(WORKLOADS[name], args.kernel, args.steps,
+                                                      args.warmup, sub=True)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def inference_record(wl, kernel: str, steps: int, warmup: int, sub: bool = False) -> dict:
+    """Time `steps` whole inferences of workload `wl` (after `warmup` untimed
+    ones) with the image resident in HBM; the bench record of that workload."""
+    import gc
+    import torch
     import paper_2508_06993_amd as octnca
     from paper_2508_06993_amd.runtime import Inference, upload_weights, to_device_image
-    from synthetic import WORKLOADS, make_weights
+    from synthetic import make_weights
     from synthetic.cache import cached_image
 
-    wl = WORKLOADS[args.workload]
-    torch.cuda.set_device(0)
-    octnca.lib()   # fail loudly if the HIP library is missing
-    print(f"# workload {wl.name}: extent {wl.extent}, levels {wl.levels}, steps {wl.steps}",
-          file=sys.stderr, flush=True)
-
-    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    print(f"# workload {wl.name}: extent {wl.extent}, levels {wl.levels}, steps {wl.steps}, "
+          f"kernel {kernel}", file=sys.stderr, flush=True)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, kernel=kernel)
     image_np = cached_image(wl)
     image = to_device_image(image_np, model)
     del image_np
     weights = upload_weights(make_weights(wl))
+    torch.cuda.synchronize()
     torch.cuda.reset_peak_memory_stats()
     run = Inference(model, wl.extent, wl.factors)
     stream = torch.cuda.current_stream()
@@ -346,24 +409,24 @@ def main(argv=None):
         run(image, weights, wl.steps, wl.fire_rate, wl.seed,
             level_events=[e.cuda_event for e in events] if events else None, stream=stream)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         one_pass()
     torch.cuda.synchronize()
-    print("# warmup done", file=sys.stderr, flush=True)
+    print(f"# {wl.name}: warmup done", file=sys.stderr, flush=True)
 
     # events: created (first record) before the timed region
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * L)] for _ in range(args.steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * L)] for _ in range(steps)]
     for row in ev:
         for e in row:
             e.record(stream)
     torch.cuda.synchronize()
 
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         one_pass(ev[k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    print("# timed passes done", file=sys.stderr, flush=True)
+    print(f"# {wl.name}: timed passes done", file=sys.stderr, flush=True)
 
     cells = wl.cells_per_level()
     cell_steps = wl.cell_steps()
@@ -374,14 +437,14 @@ def main(argv=None):
                 step_ms += row[2 * l].elapsed_time(row[2 * l + 1])
     # step-kernel launches of a pass as the library enqueues them (a launch
     # runs one step, or two on large 2D fp32 levels)
-    launches = args.steps * sum(octnca.octree_nca_infer_launches(model, wl.extent, wl.factors,
-                                                                 wl.steps))
+    launches = steps * sum(octnca.octree_nca_infer_launches(model, wl.extent, wl.factors,
+                                                            wl.steps))
     avg_launch_ms = step_ms / launches
-    flop = algorithmic_flop_per_cell_step(wl) * cell_steps * args.steps
-    byts = algorithmic_bytes_per_cell_step(wl) * cell_steps * args.steps
+    flop = algorithmic_flop_per_cell_step(wl) * cell_steps * steps
+    byts = algorithmic_bytes_per_cell_step(wl) * cell_steps * steps
     achieved_tflops = flop / (step_ms * 1e-3) / 1e12
     achieved_gbs = byts / (step_ms * 1e-3) / 1e9
-    kname, arith, arith_peak = step_kernel_arithmetic(wl)
+    kname, arith, arith_peak = step_kernel_arithmetic(wl, kernel)
     # binding roof: the larger of the two floors (bytes at HBM peak, FLOPs at
     # the peak of the arithmetic the kernel's contraction runs on)
     t_hbm = byts / (HBM_PEAK_GBS * 1e9)
@@ -398,7 +461,7 @@ def main(argv=None):
         "peak": round(peak, 1),
         "unit": unit,
         "frac": round(achieved / peak, 4),
-        "traffic": measured_traffic(wl, os.environ.get("OCTREE_NCA_STEP_KERNEL", "mfma")),
+        "traffic": measured_traffic(wl, kernel),
         "traffic_unit": "bytes per launch (HBM, profiler counters)",
         "arithmetic": arith,
         "achieved_tflops": round(achieved_tflops, 3),
@@ -412,33 +475,35 @@ def main(argv=None):
         "bytes_per_cell_step": algorithmic_bytes_per_cell_step(wl),
     }
     peak_vram = torch.cuda.max_memory_allocated() / 1e9
-
     out = {
         "metric": "NCA cell-steps/sec",
-        "value": cell_steps * args.steps / wall,
+        "value": cell_steps * steps / wall,
         "unit": "cell-steps/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": wall / args.steps * 1e3,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
+    }
+    if not sub:
+        out.update({"n_gpus": 1, "steps": steps, "warmup": warmup})
+    out.update({
+        "ms_per_step": wall / steps * 1e3,
+    })
+    if not sub:
+        out.update({"higher_is_better": True, "scaling": "weak", "vs_baseline": None})
+    out.update({
         "dtype": "f16" if wl.dtype == "f16" else "f32",
+        "arithmetic": arithmetic_label(wl, kernel),
         "data": "synthetic",
         "config": {"workload": wl.name, "extent_dhw": list(wl.extent), "levels": wl.levels,
                    "steps_per_level": list(wl.steps), "cells_per_level": cells,
                    "cell_steps_per_pass": cell_steps, "channels": wl.channels,
                    "hidden": wl.hidden, "n_in": wl.n_in, "fire_rate": wl.fire_rate,
-                   "parallelism": "single GPU"},
+                   "kernel": kernel, "parallelism": "single GPU"},
         "roofline": roofline,
         "peak_vram_gb": round(peak_vram, 3),
-        "step_kernel_ms_per_pass": round(step_ms / args.steps, 3),
-    }
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl)
-    print(json.dumps(out), flush=True)
-    return 0
+        "step_kernel_ms_per_pass": round(step_ms / steps, 3),
+    })
+    del run, image, weights
+    gc.collect()
+    torch.cuda.empty_cache()
+    return out
 
 
 if __name__ == "__main__":

@@ -62,7 +62,7 @@
 extern "C" {
 #endif
 
-#define OCTNCA_ABI_VERSION 4
+#define OCTNCA_ABI_VERSION 5
 
 typedef enum {
     OCTNCA_OK = 0,
@@ -75,18 +75,52 @@ typedef enum {
 
 typedef enum { OCTNCA_F32 = 0, OCTNCA_F16 = 1 } octnca_dtype;
 
+/* MLP arithmetic of the step kernel (octnca_model.mlp).  The step's
+ * definition (Sec. 3.1) fixes no precision; these are the operand types the
+ * kernels offer, all accumulating in fp32. */
+typedef enum {
+    OCTNCA_MLP_AUTO = 0,   /* OCTNCA_MLP_F16S for fp32 states, OCTNCA_MLP_F16 for fp16 states */
+    OCTNCA_MLP_F32 = 1,    /* matrix cores, fp32 operands */
+    OCTNCA_MLP_BF16X3 = 2, /* matrix cores, operands split into bf16 hi + lo, three products */
+    OCTNCA_MLP_F16 = 3,    /* matrix cores, fp16 operands (fp16 states only) */
+    OCTNCA_MLP_F16S = 4,   /* matrix cores, activations scaled by 2^-8 and rounded to fp16,
+                              weights split into fp16 hi + lo (fp32 states only) */
+    OCTNCA_MLP_VALU = 5    /* no matrix cores: one thread per cell, fp32 FMAs */
+} octnca_mlp;
+
+/* Work layout of the 2D matrix-core step (octnca_model.layout2d); results do
+ * not depend on it.  3D steps ignore it. */
+typedef enum {
+    OCTNCA_LAYOUT_AUTO = 0,  /* row streaming on levels of >= 2048 work items, tiles below */
+    OCTNCA_LAYOUT_ROWS = 1,  /* strips of 32 (30 for two steps) cells streamed over 128-row runs */
+    OCTNCA_LAYOUT_TILES = 2  /* 16 x 32 cell tiles */
+} octnca_layout;
+
 /* Architecture of one NCA (all levels share it; supplement S3 fixes C and H
- * at compile time).  Supported: ndim in {2, 3}, (channels, hidden) in
- * {(16, 64), (12, 48), (20, 100)} (the paper's model and the two other sizes
- * of its ablation, supplement S10), n_in in {1, 3}, state_dtype in
- * {OCTNCA_F32, OCTNCA_F16}.  The matrix-core step kernels serve C = 16,
- * H = 64; the other sizes run on the one-thread-per-cell vector kernel. */
+ * at compile time) and the step kernel that runs it.  Supported: ndim in
+ * {2, 3}, (channels, hidden) in {(16, 64), (12, 48), (20, 100)} (the paper's
+ * model and the two other sizes of its ablation, supplement S10), n_in in
+ * {1, 3}, state_dtype in {OCTNCA_F32, OCTNCA_F16}.
+ * Step kernel: a zero-initialised tail (mlp, layout2d, steps_per_launch all
+ * 0) is the library's default.  The matrix-core kernels serve C = 16,
+ * H = 64; the other sizes run on the one-thread-per-cell vector kernel and
+ * accept only OCTNCA_MLP_AUTO or OCTNCA_MLP_VALU.  Combinations that no
+ * kernel implements (OCTNCA_MLP_F16 with fp32 states, OCTNCA_MLP_F16S with
+ * fp16 states) give OCTNCA_EUNSUPPORTED; values outside the enums give
+ * OCTNCA_EINVAL.  The training entry points always use fp32 MLP operands
+ * and ignore these three fields. */
 typedef struct {
     int32_t ndim;        /* 2: 3x3 taps, d must be 1; 3: 3x3x3 taps */
     int32_t channels;    /* C: state channels per cell */
     int32_t hidden;      /* H: hidden units of the per-cell MLP */
     int32_t n_in;        /* input (image) channels, the first n_in of C */
     int32_t state_dtype; /* storage type of states and images (octnca_dtype) */
+    int32_t mlp;         /* octnca_mlp */
+    int32_t layout2d;    /* octnca_layout */
+    int32_t steps_per_launch; /* 0: two steps per launch on 2D fp32 levels in the row layout
+                                 with the OCTNCA_MLP_F16S arithmetic (the state between the
+                                 two steps stays on chip; same result bit for bit), one
+                                 elsewhere; 1: always one */
 } octnca_model;
 
 typedef struct {
@@ -112,7 +146,7 @@ typedef struct {
  *   finest         extent of level 0.
  *   levels         L >= 1.
  *   factors        host, [(L-1)*3]: (fz, fy, fx) of the transition from level l to
- *                  l+1 at factors[3l .. 3l+2]; each in {1, 2, 3, 4}; ndim 2 needs fz = 1.
+ *                  l+1 at factors[3l .. 3l+2]; each in 1 .. 8; ndim 2 needs fz = 1.
  *   level_images   host array of L-1 device pointers; level_images[l-1] receives
  *                  level l, [d_l][h_l][w_l][n_in] with d_l = d_{l-1} / fz etc.
  * I_l[z,y,x,c] = mean of I_{l-1} over the fz*fy*fx block at (fz*z, fy*y, fx*x),
@@ -138,17 +172,19 @@ int octree_nca_upsample(const octnca_model *model, const void *coarse_state,
 /* Run `steps` NCA steps t = 0 .. steps-1 of one level (Sec. 3.1; supplement
  * S3, Listing 1), out of place, alternating between two buffers: launch k
  * reads bufs[k % 2] and writes bufs[(k+1) % 2].  A launch runs one step, or
- * two (t, t+1) on large 2D fp32 levels, where the state after step t stays
- * on chip; the results are the same.
+ * two (t, t+1) where model->steps_per_launch allows it and the level runs the
+ * 2D fp32 row layout; the state after step t then stays on chip and the
+ * result is the same bit for bit.  The number of two-step launches is kept
+ * even, so the final state is in buf1 exactly when `steps` is odd, whatever
+ * kernels run and on whatever device.
  *   buf0     [extent][C], the level's state on entry.
  *   buf1     [extent][C], scratch of the same size; must not overlap buf0.
  *   weights  host pointer to one octnca_level_weights (device arrays).
  *   level    the level index, used only by the fire mask (0 = finest).
  *   steps    >= 0; 0 leaves buf0 as it is.
  *   fire_rate in [0, 1]; seed: fire-mask key.
- *   result_in_buf1  host, may be NULL: set to the parity of the number of
- *            launches, i.e. 1 when the final state is in buf1, 0 when it is
- *            in buf0 (steps % 2 with one step per launch).
+ *   result_in_buf1  host, may be NULL: set to steps % 2 (1 when the final
+ *            state is in buf1, 0 when it is in buf0).
  * Errors: EINVAL, ESHAPE, EUNSUPPORTED, EHIP. */
 int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1,
                          octnca_extent extent, const octnca_level_weights *weights,
@@ -207,8 +243,9 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
                      void *final_state, uint8_t *seg, void *const *level_events, void *stream);
 
 /* Step-kernel launches that octree_nca_infer enqueues for each level with the
- * step kernel selected at the time of the call (a measurement aid: the
- * launches of a level add up to its steps, one or two steps per launch).
+ * model's step kernel (a measurement aid: the launches of a level add up to
+ * its steps, one or two steps per launch).  The count depends only on the
+ * arguments, not on the device.
  *   launches  host, [L], written: launches[l] for level l (index 0 = finest).
  * Host only: enqueues nothing.  Errors: EINVAL (null pointer, a negative
  * step count), ESHAPE, EUNSUPPORTED. */

@@ -30,12 +30,40 @@ __all__ = [
     "octree_nca_readout_mse", "octree_nca_train_workspace_bytes", "octree_nca_train_step",
     "level_grads_struct", "EXPORTED_SYMBOLS", "OCTNCA_OK", "OCTNCA_EINVAL",
     "OCTNCA_EUNSUPPORTED", "OCTNCA_ESHAPE",
-    "OCTNCA_EHIP", "OCTNCA_ESPACE", "OCTNCA_F32", "OCTNCA_F16",
+    "OCTNCA_EHIP", "OCTNCA_ESPACE", "OCTNCA_F32", "OCTNCA_F16", "KERNEL_NAMES", "kernel_fields",
 ]
 
 OCTNCA_OK, OCTNCA_EINVAL, OCTNCA_EUNSUPPORTED, OCTNCA_ESHAPE, OCTNCA_EHIP, OCTNCA_ESPACE = \
     0, -1, -2, -3, -4, -5
 OCTNCA_F32, OCTNCA_F16 = 0, 1
+(OCTNCA_MLP_AUTO, OCTNCA_MLP_F32, OCTNCA_MLP_BF16X3, OCTNCA_MLP_F16, OCTNCA_MLP_F16S,
+ OCTNCA_MLP_VALU) = range(6)
+OCTNCA_LAYOUT_AUTO, OCTNCA_LAYOUT_ROWS, OCTNCA_LAYOUT_TILES = range(3)
+
+# Step-kernel names accepted by Model(kernel=...): a comma-separated list of
+# these, each setting one field of the C model description (octnca_model).
+KERNEL_NAMES = {
+    "mfma": {},                                   # the library's default
+    "mfma_f32": {"mlp": OCTNCA_MLP_F32},
+    "mfma_bf16x3": {"mlp": OCTNCA_MLP_BF16X3},
+    "mfma_f16": {"mlp": OCTNCA_MLP_F16},
+    "mfma_f16s": {"mlp": OCTNCA_MLP_F16S},
+    "valu": {"mlp": OCTNCA_MLP_VALU},
+    "mfma_rows": {"layout2d": OCTNCA_LAYOUT_ROWS},
+    "mfma_tiles": {"layout2d": OCTNCA_LAYOUT_TILES},
+    "mfma_1step": {"steps_per_launch": 1},
+}
+
+
+def kernel_fields(kernel: str) -> dict:
+    """octnca_model step-kernel fields (mlp, layout2d, steps_per_launch) of a
+    name such as "mfma_rows,mfma_1step"."""
+    out = {"mlp": OCTNCA_MLP_AUTO, "layout2d": OCTNCA_LAYOUT_AUTO, "steps_per_launch": 0}
+    for name in kernel.split(","):
+        if name not in KERNEL_NAMES:
+            raise ValueError(f"unknown step kernel {name!r}; known: {sorted(KERNEL_NAMES)}")
+        out.update(KERNEL_NAMES[name])
+    return out
 
 EXPORTED_SYMBOLS = (
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
@@ -58,7 +86,8 @@ class OctreeNCAError(RuntimeError):
 class _Model(ctypes.Structure):
     _fields_ = [("ndim", ctypes.c_int32), ("channels", ctypes.c_int32),
                 ("hidden", ctypes.c_int32), ("n_in", ctypes.c_int32),
-                ("state_dtype", ctypes.c_int32)]
+                ("state_dtype", ctypes.c_int32), ("mlp", ctypes.c_int32),
+                ("layout2d", ctypes.c_int32), ("steps_per_launch", ctypes.c_int32)]
 
 
 class _Extent(ctypes.Structure):
@@ -162,14 +191,17 @@ class Model:
     dtype: str = "f32"          # storage of states and images: "f32" or "f16"
     channels: int = 16
     hidden: int = 64
+    kernel: str = "mfma"        # step kernel: names of KERNEL_NAMES, comma-separated
 
     @property
     def torch_dtype(self):
         return torch.float16 if self.dtype == "f16" else torch.float32
 
     def struct(self) -> _Model:
+        k = kernel_fields(self.kernel)
         return _Model(self.ndim, self.channels, self.hidden, self.n_in,
-                      OCTNCA_F16 if self.dtype == "f16" else OCTNCA_F32)
+                      OCTNCA_F16 if self.dtype == "f16" else OCTNCA_F32, k["mlp"],
+                      k["layout2d"], k["steps_per_launch"])
 
 
 def _extent(ext: Sequence[int]) -> _Extent:
@@ -258,7 +290,7 @@ def octree_nca_upsample(model: Model, coarse_state: torch.Tensor, factor, fine_i
 
 def octree_nca_run_level(model: Model, buf0, buf1, weights, level: int, steps: int,
                          fire_rate: float, seed: int, stream=None) -> int:
-    """Returns 1 if the final state is in buf1, 0 if in buf0."""
+    """Returns 1 if the final state is in buf1, 0 if in buf0 (steps % 2)."""
     d, h, w = buf0.shape[:3]
     res = _I32(0)
     st = lib().octree_nca_run_level(ctypes.byref(model.struct()),
@@ -299,7 +331,7 @@ def octree_nca_workspace_bytes(model: Model, finest, factors, with_final_state=T
 
 def octree_nca_infer_launches(model: Model, finest, factors, steps) -> list:
     """Step-kernel launches per level (index 0 = finest) that octree_nca_infer
-    enqueues with the step kernel selected now."""
+    enqueues with the model's step kernel."""
     levels = len(factors) + 1
     out = (_I32 * levels)()
     st = lib().octree_nca_infer_launches(ctypes.byref(model.struct()), _extent(finest), levels,

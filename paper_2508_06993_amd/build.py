@@ -5,6 +5,8 @@
 Each .hip file under csrc/ is compiled to an object in parallel, then linked
 into paper_2508_06993_amd/liboctree_nca.so.  The library is replaced
 atomically, so a process that already loaded the old one keeps working.
+Beside it, liboctree_nca.stamp records a hash of the sources, headers and
+flags it was built from; ``is_current()`` compares it with the tree.
 """
 from __future__ import annotations
 
@@ -21,6 +23,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "liboctree_nca.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
+STAMP_PATH = os.path.join(PKG, "liboctree_nca.stamp")
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are disabled for every device pass: only the
@@ -41,6 +44,28 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
+def source_stamp() -> str:
+    """sha256 over the library's sources, headers and build flags."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".h")))
+    files += sorted(os.path.join(INCLUDE, f) for f in os.listdir(INCLUDE) if f.endswith(".h"))
+    for path in files:
+        h.update(os.path.relpath(path, ROOT).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    h.update(" ".join(COMMON_FLAGS + DEVICE_FLAGS).encode())
+    return h.hexdigest()
+
+
+def is_current() -> bool:
+    """Whether the built library exists and was built from the sources as they are now."""
+    if not os.path.exists(LIB_PATH) or not os.path.exists(STAMP_PATH):
+        return False
+    with open(STAMP_PATH) as f:
+        return f.read().strip() == source_stamp()
+
+
 def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -56,6 +81,7 @@ def _run(cmd, verbose):
 def build(verbose: bool = False, jobs: int | None = None) -> str:
     cc = hipcc()
     srcs = sources()
+    stamp = source_stamp()
     tmp = tempfile.mkdtemp(prefix="octnca_build_", dir=PKG)
     try:
         objs = [os.path.join(tmp, os.path.basename(s) + ".o") for s in srcs]
@@ -65,6 +91,9 @@ def build(verbose: bool = False, jobs: int | None = None) -> str:
         out_tmp = os.path.join(tmp, LIB_NAME)
         _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", out_tmp], verbose)
         os.replace(out_tmp, LIB_PATH)
+        with open(STAMP_PATH + ".tmp", "w") as f:
+            f.write(stamp + "\n")
+        os.replace(STAMP_PATH + ".tmp", STAMP_PATH)
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
     return LIB_PATH

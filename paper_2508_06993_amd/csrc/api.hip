@@ -36,7 +36,34 @@ int check_model(const octnca_model *m) {
     if (!size_ok) return OCTNCA_EUNSUPPORTED;
     if (m->n_in != 1 && m->n_in != 3) return OCTNCA_EUNSUPPORTED;
     if (m->state_dtype != OCTNCA_F32 && m->state_dtype != OCTNCA_F16) return OCTNCA_EUNSUPPORTED;
+    // step kernel choice
+    if (m->mlp < OCTNCA_MLP_AUTO || m->mlp > OCTNCA_MLP_VALU) return OCTNCA_EINVAL;
+    if (m->layout2d < OCTNCA_LAYOUT_AUTO || m->layout2d > OCTNCA_LAYOUT_TILES) return OCTNCA_EINVAL;
+    if (m->steps_per_launch != 0 && m->steps_per_launch != 1) return OCTNCA_EINVAL;
+    if (!(m->channels == 16 && m->hidden == 64) && m->mlp != OCTNCA_MLP_AUTO &&
+        m->mlp != OCTNCA_MLP_VALU)
+        return OCTNCA_EUNSUPPORTED;   // only the vector kernel serves the other sizes
+    if (m->mlp == OCTNCA_MLP_F16 && m->state_dtype != OCTNCA_F16) return OCTNCA_EUNSUPPORTED;
+    if (m->mlp == OCTNCA_MLP_F16S && m->state_dtype != OCTNCA_F32) return OCTNCA_EUNSUPPORTED;
     return OCTNCA_OK;
+}
+
+// The caller's step-kernel choice (fields checked by check_model).
+KernelChoice kernel_choice(const octnca_model *m) {
+    KernelChoice k;
+    k.valu = m->mlp == OCTNCA_MLP_VALU;
+    k.pairs = m->steps_per_launch == 0;
+    switch (m->mlp) {
+        case OCTNCA_MLP_F32: k.mlp = MfmaMlp::F32; break;
+        case OCTNCA_MLP_BF16X3: k.mlp = MfmaMlp::Bf16x3; break;
+        case OCTNCA_MLP_F16: k.mlp = MfmaMlp::F16; break;
+        case OCTNCA_MLP_F16S: k.mlp = MfmaMlp::F16S; break;
+        default: k.mlp = MfmaMlp::Default; break;
+    }
+    k.layout = m->layout2d == OCTNCA_LAYOUT_ROWS    ? Layout2d::Rows
+               : m->layout2d == OCTNCA_LAYOUT_TILES ? Layout2d::Tiles
+                                                    : Layout2d::Auto;
+    return k;
 }
 
 int check_extent(const octnca_model *m, const octnca_extent &e) {
@@ -116,6 +143,7 @@ StepArgs step_args(const octnca_model *m, const octnca_extent &e, const octnca_l
     a.threshold = threshold;
     a.channels = m->channels;
     a.hidden = m->hidden;
+    a.kc = kernel_choice(m);
     return a;
 }
 
@@ -138,18 +166,22 @@ int32_t fused_up_steps(const StepArgs &a, bool fused, int32_t steps) {
 // bufs[(k + 1) % 2], so the result is in bufs[level_launches(..) % 2].
 // seg_last: the last launch also writes the readout of its result there (null:
 // no readout); the caller passes it only where that launch's kernel can.
+// max_pairs caps the two-step launches (the remaining steps run one per
+// launch); it is unlimited by default.
 int run_steps(const octnca_model *m, void *b0, void *b1, const octnca_extent &e,
               const octnca_level_weights *w, int32_t level, int32_t t0, int32_t t1,
               uint64_t seed, uint64_t threshold, hipStream_t stream, uint32_t batch = 0,
-              uint8_t *seg_last = nullptr) {
+              uint8_t *seg_last = nullptr, int32_t max_pairs = INT32_MAX) {
     StepArgs a = step_args(m, e, w, level, seed, threshold, batch);
     void *bufs[2] = {b0, b1};
     const bool pairs = step_pairs(a);
     int k = 0;
+    int32_t pairs_left = max_pairs;
     for (int32_t t = t0; t < t1; k ^= 1) {
         a.step = (uint32_t)t;
         hipError_t err;
-        if (pairs && t + 1 < t1) {
+        if (pairs && pairs_left > 0 && t + 1 < t1) {
+            --pairs_left;
             a.seg = t + 2 == t1 ? seg_last : nullptr;
             err = launch_step_pair(a, bufs[k], bufs[k ^ 1], stream);
             a.seg = nullptr;
@@ -269,12 +301,13 @@ int octree_nca_run_level(const octnca_model *model, void *buf0, void *buf1, octn
     const size_t bytes =
         (size_t)(extent.d * extent.h * extent.w) * model->channels * elem_bytes(model);
     if (overlap(buf0, bytes, buf1, bytes)) return OCTNCA_EINVAL;
+    // An even number of two-step launches (the rest one step each) keeps the
+    // number of launches of the same parity as `steps`: the result is in buf1
+    // exactly when steps is odd, whichever kernels run.
     st = run_steps(model, buf0, buf1, extent, weights, level, 0, steps, seed, threshold,
-                   (hipStream_t)stream);
+                   (hipStream_t)stream, 0, nullptr, steps / 4 * 2);
     if (st) return st;
-    if (result_in_buf1)
-        *result_in_buf1 =
-            level_launches(step_args(model, extent, weights, level, seed, threshold, 0), 0, steps) & 1;
+    if (result_in_buf1) *result_in_buf1 = steps & 1;
     return OCTNCA_OK;
 }
 
@@ -788,94 +821,45 @@ int octree_nca_train_step(const octnca_model *model, const void *image, octnca_e
 }  // extern "C"
 
 namespace octnca {
-// Step kernel selection, read at every launch from OCTREE_NCA_STEP_KERNEL:
-//   unset / "mfma"  matrix-core kernel, MLP operands scaled fp16 activations x
-//                   split fp16 weights for fp32 states and fp16 for fp16 states;
-//   "mfma_f16s"     the fp32-state default MLP operands, named;
-//   "mfma_f32"      matrix-core kernel with fp32 MLP operands;
-//   "mfma_bf16x3"   matrix-core kernel with split bf16 operands (any storage);
-//   "mfma_f16"      matrix-core kernel with fp16 operands (fp16 states only);
-//   "mfma_rows", "mfma_tiles"  the default kernel with the 2D work layout
-//                   forced to row streaming or to 16 x 32 tiles;
-//   "mfma_1step"    the default kernel, one step per launch (no two-step
-//                   launches on large 2D fp32 levels);
-//   "valu"          one thread per cell, fp32 FMAs on the vector ALUs;
-// or a comma-separated combination of them (e.g. "mfma_rows,mfma_1step").
-struct Selection {
-    bool ok = true, valu = false, pairs = true;
-    MfmaMlp mlp = MfmaMlp::Default;
-    Layout2d layout = Layout2d::Auto;
-};
-
-Selection select_step_kernel() {
-    Selection r;
-    const char *env = getenv("OCTREE_NCA_STEP_KERNEL");
-    if (env == nullptr) return r;
-    // a comma-separated list of the names above, e.g. "mfma_rows,mfma_1step"
-    const char *p = env;
-    while (true) {
-        const char *e = strchr(p, ',');
-        const size_t len = e ? (size_t)(e - p) : strlen(p);
-        auto is = [&](const char *name) { return strlen(name) == len && strncmp(p, name, len) == 0; };
-        if (len == 0 || is("mfma")) {
-        } else if (is("valu")) r.valu = true;
-        else if (is("mfma_f32")) r.mlp = MfmaMlp::F32;
-        else if (is("mfma_bf16x3")) r.mlp = MfmaMlp::Bf16x3;
-        else if (is("mfma_f16")) r.mlp = MfmaMlp::F16;
-        else if (is("mfma_f16s")) r.mlp = MfmaMlp::F16S;
-        else if (is("mfma_rows")) r.layout = Layout2d::Rows;
-        else if (is("mfma_tiles")) r.layout = Layout2d::Tiles;
-        else if (is("mfma_1step")) r.pairs = false;
-        else r.ok = false;
-        if (e == nullptr) break;
-        p = e + 1;
-    }
-    return r;
-}
-
+// The step kernel comes with the arguments (StepArgs::kc, filled from the
+// caller's octnca_model); nothing here reads the environment.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
     // the matrix-core kernels are built for C = 16, H = 64; the other model
     // sizes always run on the vector kernel
-    if (a.channels != kC || a.hidden != kH) return launch_step_valu(a, src, dst, stream);
-    const Selection sel = select_step_kernel();
-    if (!sel.ok) return hipErrorInvalidValue;
-    if (sel.valu) return launch_step_valu(a, src, dst, stream);
-    return launch_step_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+    if (a.channels != kC || a.hidden != kH || a.kc.valu)
+        return launch_step_valu(a, src, dst, stream);
+    return launch_step_mfma(a, a.kc.mlp, a.kc.layout, src, dst, stream);
 }
 
 bool step_single_fuses_readout(const StepArgs &a) {
-    const Selection sel = select_step_kernel();
-    return sel.ok && !sel.valu && step_mfma_single_readout(a, sel.mlp);
+    return !a.kc.valu && step_mfma_single_readout(a, a.kc.mlp);
 }
 
 bool step_pairs(const StepArgs &a) {
-    const Selection sel = select_step_kernel();
-    return sel.ok && !sel.valu && sel.pairs && step_mfma_pairs(a, sel.mlp, sel.layout);
+    return !a.kc.valu && a.kc.pairs && step_mfma_pairs(a, a.kc.mlp, a.kc.layout);
 }
 
 hipError_t launch_step_pair(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
-    const Selection sel = select_step_kernel();
-    return launch_step2_mfma(a, sel.mlp, sel.layout, src, dst, stream);
+    if (!step_pairs(a)) return hipErrorInvalidValue;
+    return launch_step2_mfma(a, a.kc.mlp, a.kc.layout, src, dst, stream);
 }
 
 hipError_t launch_step_pair_up(const StepArgs &a, const void *coarse, int coarse_w, int fz,
                                int fy, int fx, const void *img, void *dst, hipStream_t stream) {
-    if (fz != 1 || !step_fuses_upsample(a)) return hipErrorInvalidValue;
-    const Selection sel = select_step_kernel();
-    return launch_step2_mfma_up(a, sel.mlp, sel.layout, coarse, coarse_w, fy, fx, img, dst,
+    if (fz != 1 || !step_pairs(a) || !step_fuses_upsample(a)) return hipErrorInvalidValue;
+    return launch_step2_mfma_up(a, a.kc.mlp, a.kc.layout, coarse, coarse_w, fy, fx, img, dst,
                                 stream);
 }
 
 bool step_fuses_upsample(const StepArgs &a) {
-    const Selection sel = select_step_kernel();
-    return sel.ok && !sel.valu && step_mfma_fuses_upsample(a, sel.mlp, sel.layout);
+    return !a.kc.valu && step_mfma_fuses_upsample(a, a.kc.mlp, a.kc.layout);
 }
 
 hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, int coarse_w,
                           int fz, int fy, int fx, const void *img, void *dst,
                           hipStream_t stream) {
-    const Selection sel = select_step_kernel();
-    return launch_step_mfma_up(a, sel.layout, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
+    if (!step_fuses_upsample(a)) return hipErrorInvalidValue;
+    return launch_step_mfma_up(a, a.kc.layout, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
                                stream);
 }
 }  // namespace octnca

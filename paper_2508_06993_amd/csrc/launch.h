@@ -33,6 +33,23 @@ hipError_t launch_readout_classes(Dtype dt, const void *state, int64_t cells, in
 hipError_t launch_fire_mask(uint64_t seed, uint32_t level, uint32_t step, int64_t cells,
                             uint64_t threshold, uint8_t *mask, hipStream_t stream);
 
+// MLP operand precision of the MFMA step kernel.  Default: scaled fp16
+// activations with split fp16 weights (F16S) for fp32 states, fp16 for fp16 states.
+enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3, F16S = 4 };
+// Work layout of the 2D MFMA step.  Auto: row streaming on large levels,
+// 16 x 32 tiles on small ones; Rows / Tiles force one (3D steps ignore it).
+enum class Layout2d : int { Auto = 0, Rows = 1, Tiles = 2 };
+// Step kernel chosen by the caller (the model description of the C ABI):
+// vector kernel or matrix cores, MLP operands, 2D work layout, and whether
+// two steps may run in one launch.  The default-constructed value is the
+// library's default.
+struct KernelChoice {
+    bool valu = false;    // one thread per cell on the vector ALUs
+    bool pairs = true;    // two steps per launch where the two-step kernel applies
+    MfmaMlp mlp = MfmaMlp::Default;
+    Layout2d layout = Layout2d::Auto;
+};
+
 // One NCA step src -> dst over a level of extent `ext`.
 struct StepArgs {
     Dtype dtype;
@@ -51,6 +68,7 @@ struct StepArgs {
     // fp16 3D kernel (see step_single_fuses_readout), also writes the
     // two-class readout of the state it stores.
     uint8_t *seg = nullptr;
+    KernelChoice kc;      // step kernel of the matrix-core / vector paths
 };
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 // Whether launch_step would fuse a level's first step with the upsample from
@@ -86,12 +104,6 @@ size_t mse_workspace_doubles(int64_t cells);
 hipError_t launch_readout_mse(const float *state, const float *target, int64_t cells, int channels,
                               float *grad, double *loss, double *ws, hipStream_t stream);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t stream);
-// MLP operand precision of the MFMA step kernel.  Default: scaled fp16
-// activations with split fp16 weights (F16S) for fp32 states, fp16 for fp16 states.
-enum class MfmaMlp : int { Default = 0, F32 = 1, Bf16x3 = 2, F16 = 3, F16S = 4 };
-// Work layout of the 2D MFMA step.  Auto: row streaming on large levels,
-// 16 x 32 tiles on small ones; Rows / Tiles force one (3D steps ignore it).
-enum class Layout2d : int { Auto = 0, Rows = 1, Tiles = 2 };
 hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                             void *dst, hipStream_t stream);
 // The first step of a level fused with the upsample + inject from the next

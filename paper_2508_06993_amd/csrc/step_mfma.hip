@@ -2109,6 +2109,8 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     }
 }
 
+// ==== host side: launch plans and dispatch ====
+
 // Compute units of the current device, cached per device.  Host threads may
 // call this concurrently: racing first calls store the same value.
 int device_cus() {
@@ -2129,11 +2131,16 @@ constexpr int kBlocksPerCu = 2;
 
 // Work layout of a 2D level.  Large levels: row streaming over strips of 32
 // cells and runs of k2RunRows rows, once there is at least one run per wave
-// slot.  Small levels: 16 x 32 tiles, where the per-run start-up of the row
-// kernel (two rows loaded and waited for) would not be amortised.
+// slot of a full MI355X (256 CUs x 4 SIMDs x 2 waves).  Small levels: 16 x 32
+// tiles, where the per-run start-up of the row kernel (two rows loaded and
+// waited for) would not be amortised.  The choice uses that fixed slot count,
+// not the device's, so the launch sequence (and with it the buffer that holds
+// a result) is the same on every device; only grid sizes follow the device.
+constexpr int64_t kPlanSlots = 256 * 4 * k2WavesPerSimd;
+
 struct RowsPlan {
     int tiles_x;
-    int64_t runs, items, slots;
+    int64_t runs, items, slots;   // slots: wave slots of this device (grid size)
 };
 
 RowsPlan rows_plan(const StepArgs &a) {
@@ -2147,7 +2154,7 @@ RowsPlan rows_plan(const StepArgs &a) {
 
 bool uses_rows(const StepArgs &a, Layout2d layout) {
     return layout == Layout2d::Rows ||
-           (layout == Layout2d::Auto && rows_plan(a).items >= rows_plan(a).slots);
+           (layout == Layout2d::Auto && rows_plan(a).items >= kPlanSlots);
 }
 
 // Row kernel launch; UP: the first step of a level fused with the upsample
@@ -2184,7 +2191,7 @@ bool uses_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
            a.ext.h * a.ext.w < (int64_t(1) << 32) &&   // 32-bit cell indices in the kernel
            (mlp == MfmaMlp::Default || mlp == MfmaMlp::F16S) &&
            (layout == Layout2d::Rows ||
-            (layout == Layout2d::Auto && pair_plan(a).items >= pair_plan(a).slots));
+            (layout == Layout2d::Auto && pair_plan(a).items >= kPlanSlots));
 }
 
 // UP: src is the coarse state (width cdw) upsampled by (fy, fx), img the

@@ -16,9 +16,10 @@ def pytest_configure(config):
 
 
 def _ensure_library():
-    """Load what is built; build only when no library exists yet."""
-    from paper_2508_06993_amd.build import LIB_PATH, build
-    if not os.path.exists(LIB_PATH):
+    """The built library, rebuilt first when it is missing or was built from
+    other sources than the tree's (its stamp differs)."""
+    from paper_2508_06993_amd.build import LIB_PATH, build, is_current
+    if not is_current():
         build()
     return LIB_PATH
 
@@ -30,8 +31,9 @@ def library_path():
 
 @pytest.fixture(scope="session")
 def gpu():
-    """The GPU tests' device.  No GPU (or no library) is an error, not a skip,
-    on a machine that runs them: the HIP path must be the one that runs."""
+    """The GPU tests' device.  Where no GPU is visible (a CPU-only machine)
+    the GPU tests are skipped; where one is, the library must build and load:
+    a failure there is an error, and there is no CPU fallback to pass on."""
     import torch
     if not torch.cuda.is_available():
         pytest.skip("no GPU in this environment")
@@ -46,14 +48,13 @@ STEP_KERNELS = ("mfma", "mfma_rows", "mfma_tiles", "mfma_f32", "mfma_bf16x3", "v
 
 
 @pytest.fixture(params=STEP_KERNELS)
-def step_kernel(request, monkeypatch):
-    """Run a test once per fused-step kernel (the library reads
-    OCTREE_NCA_STEP_KERNEL at every launch).  "mfma" is the default kernel:
-    scaled fp16 activations with split fp16 weights for fp32 states, fp16
-    operands for fp16 states, and for 2D the work layout chosen by level
-    size; "mfma_rows" and "mfma_tiles" force the 2D layout (row streaming,
-    16 x 32 tiles) so both are covered at test sizes; "mfma_f32" uses fp32 MLP
-    operands, "mfma_bf16x3" split-bf16 ones; "valu" is the one-thread-per-cell
-    vector kernel."""
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", request.param)
+def step_kernel(request):
+    """Run a test once per fused-step kernel; the test passes the name to
+    ``Model(kernel=...)``, which sets the step-kernel fields of the C model
+    description.  "mfma" is the default kernel: scaled fp16 activations with
+    split fp16 weights for fp32 states, fp16 operands for fp16 states, and for
+    2D the work layout chosen by level size; "mfma_rows" and "mfma_tiles"
+    force the 2D layout (row streaming, 16 x 32 tiles) so both are covered at
+    test sizes; "mfma_f32" uses fp32 MLP operands, "mfma_bf16x3" split-bf16
+    ones; "valu" is the one-thread-per-cell vector kernel."""
     return request.param

@@ -55,7 +55,7 @@ def test_library_exports_every_declared_symbol(lib, library_path):
 
 def test_version_and_strerror(lib):
     declared = int(re.search(r"#define OCTNCA_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
-    assert lib.octree_nca_abi_version() == declared == 4
+    assert lib.octree_nca_abi_version() == declared == 5
     for st in (0, -1, -2, -3, -4, -5):
         assert lib.octree_nca_strerror(st).decode() not in ("", "unknown status")
     assert lib.octree_nca_strerror(17).decode() == "unknown status"
@@ -345,25 +345,75 @@ def test_train_workspace_and_step_validation(lib):
                                      FAKE2, big, n, gs, None, None, None) == EINVAL
 
 
-def test_infer_launches_counts_two_step_launches(monkeypatch):
+def test_infer_launches_counts_two_step_launches():
     """Host query of the launches octree_nca_infer enqueues: on the 184.5 MP
     pyramid the three large levels run their 20 steps in 10 two-step launches,
     the first fused with the upsample; an odd count adds one single step; the
     smaller levels and the one-step selection run one launch per step."""
     m = octnca.Model(ndim=2, n_in=3)
     f = [(1, 2, 2)] * 5
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma")
     assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == \
         [10, 10, 10, 20, 20, 20]
     assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [19, 1, 2, 20, 20, 20]) == \
         [10, 1, 1, 20, 20, 20]
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_1step")
-    assert octnca.octree_nca_infer_launches(m, (1, 11264, 16384), f, [20] * 6) == [20] * 6
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
-    assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 0]) == \
+    one = octnca.Model(ndim=2, n_in=3, kernel="mfma_1step")
+    assert octnca.octree_nca_infer_launches(one, (1, 11264, 16384), f, [20] * 6) == [20] * 6
+    rows = octnca.Model(ndim=2, n_in=3, kernel="mfma_rows")
+    assert octnca.octree_nca_infer_launches(rows, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 0]) == \
         [3, 2, 0]
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "valu")
-    assert octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 3]) == \
+    valu = octnca.Model(ndim=2, n_in=3, kernel="valu")
+    assert octnca.octree_nca_infer_launches(valu, (1, 64, 64), [(1, 2, 2)] * 2, [5, 4, 3]) == \
         [5, 4, 3]
+    # the plan is a function of the arguments: the level of 2048 two-step work
+    # items (1920 = 64 strips of 30 cells, 4096 rows = 32 runs of 128) pairs,
+    # one of 1984 items does not, on any device
+    assert octnca.octree_nca_infer_launches(m, (1, 4096, 1920), [], [20]) == [10]
+    assert octnca.octree_nca_infer_launches(m, (1, 3968, 1920), [], [20]) == [20]
     with pytest.raises(octnca.OctreeNCAError):
         octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, -1, 3])
+
+
+def test_model_kernel_fields_are_checked(lib):
+    """The step-kernel fields of octnca_model: values outside their enums are
+    EINVAL, combinations no kernel implements EUNSUPPORTED; checked before
+    anything else, with no launch."""
+    def m(mlp=0, layout=0, spl=0, c=16, h=64, dt=0):
+        return ctypes.byref(_Model(2, c, h, 3, dt, mlp, layout, spl))
+    steps = (ctypes.c_int32 * 1)(3)
+    out = (ctypes.c_int32 * 1)()
+    f = (ctypes.c_int32 * 3)(1, 1, 1)
+    call = lambda mm: lib.octree_nca_infer_launches(mm, _Extent(1, 8, 8), 1, f, steps, out)
+    assert call(m()) == 0 and out[0] == 3                      # host-only query
+    for bad in (m(mlp=6), m(mlp=-1), m(layout=3), m(spl=2), m(spl=-1)):
+        assert call(bad) == EINVAL
+    assert call(m(mlp=octnca.OCTNCA_MLP_F16)) == EUNSUP             # fp16 operands, fp32 states
+    assert call(m(mlp=octnca.OCTNCA_MLP_F16S, dt=1)) == EUNSUP      # split operands, fp16 states
+    assert call(m(mlp=octnca.OCTNCA_MLP_F32, c=12, h=48)) == EUNSUP # MFMA only for 16 / 64
+    assert call(m(mlp=octnca.OCTNCA_MLP_VALU, c=12, h=48)) == 0     # vector kernel: accepted
+    for name in octnca.KERNEL_NAMES:
+        octnca.kernel_fields(name)
+    assert octnca.kernel_fields("mfma_rows,mfma_1step") == {
+        "mlp": 0, "layout2d": octnca.OCTNCA_LAYOUT_ROWS, "steps_per_launch": 1}
+    with pytest.raises(ValueError):
+        octnca.kernel_fields("mfma_fast")
+
+
+def test_run_level_result_parity_is_steps_mod_2(lib):
+    """run_level reports where its result is without a device: validation of
+    every argument happens first, so an invalid call leaves the flag alone; the
+    documented rule is steps % 2 for every kernel (checked on the GPU)."""
+    res = ctypes.c_int32(7)
+    ext = _Extent(1, 8, 8)
+    assert lib.octree_nca_run_level(model(), FAKE, FAKE2, ext, weights(), 0, -1, 0.5, 0,
+                                    ctypes.byref(res), None) == EINVAL
+    assert res.value == 7
+
+
+def test_build_stamp_tracks_sources(library_path, monkeypatch):
+    """The library carries a stamp of the sources, headers and flags it was
+    built from; the test session rebuilds whenever the stamp differs."""
+    from paper_2508_06993_amd import build as b
+    assert b.is_current()
+    assert b.source_stamp() == b.source_stamp()
+    monkeypatch.setattr(b, "COMMON_FLAGS", b.COMMON_FLAGS + ["-DSTAMP_PROBE"])
+    assert not b.is_current()

@@ -26,9 +26,9 @@ from parity import assert_seg_close, assert_state_close, to_np
 pytestmark = pytest.mark.gpu
 
 
-def gpu_infer(wl, image, weights, want_state=True):
+def gpu_infer(wl, image, weights, want_state=True, kernel="mfma"):
     model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, channels=wl.channels,
-                         hidden=wl.hidden)
+                         hidden=wl.hidden, kernel=kernel)
     run = Inference(model, wl.extent, wl.factors, want_state=want_state)
     state, seg = run(to_device_image(image, model), upload_weights(weights), wl.steps,
                      wl.fire_rate, wl.seed)
@@ -69,7 +69,7 @@ SMALL = [
 def test_infer_matches_oracle(gpu, step_kernel, wl):
     image = make_image(wl)
     weights = make_weights(wl)
-    state, seg = gpu_infer(wl, image, weights)
+    state, seg = gpu_infer(wl, image, weights, kernel=step_kernel)
     want_state, want_seg = oracle_infer(wl, image, weights)
     got = to_np(state)
     assert got.dtype == storage_dtype(wl)
@@ -88,7 +88,7 @@ def test_infer_batch_matches_oracle(gpu, step_kernel, wl):
     against the oracle with that batch index; image 0 bit for bit equal to a
     single-image inference."""
     batch = 3
-    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, kernel=step_kernel)
     rng = np.random.default_rng(21)
     images = np.stack([make_image(wl)] + [rng.uniform(0, 1, make_image(wl).shape)
                                           .astype(storage_dtype(wl)) for _ in range(batch - 1)])
@@ -111,7 +111,7 @@ def test_infer_batch_matches_oracle(gpu, step_kernel, wl):
         np.testing.assert_array_equal(got_states[b][..., :wl.n_in], images[b])
         assert_state_close(got_states[b], want_state, wl.dtype)
         assert_seg_close(got_segs[b], want_seg, want_state, wl.dtype)
-    single_state, single_seg = gpu_infer(wl, images[0], weights)
+    single_state, single_seg = gpu_infer(wl, images[0], weights, kernel=step_kernel)
     np.testing.assert_array_equal(got_states[0], to_np(single_state))
     np.testing.assert_array_equal(got_segs[0], to_np(single_seg))
     # image 1's masks differ from image 0's: same image, other batch index
@@ -144,17 +144,16 @@ FUSION_CASES = [scaled(TINY_2D, (1, 64, 96), steps=(3, 2, 4)),
 
 
 @pytest.mark.parametrize("wl", FUSION_CASES, ids=lambda w: w.name)
-def test_fused_first_step_equals_separate_upsample(gpu, monkeypatch, wl):
+def test_fused_first_step_equals_separate_upsample(gpu, wl):
     """octree_nca_infer fuses each level's first step with the upsample +
     inject where the level runs the 2D row-streaming kernel (forced here) or
     the fp16 3D kernel.  The same pipeline built from the separate entry points
     (pyramid, upsample, run_level: the same kernels without fusion) must give
     the same bits."""
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_rows")
-    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, kernel="mfma_rows")
     image = make_image(wl)
     weights = make_weights(wl)
-    fused_state, fused_seg = gpu_infer(wl, image, weights)
+    fused_state, fused_seg = gpu_infer(wl, image, weights, kernel="mfma_rows")
 
     levels = len(wl.steps)
     dev_img = to_device_image(image, model)
@@ -261,16 +260,15 @@ def test_full_size_sampled_boxes(gpu, wl):
 @pytest.mark.parametrize("kernel", ["mfma_rows", "mfma_rows,mfma_1step", "mfma_tiles"])
 @pytest.mark.parametrize("steps", [(4, 2, 3), (5, 2, 3), (2, 2, 3), (0, 2, 3)],
                          ids=lambda s: "s" + "-".join(map(str, s)))
-def test_fused_readout_equals_readout_of_final_state(gpu, monkeypatch, kernel, steps):
+def test_fused_readout_equals_readout_of_final_state(gpu, kernel, steps):
     """Where the finest level's last launch runs two steps (with the upsample
     fused into it or not), that launch writes the readout; it must equal the
     readout kernel applied to the final state, byte for byte.  Elsewhere the
     readout kernel runs."""
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
     wl = Workload(name="fused_readout", ndim=2, extent=(1, 72, 100), n_in=3,
                   factors=((1, 2, 2), (1, 2, 2)), steps=steps, image_kind="uniform")
     print(f"fused readout kernel={kernel} steps={steps}", flush=True)
-    state, seg = gpu_infer(wl, make_image(wl), make_weights(wl))
+    state, seg = gpu_infer(wl, make_image(wl), make_weights(wl), kernel=kernel)
     model = octnca.Model(ndim=2, n_in=3)
     want = torch.empty_like(seg)
     octnca.octree_nca_readout(model, state, want)
@@ -280,11 +278,10 @@ def test_fused_readout_equals_readout_of_final_state(gpu, monkeypatch, kernel, s
 
 
 @pytest.mark.parametrize("steps", [(3, 2), (1, 2), (2, 3)], ids=lambda s: "s" + "-".join(map(str, s)))
-def test_fused_readout_fp16_3d(gpu, monkeypatch, steps):
+def test_fused_readout_fp16_3d(gpu, steps):
     """fp16 3D (2D+t): the finest level's last single-step launch writes the
     readout (when it is not the level's first, upsample-fused step); it must
     equal the readout kernel applied to the final state, byte for byte."""
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma")
     wl = Workload(name="fused_readout_f16", ndim=3, extent=(12, 24, 40), n_in=3,
                   factors=((1, 2, 2),), steps=steps, dtype="f16", image_kind="uniform")
     print(f"fused readout fp16 3D steps={steps}", flush=True)

@@ -229,7 +229,8 @@ def test_one_step_matches_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     rng = np.random.default_rng(11)
     w = rand_weights(rng, ndim)
     s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
-    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt), s, w, 2, 1, 0.5, 42)
+    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, kernel=step_kernel),
+                               s, w, 2, 1, 0.5, 42)
     assert which == 1
     want = oracle.nca_step(s, w, n_in, ndim, 2, 0, 42, 0.5, NP_DT[dt])
     tol = STEP_TOL[(dt, step_kernel)][0]
@@ -252,8 +253,8 @@ def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     w = rand_weights(rng, ndim)
     s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
     steps = 9
-    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt), s, w, 1, steps,
-                               0.5, 3)
+    got, which = run_level_gpu(octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, kernel=step_kernel),
+                               s, w, 1, steps, 0.5, 3)
     assert which == steps % 2
     want = oracle.run_level(s, w, n_in, ndim, 1, steps, 3, 0.5, NP_DT[dt])
     tol = STEP_TOL[(dt, step_kernel)][1]
@@ -297,7 +298,7 @@ def test_fire_rate_zero_and_zero_w2_are_identity(gpu, step_kernel, ndim):
     shape = (1, 23, 41) if ndim == 2 else (5, 10, 12)
     s = rng.normal(0, 1, shape + (C,)).astype(np.float32)
     w = rand_weights(rng, ndim)
-    m = octnca.Model(ndim=ndim, n_in=3)
+    m = octnca.Model(ndim=ndim, n_in=3, kernel=step_kernel)
     got, _ = run_level_gpu(m, s, w, 0, 3, 0.0, 5)
     np.testing.assert_array_equal(got, s)
     w.w2[:] = 0
@@ -310,7 +311,7 @@ def test_translation_equivariance_on_gpu(gpu, step_kernel):
     enough from the border)."""
     rng = np.random.default_rng(4)
     w = rand_weights(rng, 2)
-    m = octnca.Model(ndim=2, n_in=3)
+    m = octnca.Model(ndim=2, n_in=3, kernel=step_kernel)
     base = rng.normal(0, 1, (1, 48, 64, C)).astype(np.float32)
     shifted = np.roll(base, (5, 9), axis=(1, 2))
     a, _ = run_level_gpu(m, base, w, 0, 4, 1.0, 0)
@@ -324,18 +325,18 @@ def test_step_is_deterministic(gpu, step_kernel):
     rng = np.random.default_rng(6)
     w = rand_weights(rng, 3)
     s = rng.normal(0, 1, (9, 17, 19, C)).astype(np.float32)
-    m = octnca.Model(ndim=3, n_in=1)
+    m = octnca.Model(ndim=3, n_in=1, kernel=step_kernel)
     a, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
     b, _ = run_level_gpu(m, s, w, 0, 5, 0.5, 1)
     np.testing.assert_array_equal(a, b)
 
 
-def test_split_bf16_kernel_on_fp16_states(gpu, monkeypatch):
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_bf16x3")
+def test_split_bf16_kernel_on_fp16_states(gpu):
     rng = np.random.default_rng(13)
     w = rand_weights(rng, 3)
     s = rng.normal(0, 1, (6, 11, 35, C)).astype(np.float16)
-    got, _ = run_level_gpu(octnca.Model(ndim=3, n_in=3, dtype="f16"), s, w, 0, 4, 0.5, 8)
+    got, _ = run_level_gpu(octnca.Model(ndim=3, n_in=3, dtype="f16", kernel="mfma_bf16x3"), s, w,
+                           0, 4, 0.5, 8)
     want = oracle.run_level(s, w, 3, 3, 0, 4, 8, 0.5, np.float16)
     assert max_rel_err(got, want) <= 5e-3
 
@@ -356,13 +357,13 @@ def test_scaled_fp16_mlp_keeps_large_fp32_states_in_range(gpu):
         assert max_rel_err(got, want) <= STEP_TOL[("f32", "mfma")][0]
 
 
-def test_fp16_operands_refused_for_fp32_states(gpu, monkeypatch):
-    """fp16 MLP operands are not offered for fp32 states: the launch is
+def test_fp16_operands_refused_for_fp32_states(gpu):
+    """fp16 MLP operands are not offered for fp32 states: the call is
     refused before anything is enqueued."""
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", "mfma_f16")
     s = np.zeros((1, 8, 8, C), np.float32)
     b0 = dev(s)
     b1 = torch.empty_like(b0)
     w = upload_weights([rand_weights(np.random.default_rng(0), 2)])[0]
     with pytest.raises(octnca.OctreeNCAError):
-        octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=3), b0, b1, w, 0, 1, 0.5, 0)
+        octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=3, kernel="mfma_f16"), b0, b1, w,
+                                    0, 1, 0.5, 0)

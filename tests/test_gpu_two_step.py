@@ -32,11 +32,12 @@ def rand_weights(rng, scale=0.3):
         w2=rng.normal(0, scale, (C, H)).astype(np.float32))
 
 
-def run(monkeypatch, kernel, state, w, n_in, steps, rate, level=1, seed=5):
-    monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
+def run(kernel, state, w, n_in, steps, rate, level=1, seed=5):
+    """run_level with the given step kernel; its result is in buf1 exactly
+    when steps is odd (it runs an even number of two-step launches)."""
     b0 = state.clone()
     b1 = torch.full_like(b0, float("nan"))
-    which = octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=n_in), b0, b1,
+    which = octnca.octree_nca_run_level(octnca.Model(ndim=2, n_in=n_in, kernel=kernel), b0, b1,
                                         upload_weights([w])[0], level, steps, rate, seed)
     torch.cuda.synchronize()
     return (b1 if which else b0), which
@@ -48,43 +49,47 @@ SHAPES = [(1, 1, 1), (1, 2, 29), (1, 3, 30), (1, 5, 31), (1, 9, 59), (1, 33, 61)
 
 @pytest.mark.parametrize("shape", SHAPES, ids=lambda s: f"{s[1]}x{s[2]}")
 @pytest.mark.parametrize("n_in", [1, 3])
-def test_two_step_launches_equal_single_steps(gpu, monkeypatch, shape, n_in):
+def test_two_step_launches_equal_single_steps(gpu, shape, n_in):
     rng = np.random.default_rng(hash((shape, n_in)) % 2**32)
     w = rand_weights(rng)
     s = torch.from_numpy(rng.normal(0, 1, shape + (C,)).astype(np.float32)).cuda()
-    for steps in (1, 2, 5):
+    # 4 steps: two two-step launches; 5: two and one single; 7: two and three
+    for steps in (1, 4, 5, 7):
         print(f"two-step shape={shape} n_in={n_in} steps={steps}", flush=True)
-        got, which = run(monkeypatch, "mfma_rows", s, w, n_in, steps, 0.5)
-        want, which1 = run(monkeypatch, "mfma_rows,mfma_1step", s, w, n_in, steps, 0.5)
+        got, which = run("mfma_rows", s, w, n_in, steps, 0.5)
+        want, which1 = run("mfma_rows,mfma_1step", s, w, n_in, steps, 0.5)
         assert which1 == steps % 2
-        assert which == ((steps + 1) // 2) % 2
+        assert which == steps % 2
         assert torch.equal(got, want), (shape, n_in, steps)
         # the input channels are never written
         assert torch.equal(got[..., :n_in], s[..., :n_in])
 
 
 @pytest.mark.parametrize("rate", [0.0, 1.0])
-def test_two_step_fire_rate_extremes(gpu, monkeypatch, rate):
+def test_two_step_fire_rate_extremes(gpu, rate):
     rng = np.random.default_rng(7)
     w = rand_weights(rng)
     s = torch.from_numpy(rng.normal(0, 1, (1, 70, 97, C)).astype(np.float32)).cuda()
-    got, _ = run(monkeypatch, "mfma_rows", s, w, 3, 4, rate)
-    want, _ = run(monkeypatch, "mfma_rows,mfma_1step", s, w, 3, 4, rate)
+    got, _ = run("mfma_rows", s, w, 3, 4, rate)
+    want, _ = run("mfma_rows,mfma_1step", s, w, 3, 4, rate)
     assert torch.equal(got, want)
     if rate == 0.0:
         assert torch.equal(got, s)
 
 
-def test_two_step_default_on_a_large_level(gpu, monkeypatch):
+def test_two_step_default_on_a_large_level(gpu):
     """A level large enough for the default layout to pick the row kernel (and
-    with it the two-step launches): 4096 x 1920 cells, strips x runs = 2048."""
+    with it the two-step launches): 4096 x 1920 cells, strips x runs = 2048.
+    Four steps run as two two-step launches, against four single steps."""
     rng = np.random.default_rng(8)
     w = rand_weights(rng, scale=0.2)
     g = torch.Generator(device="cuda").manual_seed(3)
     s = torch.randn((1, 4096, 1920, C), generator=g, device="cuda", dtype=torch.float32)
-    got, which = run(monkeypatch, "mfma", s, w, 3, 3, 0.5, level=0)
-    want, which1 = run(monkeypatch, "mfma_1step", s, w, 3, 3, 0.5, level=0)
-    assert (which, which1) == (0, 1)   # 2 launches against 3
+    assert octnca.octree_nca_infer_launches(octnca.Model(ndim=2, n_in=3), (1, 4096, 1920), [],
+                                            [4]) == [2]
+    got, which = run("mfma", s, w, 3, 4, 0.5, level=0)
+    want, which1 = run("mfma_1step", s, w, 3, 4, 0.5, level=0)
+    assert (which, which1) == (0, 0)
     assert torch.equal(got, want)
 
 
@@ -92,7 +97,7 @@ def test_two_step_default_on_a_large_level(gpu, monkeypatch):
                          ids=lambda s: "s" + "-".join(map(str, s)))
 @pytest.mark.parametrize("factors", [((1, 2, 2), (1, 2, 2)), ((1, 3, 2), (1, 1, 3))],
                          ids=["f22", "f32-13"])
-def test_two_step_inference_equals_single_steps(gpu, monkeypatch, steps, factors):
+def test_two_step_inference_equals_single_steps(gpu, steps, factors):
     """Whole inference with two-step launches (the first of a level fused with
     the upsample when the level has two or more steps) against one step per
     launch: the final state and the readout are equal bit for bit."""
@@ -100,12 +105,11 @@ def test_two_step_inference_equals_single_steps(gpu, monkeypatch, steps, factors
     from paper_2508_06993_amd.runtime import Inference, to_device_image
     wl = Workload(name="two_step_infer", ndim=2, extent=(1, 72, 96), n_in=3, factors=factors,
                   steps=steps, image_kind="uniform")
-    model = octnca.Model(ndim=2, n_in=3)
-    image = to_device_image(make_image(wl), model)
+    image = to_device_image(make_image(wl), octnca.Model(ndim=2, n_in=3))
     weights = upload_weights(make_weights(wl))
     out = {}
     for kernel in ("mfma_rows", "mfma_rows,mfma_1step"):
-        monkeypatch.setenv("OCTREE_NCA_STEP_KERNEL", kernel)
+        model = octnca.Model(ndim=2, n_in=3, kernel=kernel)
         print(f"two-step inference steps={steps} factors={factors} kernel={kernel}", flush=True)
         run = Inference(model, wl.extent, wl.factors)
         state, seg = run(image, weights, wl.steps, wl.fire_rate, wl.seed)
