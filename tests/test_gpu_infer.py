@@ -67,6 +67,9 @@ SMALL = [
 
 @pytest.mark.parametrize("wl", SMALL, ids=lambda w: w.name)
 def test_infer_matches_oracle(gpu, step_kernel, wl):
+    if (wl.channels, wl.hidden) != (16, 64) and step_kernel in ("mfma_f32", "mfma_bf16x3"):
+        pytest.skip("the matrix-core operand choices serve C/H = 16/64 only; the other "
+                    "sizes run on the vector kernel (the 'mfma' and 'valu' cases)")
     image = make_image(wl)
     weights = make_weights(wl)
     state, seg = gpu_infer(wl, image, weights, kernel=step_kernel)
