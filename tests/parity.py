@@ -28,6 +28,18 @@ def max_rel_err(got, ref):
     return diff / scale if scale > 0 else diff
 
 
+def elementwise_rel_err(got, ref, floor=1e-6):
+    """max over cells and channels of |g - o| / max(|o|, floor * max |o|): the
+    elementwise companion of max_rel_err (reported, not bounded)."""
+    g = np.asarray(got, dtype=np.float64)
+    o = np.asarray(ref, dtype=np.float64)
+    if not o.size:
+        return 0.0
+    den = np.maximum(np.abs(o), floor * float(np.max(np.abs(o))))
+    den[den == 0] = 1.0
+    return float(np.max(np.abs(g - o) / den))
+
+
 def assert_state_close(got, ref, dtype: str, tol=None, what="state"):
     tol = STATE_TOL[dtype] if tol is None else tol
     assert np.all(np.isfinite(np.asarray(got, dtype=np.float64))), f"{what}: non-finite values"
