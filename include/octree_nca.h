@@ -252,6 +252,35 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
 int octree_nca_infer_launches(const octnca_model *model, octnca_extent finest, int32_t levels,
                               const int32_t *factors, const int32_t *steps, int32_t *launches);
 
+/* Size of the static device array octree_nca_infer_static uses as its
+ * workspace (64 MiB per device). */
+#define OCTNCA_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* octree_nca_infer for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same inference, with the workspace taken from a static device array of
+ * OCTNCA_STATIC_SCRATCH_BYTES that the library holds on each device it runs
+ * on until the process ends.  The call allocates nothing (no hipMalloc, no
+ * hipFree, no allocating library routine); the first call on a device looks
+ * the array's address up once.  The caller passes inputs and outputs as for
+ * octree_nca_infer; final_state is required.
+ *   Arguments: as octree_nca_infer, without workspace and level_events.
+ *   final_state  [finest][C], written; must not be NULL.
+ * Workspace needed: octree_nca_workspace_bytes(..., with_final_state = 1)
+ * (pyramid images of levels 1..L-1 plus one finest-size state buffer); a
+ * larger need returns OCTNCA_ESPACE before anything is enqueued.
+ * Every call on one device uses that device's one array, which keeps what the
+ * last call left there (nothing in it needs to start at zero): calls that may
+ * run at the same time on one device (other streams, other host threads) race
+ * and must be serialised by the caller.
+ * Errors: EINVAL (as octree_nca_infer; final_state NULL), ESHAPE, EUNSUPPORTED,
+ * ESPACE (the workspace would exceed the static array), EHIP. */
+int octree_nca_infer_static(const octnca_model *model, const void *image, octnca_extent finest,
+                            int32_t levels, const int32_t *factors,
+                            const octnca_level_weights *weights, const int32_t *steps,
+                            float fire_rate, uint64_t seed, void *final_state, uint8_t *seg,
+                            void *stream);
+
 /* Inference of a batch of images of the same extent (the paper's kernel
  * works on one image and notes that a batch is an extra dimension to iterate
  * over, supplement S3): image b runs exactly as octree_nca_infer, with the

@@ -23,6 +23,7 @@ __all__ = [
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
     "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_infer_launches",
+    "octree_nca_infer_static", "OCTNCA_STATIC_SCRATCH_BYTES",
     "octree_nca_first_level_steps",
     "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
     "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
@@ -39,6 +40,7 @@ OCTNCA_F32, OCTNCA_F16 = 0, 1
 (OCTNCA_MLP_AUTO, OCTNCA_MLP_F32, OCTNCA_MLP_BF16X3, OCTNCA_MLP_F16, OCTNCA_MLP_F16S,
  OCTNCA_MLP_VALU) = range(6)
 OCTNCA_LAYOUT_AUTO, OCTNCA_LAYOUT_ROWS, OCTNCA_LAYOUT_TILES = range(3)
+OCTNCA_STATIC_SCRATCH_BYTES = 64 << 20   # octree_nca_infer_static's device array
 
 # Step-kernel names accepted by Model(kernel=...): a comma-separated list of
 # these, each setting one field of the C model description (octnca_model).
@@ -69,6 +71,7 @@ EXPORTED_SYMBOLS = (
     "octree_nca_build_pyramid", "octree_nca_upsample", "octree_nca_run_level",
     "octree_nca_readout", "octree_nca_readout_classes", "octree_nca_workspace_bytes",
     "octree_nca_infer", "octree_nca_infer_batch", "octree_nca_infer_launches",
+    "octree_nca_infer_static",
     "octree_nca_first_level_steps",
     "octree_nca_fire_mask", "octree_nca_strerror", "octree_nca_abi_version",
     "octree_nca_step_backward_workspace_bytes", "octree_nca_step_backward",
@@ -125,6 +128,10 @@ _SIGS = {
                                 ctypes.POINTER(_LevelWeights), ctypes.POINTER(_I32),
                                 ctypes.c_float, ctypes.c_uint64, _P, ctypes.c_size_t, _P, _P,
                                 ctypes.POINTER(_P), _P]),
+    "octree_nca_infer_static": (_I32, [ctypes.POINTER(_Model), _P, _Extent, _I32,
+                                       ctypes.POINTER(_I32), ctypes.POINTER(_LevelWeights),
+                                       ctypes.POINTER(_I32), ctypes.c_float, ctypes.c_uint64, _P,
+                                       _P, _P]),
     "octree_nca_infer_batch": (_I32, [ctypes.POINTER(_Model), _P, _I32, _Extent, _I32,
                                       ctypes.POINTER(_I32), ctypes.POINTER(_LevelWeights),
                                       ctypes.POINTER(_I32), ctypes.c_float, ctypes.c_uint64, _P,
@@ -359,6 +366,24 @@ def octree_nca_infer(model: Model, image, factors, weights, steps, fire_rate: fl
                                 _ptr(final_state, model.torch_dtype, "final_state"),
                                 _ptr(seg, torch.uint8, "seg"), ev, _stream(stream))
     _check(st, "octree_nca_infer")
+
+
+def octree_nca_infer_static(model: Model, image, factors, weights, steps, fire_rate: float,
+                            seed: int, final_state, seg=None, stream=None) -> None:
+    """octree_nca_infer with the library's static device workspace (no
+    allocation in the call); final_state is required.  Calls on one device
+    share that workspace and must not overlap."""
+    levels = len(steps)
+    d, h, w = image.shape[:3]
+    ws = (_LevelWeights * levels)(*[level_weights_struct(x) for x in weights])
+    st = lib().octree_nca_infer_static(ctypes.byref(model.struct()),
+                                       _ptr(image, model.torch_dtype, "image"),
+                                       _extent((d, h, w)), levels, _factors(factors), ws,
+                                       (_I32 * levels)(*[int(s) for s in steps]),
+                                       float(fire_rate), int(seed),
+                                       _ptr(final_state, model.torch_dtype, "final_state"),
+                                       _ptr(seg, torch.uint8, "seg"), _stream(stream))
+    _check(st, "octree_nca_infer_static")
 
 
 def octree_nca_infer_batch(model: Model, images, factors, weights, steps, fire_rate: float,

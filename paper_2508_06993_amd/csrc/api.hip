@@ -9,6 +9,7 @@
 
 #include <cmath>
 #include <algorithm>
+#include <mutex>
 #include <utility>
 #include "launch.h"
 #include "octree_nca.h"
@@ -515,6 +516,63 @@ int octree_nca_infer(const octnca_model *model, const void *image, octnca_extent
                      void *const *level_events, void *stream) {
     return infer_impl(model, image, finest, levels, factors, weights, steps, fire_rate, seed,
                       workspace, workspace_bytes, final_state, seg, level_events, stream, 0,
+                      false);
+}
+
+// ---------------------------------------------------------------------------
+// Inference without allocation: the workspace is a static device array.
+// ---------------------------------------------------------------------------
+
+}  // extern "C"
+
+namespace {
+
+// Static scratch of octree_nca_infer_static: the pyramid images and the second
+// state buffer of one inference.  Each device the library runs on holds its
+// own copy until the process ends.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, per device.
+__device__ __align__(256) unsigned char scratch[OCTNCA_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of the current device's scratch, looked up once per device
+// (with that device current) and kept; nullptr if the lookup failed.
+void *scratch_ptr() {
+    static std::mutex mu;
+    static void *ptrs[kMaxDevices] = {};
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (ptrs[dev] == nullptr) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return nullptr;
+        ptrs[dev] = p;
+    }
+    return ptrs[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+int octree_nca_infer_static(const octnca_model *model, const void *image, octnca_extent finest,
+                            int32_t levels, const int32_t *factors,
+                            const octnca_level_weights *weights, const int32_t *steps,
+                            float fire_rate, uint64_t seed, void *final_state, uint8_t *seg,
+                            void *stream) {
+    Plan p;
+    int st = make_plan(model, finest, levels, factors, true, &p);
+    if (st) return st;
+    if (final_state == nullptr) return OCTNCA_EINVAL;
+    if (p.bytes > (size_t)OCTNCA_STATIC_SCRATCH_BYTES) return OCTNCA_ESPACE;
+    void *ws = scratch_ptr();
+    if (ws == nullptr) return OCTNCA_EHIP;
+    // Nothing in the workspace needs to start at zero: every pyramid image is
+    // written by the pooling and the state buffer by the seed or a step before
+    // it is read.
+    return infer_impl(model, image, finest, levels, factors, weights, steps, fire_rate, seed, ws,
+                      (size_t)OCTNCA_STATIC_SCRATCH_BYTES, final_state, seg, nullptr, stream, 0,
                       false);
 }
 

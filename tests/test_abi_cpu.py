@@ -417,3 +417,23 @@ def test_build_stamp_tracks_sources(library_path, monkeypatch):
     assert b.source_stamp() == b.source_stamp()
     monkeypatch.setattr(b, "COMMON_FLAGS", b.COMMON_FLAGS + ["-DSTAMP_PROBE"])
     assert not b.is_current()
+
+
+def test_infer_static_validates_before_anything(lib):
+    """octree_nca_infer_static checks its arguments (final_state required) and
+    the workspace need against the static array before it looks the array
+    up or enqueues anything."""
+    f = (ctypes.c_int32 * 3)(1, 2, 2)
+    steps = (ctypes.c_int32 * 2)(2, 2)
+    ws = (_LevelWeights * 2)(*[_LevelWeights(FAKE, FAKE, FAKE, FAKE, FAKE)] * 2)
+    call = lambda m, ext, final: lib.octree_nca_infer_static(m, FAKE, _Extent(*ext), 2, f, ws,
+                                                            steps, 0.5, 0, final, None, None)
+    assert call(model(), (1, 64, 64), None) == EINVAL
+    assert call(model(), (1, 1024, 1024), FAKE2) == ESPACE       # 64 MiB state + pyramid
+    assert call(model(c=13), (1, 64, 64), FAKE2) == EUNSUP
+    assert call(model(), (1, 63, 64), FAKE2) == ESHAPE
+    need = lib.octree_nca_workspace_bytes(model(), _Extent(1, 1024, 1024), 2, f, 1)
+    assert need > octnca.OCTNCA_STATIC_SCRATCH_BYTES
+    hdr = open(HEADER).read()
+    assert re.search(r"#define OCTNCA_STATIC_SCRATCH_BYTES \(\(size_t\)64 << 20\)", hdr)
+    assert octnca.OCTNCA_STATIC_SCRATCH_BYTES == 64 << 20
