@@ -227,7 +227,12 @@ def parity_report(wl, got, want, got_seg, want_seg, what):
     agree = assert_seg_close(got_seg, want_seg, want, wl.dtype, what=what)
     elem = elementwise_rel_err(got, want)
     n = int(np.prod(np.asarray(want_seg).shape))
+    g64, o64 = np.asarray(got, np.float64), np.asarray(want, np.float64)
+    per_cell = np.max(np.abs(g64 - o64), axis=-1).reshape(-1) / max(float(np.max(np.abs(o64))),
+                                                                    1e-30)
+    q = np.quantile(per_cell, [0.5, 0.999, 0.99999])
     print(f"PARITY {wl.name} {what}: cells={n} max_rel_err={err:.3e} "
+          f"(per-cell quantiles 50%={q[0]:.2e} 99.9%={q[1]:.2e} 99.999%={q[2]:.2e}) "
           f"elementwise_rel_err={elem:.3e} agreement={agree:.6f} "
           f"disagreements={int(np.sum(np.asarray(got_seg) != np.asarray(want_seg)))}", flush=True)
 
