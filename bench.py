@@ -330,6 +330,8 @@ def main(argv=None):
     ap.add_argument("--extra", default="video2dt",
                     help="comma-separated further workloads timed in the same run and reported "
                          "under 'workloads' in the same JSON line ('' for none)")
+    ap.add_argument("--model", default="c16h64", choices=sorted(MODEL_SIZES),
+                    help="model size C/H: the paper's 16/64 or the ablation's 12/48, 20/100")
     ap.add_argument("--kernel", default="mfma",
                     help="step kernel, a name accepted by Model(kernel=...), e.g. mfma, "
                          "mfma_1step, mfma_f32, valu")
@@ -368,18 +370,32 @@ def main(argv=None):
     import paper_2508_06993_amd as octnca
     octnca.lib()   # fail loudly if the HIP library is missing
     torch.cuda.set_device(0)
-    wl = WORKLOADS[args.workload]
+    wl = with_model(WORKLOADS[args.workload], args.model)
     out = inference_record(wl, args.kernel, args.steps, args.warmup)
     extras = [w for w in (args.extra.split(",") if args.extra else []) if w and w != wl.name]
     if extras:
         out["workloads"] = {}
         for name in extras:
-            out["workloads"][name] = inference_record(WORKLOADS[name], args.kernel, args.steps,
-                                                      args.warmup, sub=True)
+            out["workloads"][name] = inference_record(with_model(WORKLOADS[name], args.model),
+                                                      args.kernel, args.steps, args.warmup,
+                                                      sub=True)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)
     return 0
+
+
+MODEL_SIZES = {"c16h64": (16, 64), "c12h48": (12, 48), "c20h100": (20, 100)}
+
+
+def with_model(wl, model: str):
+    """The workload with another of the ablation's model sizes (supplement
+    S10): C state channels and H hidden units, the same image and octree."""
+    import dataclasses
+    c, h = MODEL_SIZES[model]
+    if (c, h) == (wl.channels, wl.hidden):
+        return wl
+    return dataclasses.replace(wl, channels=c, hidden=h, name=f"{wl.name}_{model}")
 
 
 def inference_record(wl, kernel: str, steps: int, warmup: int, sub: bool = False) -> dict:
@@ -394,7 +410,8 @@ def inference_record(wl, kernel: str, steps: int, warmup: int, sub: bool = False
 
     print(f"# workload {wl.name}: extent {wl.extent}, levels {wl.levels}, steps {wl.steps}, "
           f"kernel {kernel}", file=sys.stderr, flush=True)
-    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, kernel=kernel)
+    model = octnca.Model(ndim=wl.ndim, n_in=wl.n_in, dtype=wl.dtype, channels=wl.channels,
+                         hidden=wl.hidden, kernel=kernel)
     image_np = cached_image(wl)
     image = to_device_image(image_np, model)
     del image_np

@@ -102,10 +102,10 @@ typedef enum {
  * model and the two other sizes of its ablation, supplement S10), n_in in
  * {1, 3}, state_dtype in {OCTNCA_F32, OCTNCA_F16}.
  * Step kernel: a zero-initialised tail (mlp, layout2d, steps_per_launch all
- * 0) is the library's default.  The matrix-core kernels serve C = 16,
- * H = 64; the other sizes run on the one-thread-per-cell vector kernel and
- * accept only OCTNCA_MLP_AUTO or OCTNCA_MLP_VALU.  Combinations that no
- * kernel implements (OCTNCA_MLP_F16 with fp32 states, OCTNCA_MLP_F16S with
+ * 0) is the library's default.  C = 16, H = 64 takes every option; the
+ * other sizes take OCTNCA_MLP_AUTO (a generic matrix-core step with the
+ * default arithmetic) or OCTNCA_MLP_VALU only.  Combinations that no kernel
+ * implements (OCTNCA_MLP_F16 with fp32 states, OCTNCA_MLP_F16S with
  * fp16 states) give OCTNCA_EUNSUPPORTED; values outside the enums give
  * OCTNCA_EINVAL.  The training entry points always use fp32 MLP operands
  * and ignore these three fields. */

@@ -882,10 +882,10 @@ namespace octnca {
 // The step kernel comes with the arguments (StepArgs::kc, filled from the
 // caller's octnca_model); nothing here reads the environment.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
-    // the matrix-core kernels are built for C = 16, H = 64; the other model
-    // sizes always run on the vector kernel
-    if (a.channels != kC || a.hidden != kH || a.kc.valu)
-        return launch_step_valu(a, src, dst, stream);
+    if (a.kc.valu) return launch_step_valu(a, src, dst, stream);
+    // the specialised matrix-core kernels are built for C = 16, H = 64; the
+    // ablation's other sizes run on the generic matrix-core kernel
+    if (a.channels != kC || a.hidden != kH) return launch_step_gen(a, src, dst, stream);
     return launch_step_mfma(a, a.kc.mlp, a.kc.layout, src, dst, stream);
 }
 

@@ -78,6 +78,10 @@ hipError_t launch_step_up(const StepArgs &a, const void *coarse, int coarse_h, i
                           int fz, int fy, int fx, const void *img, void *dst,
                           hipStream_t stream);
 hipError_t launch_step_valu(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
+// Matrix-core step for the model sizes other than C = 16, H = 64 (the
+// ablation's 12 / 48 and 20 / 100): whether it serves `a`, and the launch.
+bool step_gen_serves(const StepArgs &a);
+hipError_t launch_step_gen(const StepArgs &a, const void *src, void *dst, hipStream_t stream);
 // Whether launch_step_pair runs steps a.step and a.step + 1 in one launch, and
 // that launch (the state after step a.step is not written to memory).
 bool step_pairs(const StepArgs &a);

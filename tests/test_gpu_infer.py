@@ -60,12 +60,19 @@ SMALL = [
     Workload(name="odd_steps_f16_2d", ndim=2, extent=(1, 48, 36), n_in=1,
              factors=((1, 2, 2), (1, 3, 3)), steps=(3, 1, 5), dtype="f16",
              image_kind="uniform"),
-    # the ablation's model sizes (supplement S10), on the vector kernel
+    # the ablation's model sizes (supplement S10): the generic matrix-core
+    # kernel ("mfma" cases) and the vector kernel ("valu")
     Workload(name="c12h48_2d", ndim=2, extent=(1, 64, 96), n_in=3, factors=((1, 2, 2),) * 2,
              steps=(4, 3, 5), image_kind="uniform", channels=12, hidden=48),
     Workload(name="c20h100_3d_f16", ndim=3, extent=(8, 16, 24), n_in=3,
              factors=((1, 2, 2), (2, 2, 2)), steps=(3, 2, 4), dtype="f16",
              image_kind="uniform", channels=20, hidden=100),
+    Workload(name="c20h100_2d", ndim=2, extent=(1, 72, 136), n_in=3,
+             factors=((1, 2, 2),) * 2, steps=(5, 4, 3), image_kind="uniform",
+             channels=20, hidden=100),
+    Workload(name="c12h48_3d_nin1", ndim=3, extent=(10, 24, 40), n_in=1,
+             factors=((1, 2, 2), (2, 2, 2)), steps=(4, 3, 2), image_kind="uniform",
+             channels=12, hidden=48),
 ]
 
 

@@ -261,27 +261,34 @@ def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     assert max_rel_err(got, want) <= tol
 
 
+@pytest.mark.parametrize("kernel", ["mfma", "valu"])
 @pytest.mark.parametrize("dt,ndim,n_in,c,h,shape", [
     ("f32", 2, 3, 12, 48, (1, 37, 45)), ("f32", 3, 1, 20, 100, (5, 9, 17)),
     ("f16", 2, 1, 20, 100, (1, 21, 30)), ("f16", 3, 3, 12, 48, (6, 11, 10)),
-    ("f32", 3, 3, 12, 48, (4, 10, 12)), ("f16", 2, 3, 12, 48, (1, 16, 40))])
-def test_other_model_sizes_match_oracle(gpu, dt, ndim, n_in, c, h, shape):
-    """The ablation's model sizes C/H = 12/48 and 20/100 (supplement S10) run on
-    the vector kernel: one step and nine steps against the oracle, input
-    channels unchanged, non-firing cells copied bit for bit."""
+    ("f32", 3, 3, 12, 48, (4, 10, 12)), ("f16", 2, 3, 12, 48, (1, 16, 40)),
+    ("f32", 2, 3, 20, 100, (1, 19, 70)), ("f32", 2, 1, 12, 48, (1, 33, 65)),
+    ("f16", 3, 1, 20, 100, (7, 9, 33)), ("f32", 3, 3, 20, 100, (3, 5, 40)),
+    ("f32", 2, 3, 12, 48, (1, 1, 1)), ("f16", 3, 3, 20, 100, (1, 1, 1))])
+def test_other_model_sizes_match_oracle(gpu, kernel, dt, ndim, n_in, c, h, shape):
+    """The ablation's model sizes C/H = 12/48 and 20/100 (supplement S10), on
+    the generic matrix-core kernel ("mfma", the default) and the vector kernel:
+    one step and nine steps against the oracle (several tiles, ragged tails,
+    a single cell), input channels unchanged, non-firing cells copied bit for
+    bit."""
     rng = np.random.default_rng(13)
     w = rand_weights(rng, ndim, c=c, h=h)
     s = rng.normal(0, 1, shape + (c,)).astype(NP_DT[dt])
-    model = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, channels=c, hidden=h)
+    model = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, channels=c, hidden=h, kernel=kernel)
     got, which = run_level_gpu(model, s, w, 2, 1, 0.5, 42)
+    assert which == 1
     want = oracle.nca_step(s, w, n_in, ndim, 2, 0, 42, 0.5, NP_DT[dt])
-    assert max_rel_err(got, want) <= STEP_TOL[(dt, "valu")][0]
+    assert max_rel_err(got, want) <= STEP_TOL[(dt, kernel)][0]
     np.testing.assert_array_equal(got[..., :n_in], s[..., :n_in])
     mask = oracle.fire_mask(42, 2, 0, shape, 0.5)
     np.testing.assert_array_equal(got[~mask], s[~mask])
     got9, _ = run_level_gpu(model, s, w, 1, 9, 0.5, 3)
     want9 = oracle.run_level(s, w, n_in, ndim, 1, 9, 3, 0.5, NP_DT[dt])
-    assert max_rel_err(got9, want9) <= STEP_TOL[(dt, "valu")][1]
+    assert max_rel_err(got9, want9) <= STEP_TOL[(dt, kernel)][1]
 
 
 def test_zero_steps_leave_state(gpu):
