@@ -380,7 +380,7 @@ int octree_nca_readout_mse(const octnca_model *model, const void *state, const f
                            size_t workspace_bytes, void *stream);
 
 /* Bytes of workspace octree_nca_train_step needs: pyramid images, every state
- * of every level, two finest-size gradients and the step-backward workspace
+ * of every level, two finest-size gradients and the backward's workspace
  * (0 if an argument is invalid). */
 size_t octree_nca_train_workspace_bytes(const octnca_model *model, octnca_extent finest,
                                         int32_t levels, const int32_t *factors,

@@ -717,7 +717,7 @@ namespace {
 
 // Workspace of a training step: pyramid images 1..L-1, the states of every
 // level (before each step and after the last), two finest-size gradient
-// buffers, the step-backward workspace (finest size) and the loss partials.
+// buffers, the level-backward workspace (finest size) and the loss partials.
 struct TrainPlan {
     octnca_extent ext[kMaxLevels];
     size_t image_off[kMaxLevels];
@@ -753,7 +753,7 @@ int make_train_plan(const octnca_model *m, octnca_extent finest, int32_t levels,
     off += gb;
     p->bwd_off = off;
     // the finest level needs the most (every level's extent is at most the finest's)
-    off += align_up(step_backward_workspace_floats(m->ndim, m->channels, m->hidden, ext3(finest)) *
+    off += align_up(level_backward_workspace_floats(m->ndim, m->channels, m->hidden, ext3(finest)) *
                     4);
     p->mse_off = off;
     off += align_up(mse_workspace_doubles(cells) * sizeof(double));
@@ -860,10 +860,13 @@ int octree_nca_train_step(const octnca_model *model, const void *image, octnca_e
         StepArgs a = step_args(model, p.ext[l], &weights[l], l, seed, threshold, 0);
         const LevelGradsDev gd{grads[l].conv_w, grads[l].conv_b, grads[l].w1, grads[l].b1,
                                grads[l].w2};
-        for (int t = steps[l] - 1; t >= 0; --t) {
-            a.step = (uint32_t)t;
-            if (!ok(launch_step_backward(a, tape(l, t), g, g, gd, (float *)(ws + p.bwd_off), s)))
+        // all steps of the level, last first (dL/dS of its first state lands
+        // in the other gradient buffer)
+        if (steps[l] > 0) {
+            if (!ok(launch_level_backward(a, steps[l], tape(l, 0), g, g_other, gd,
+                                          (float *)(ws + p.bwd_off), s)))
                 return OCTNCA_EHIP;
+            std::swap(g, g_other);
         }
         if (l + 1 < levels) {
             if (!ok(launch_upsample_adjoint(g, ext3(p.ext[l + 1]), factors[3 * l],

@@ -99,6 +99,16 @@ hipError_t launch_step_pair_up(const StepArgs &a, const void *coarse, int coarse
 size_t step_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 extent);
 hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,
                                 float *gin, LevelGradsDev g, float *ws, hipStream_t stream);
+// Backward of all `steps` steps of a level (a.step unused): states holds the
+// level's states before steps 0 .. steps-1 (state t at states + t * cells * C),
+// gout = dL/dS after the last step; gin receives dL/dS of the level's first
+// state (must not alias gout or states) and the weight gradients are added to
+// g.  ws holds level_backward_workspace_floats floats.  steps = 0 enqueues
+// nothing (gin is not written).
+size_t level_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 extent);
+hipError_t launch_level_backward(const StepArgs &a, int32_t steps, const float *states,
+                                 const float *gout, float *gin, LevelGradsDev g, float *ws,
+                                 hipStream_t stream);
 // Adjoint of the upsample + inject from `coarse` (extent of the coarse level).
 hipError_t launch_upsample_adjoint(const float *gfine, Extent3 coarse, int fz, int fy, int fx,
                                    int n_in, int channels, float *gcoarse, hipStream_t stream);

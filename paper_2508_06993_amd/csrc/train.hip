@@ -8,7 +8,7 @@
 //   gu = m G' (hidden channels), dW2 += gu h^T, ga = (W2^T gu) * [a > 0],
 //   dW1 += ga f^T, db1 += ga, [gS, gP] = W1^T ga, dconv_b += gP,
 //   dK[c][t] += gP[p][c] S[p + o_t][c], dL/dS = G' + gS + conv^T(gP).
-// Three launches:
+// Three kernels:
 //   1. bwd_cell: four lanes per cell, blocks of 64 cells (halo tile of S in
 //      LDS): perception, then the hidden units streamed once, a quarter per
 //      lane, each giving a, h, gh and ga; writes G' + gS and gP to memory and
@@ -21,6 +21,10 @@
 //      (wave w takes rows w, w + 16, ... in order, then the waves' sums in
 //      wave order) to the caller's gradients (accumulated, so the steps of a
 //      level sum up).
+// One step (octree_nca_step_backward) runs the three.  A level of a training
+// step runs bwd_cell once per step, each after the first forming its G' from
+// the previous one's (G' + gS, gP) with the transposed convolution fused and
+// adding to its block's partial row, then bwd_conv_t and wgrad_reduce once.
 #include "launch.h"
 
 namespace octnca {
@@ -81,7 +85,11 @@ __device__ __forceinline__ void stage(Load load, Store store) {
 // per cell a job reads two 16-byte words and does up to 16 FMAs, in cell
 // order.  out receives the G::N sums (one block-major row).
 template <int NDIM, int C, int H, class State>
-__device__ __forceinline__ void wgrad_block(const float *recs, State state, float *out) {
+__device__ __forceinline__ void wgrad_block(const float *recs, State state, float *out,
+                                            bool accumulate) {
+    // the sums start from the block's row (accumulate: the steps of a level,
+    // in order) or from zero
+    auto start = [&](int o) { return accumulate ? out[o] : 0.f; };
     using R = Rec<C, H>;
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
     using G = WG<C, H, TAPS>;
@@ -107,7 +115,11 @@ __device__ __forceinline__ void wgrad_block(const float *recs, State state, floa
                 ea = R::GU + 4 * cb; eb = R::Hh + 4 * jb;
                 o0 = G::W2 + 4 * cb * H + 4 * jb; os = H;
             }
-            float acc[4][4] = {};
+            float acc[4][4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < 4; ++c) acc[r][c] = start(o0 + r * os + c);
 #pragma unroll 4
             for (int i = 0; i < kWgCells; ++i) {
                 const float4 av = quad(i, ea), bv = quad(i, eb);
@@ -125,7 +137,7 @@ __device__ __forceinline__ void wgrad_block(const float *recs, State state, floa
             const int jj = job - J1 - J2;
             const int e = jj < JB ? R::GA + 4 * jj : R::GP + 4 * (jj - JB);
             const int o0 = jj < JB ? G::B1 + 4 * jj : G::CB + 4 * (jj - JB);
-            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            float sum[4] = {start(o0), start(o0 + 1), start(o0 + 2), start(o0 + 3)};
             for (int i = 0; i < kWgCells; ++i) {
                 const float4 v = quad(i, e);
                 sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
@@ -135,7 +147,9 @@ __device__ __forceinline__ void wgrad_block(const float *recs, State state, floa
         } else {                                 // dconv_w[c][t] = sum gP[c] S[p + o_t][c]
             const int jj = job - J1 - J2 - JB - JC;
             const int cq = jj / TAPS, t = jj % TAPS;
-            float sum[4] = {0.f, 0.f, 0.f, 0.f};
+            float sum[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sum[r] = start(G::CW + (4 * cq + r) * TAPS + t);
 #pragma unroll 4
             for (int i = 0; i < kWgCells; ++i) {
                 const float4 gpv = quad(i, R::GP + 4 * cq);
@@ -162,14 +176,23 @@ template <int NDIM> struct BwdCellTile;
 template <> struct BwdCellTile<2> { static constexpr int TZ = 1, TY = 2, TX = 32; };
 template <> struct BwdCellTile<3> { static constexpr int TZ = 2, TY = 4, TX = 8; };
 
+// G' (dL/dS' of the step) comes from gout, or, when gp_prev is not null,
+// from the previous backward step (the step after this one in the forward)
+// as gout + conv^T(gp_prev): its pass-through part and the transposed
+// convolution of its perception gradient, formed here for the block's cells
+// (the tile of gp_prev with a one-cell halo in LDS), so that no separate
+// launch has to write dL/dS between the steps of a level.  accumulate: the
+// block's weight-gradient sums are added to its partial row (the steps of a
+// level, in order) instead of replacing it.
 template <int NDIM, int NIN, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
-    const float *__restrict__ src, const float *__restrict__ gout, int dd, int dh, int dw,
+    const float *__restrict__ src, const float *__restrict__ gout,
+    const float *__restrict__ gp_prev, int dd, int dh, int dw,
     int tiles_x, int tiles_y, const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
     float *__restrict__ gpart, float *__restrict__ gp, float *__restrict__ partial,
-    int64_t cells) {
+    int64_t cells, int accumulate) {
     using T = BwdCellTile<NDIM>;
     using R = Rec<C, H>;
     constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
@@ -184,6 +207,10 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     __shared__ float sb1[H];
     constexpr int RS = R::N + 4;   // words per record row (16-byte aligned rows)
     __shared__ __align__(16) float recs[kWgCells * RS];   // [cell][entry]
+    // gp_prev of the tile and its halo ([c][cell], for the fused G'), in the
+    // record rows' space: read before the first record is written
+    static_assert(C * NCELL <= kWgCells * RS, "gp_prev tile fits the record rows");
+    float *const gtile = recs;
 
     int b = blockIdx.x;
     const int bx = b % tiles_x;
@@ -203,6 +230,19 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
             return in ? v : 0.f;
         },
         [&](int i, float v) { tile[i / NCELL][i % NCELL] = v; });
+    if (gp_prev != nullptr)
+        stage<NCELL * C, 8>(
+            [&](int i) {
+                const int c = i / NCELL, cell = i % NCELL;
+                const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+                const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+                const bool in = gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+                const int cx = min(max(gx, 0), dw - 1), cy = min(max(gy, 0), dh - 1),
+                          cz = min(max(gz, 0), dd - 1);
+                const float v = gp_prev[c * cells + ((int64_t)cz * dh + cy) * dw + cx];
+                return in ? v : 0.f;
+            },
+            [&](int i, float v) { gtile[i] = v; });
     stage<H * 2 * C, 8>([&](int i) { return w1[i]; },
                         [&](int i, float v) { sw1[i / (2 * C)][i % (2 * C)] = v; });
     stage<C * H, 8>([&](int i) { return w2[i]; },
@@ -234,12 +274,40 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
         for (int c = 0; c < C; ++c) f[C + c] = fmaf(conv_w[c * TAPS + t], tile[c][nb], f[C + c]);
     }
     const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
-    const float *g = gout + idx * C;
+    constexpr int FP = 2 * C / kParts, CP = C / kParts;
+    // G' = dL/dS' of this cell, the quad's part: channels part * CP + k
+    float gq[CP];
+#pragma unroll
+    for (int k = 0; k < CP; ++k) gq[k] = gout[idx * C + part * CP + k];
+    if (gp_prev != nullptr) {
+        // cell p receives K[c][t] gP[p - o_t] from each tap t
+#pragma unroll
+        for (int t = 0; t < TAPS; ++t) {
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            const int nb = centre - (dz * HY + dy) * HX - dx;
+#pragma unroll
+            for (int k = 0; k < CP; ++k) {
+                const int c = part * CP + k;
+                gq[k] = fmaf(conv_w[c * TAPS + t], gtile[c * NCELL + nb], gq[k]);
+            }
+        }
+        __syncthreads();   // every lane has read gtile before the records overwrite it
+    }
+    float *r = recs + cl * RS;   // this cell's record row
+    // the quad's parts share gu = m G' (hidden channels) through the record
+    // row; the four lanes of a cell are in one wave, whose LDS accesses
+    // complete in order
+#pragma unroll
+    for (int k = 0; k < CP; ++k) {
+        const int c = part * CP + k;
+        r[R::GU + c] = (c >= NIN && fire) ? gq[k] : 0.f;
+    }
+    __builtin_amdgcn_wave_barrier();
     float gu[C];
 #pragma unroll
-    for (int c = 0; c < C; ++c) gu[c] = (c >= NIN && fire) ? g[c] : 0.f;
+    for (int c = 0; c < C; ++c) gu[c] = r[R::GU + c];
+    __builtin_amdgcn_wave_barrier();
 
-    float *r = recs + cl * RS;   // this cell's record row
     float gf[2 * C];
 #pragma unroll
     for (int k = 0; k < 2 * C; ++k) gf[k] = 0.f;
@@ -264,7 +332,6 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
         gf[k] += __shfl_xor(gf[k], 1);
         gf[k] += __shfl_xor(gf[k], 2);
     }
-    constexpr int FP = 2 * C / kParts, CP = C / kParts;
 #pragma unroll
     for (int k = 0; k < 2 * C; ++k)
         if (k / FP == part) r[R::F + k] = valid ? f[k] : 0.f;
@@ -275,7 +342,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
             r[R::GP + c] = valid ? gf[C + c] : 0.f;
             if (valid) {
                 gp[c * cells + idx] = gf[C + c];
-                gpart[idx * C + c] = g[c] + gf[c];
+                gpart[idx * C + c] = gq[c - part * CP] + gf[c];
             }
         }
     __syncthreads();
@@ -286,7 +353,7 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
         const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
         const int nb = ((pz + (NDIM == 3 ? 1 : 0) + dz) * HY + py + 1 + dy) * HX + px + 1 + dx;
         return tile[c][nb];
-    }, partial + (int64_t)blockIdx.x * WG<C, H, TAPS>::N);
+    }, partial + (int64_t)blockIdx.x * WG<C, H, TAPS>::N, accumulate != 0);
 }
 
 template <int NDIM, int C, int H>
@@ -371,39 +438,99 @@ __global__ __launch_bounds__(64 * kRedWaves) void wgrad_reduce(const float *__re
     *dst = (float)((double)*dst + t);
 }
 
+// Block counts of the two backward tilings of a level.
+template <int NDIM>
+struct BwdGrid {
+    int tiles_x, tiles_y, ctiles_x, ctiles_y;
+    int64_t blocks, cblocks;
+    explicit BwdGrid(const Extent3 &e) {
+        using T = BwdTile<NDIM>;
+        using TC = BwdCellTile<NDIM>;
+        tiles_x = (int)((e.w + T::TX - 1) / T::TX);
+        tiles_y = (int)((e.h + T::TY - 1) / T::TY);
+        blocks = (int64_t)tiles_x * tiles_y * ((e.d + T::TZ - 1) / T::TZ);
+        ctiles_x = (int)((e.w + TC::TX - 1) / TC::TX);
+        ctiles_y = (int)((e.h + TC::TY - 1) / TC::TY);
+        cblocks = (int64_t)ctiles_x * ctiles_y * ((e.d + TC::TZ - 1) / TC::TZ);
+    }
+};
+
+template <int NDIM, int NIN, int C, int H>
+void enqueue_bwd_cell(const StepArgs &a, const BwdGrid<NDIM> &gr, const float *src,
+                      const float *gout, const float *gp_prev, float *gpart, float *gp,
+                      float *partial, bool accumulate, hipStream_t stream) {
+    bwd_cell<NDIM, NIN, C, H><<<(unsigned)gr.cblocks, kBwdThreads, 0, stream>>>(
+        src, gout, gp_prev, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, gr.ctiles_x, gr.ctiles_y,
+        a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
+        a.threshold, gpart, gp, partial, a.ext.cells(), accumulate ? 1 : 0);
+}
+
+template <int NDIM, int C, int H>
+void enqueue_tail(const StepArgs &a, const BwdGrid<NDIM> &gr, const float *gpart, const float *gp,
+                  float *gin, const float *partial, LevelGradsDev g, hipStream_t stream) {
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    bwd_conv_t<NDIM, C, H><<<(unsigned)gr.blocks, kBwdThreads, 0, stream>>>(
+        gpart, gp, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, gr.tiles_x, gr.tiles_y, a.w.conv_w,
+        gin, a.ext.cells());
+    wgrad_reduce<C, H, TAPS><<<(WG<C, H, TAPS>::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(
+        partial, gr.cblocks, g);
+}
+
+// One step: bwd_cell, bwd_conv_t, wgrad_reduce.
 template <int NDIM, int NIN, int C, int H>
 hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, float *gin,
                       LevelGradsDev g, float *ws, hipStream_t stream) {
-    using T = BwdTile<NDIM>;
-    using TC = BwdCellTile<NDIM>;
-    constexpr int TAPS = NDIM == 3 ? 27 : 9;
     const int64_t cells = a.ext.cells();
     if (cells == 0) return hipSuccess;
-    const int tiles_x = (int)((a.ext.w + T::TX - 1) / T::TX);
-    const int tiles_y = (int)((a.ext.h + T::TY - 1) / T::TY);
-    const int tiles_z = (int)((a.ext.d + T::TZ - 1) / T::TZ);
-    const int64_t blocks = (int64_t)tiles_x * tiles_y * tiles_z;
-    const int ctiles_x = (int)((a.ext.w + TC::TX - 1) / TC::TX);
-    const int ctiles_y = (int)((a.ext.h + TC::TY - 1) / TC::TY);
-    const int64_t cblocks = (int64_t)ctiles_x * ctiles_y * ((a.ext.d + TC::TZ - 1) / TC::TZ);
+    const BwdGrid<NDIM> gr(a.ext);
     float *gpart = ws;                 // G' + gS
     float *gp = gpart + cells * C;     // gP, [C][cells]
     float *partial = gp + cells * C;   // [cblocks][entries]
-    bwd_cell<NDIM, NIN, C, H><<<(unsigned)cblocks, kBwdThreads, 0, stream>>>(
-        src, gout, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, ctiles_x, ctiles_y, a.w.conv_w,
-        a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold, gpart,
-        gp, partial, cells);
-    bwd_conv_t<NDIM, C, H><<<(unsigned)blocks, kBwdThreads, 0, stream>>>(
-        gpart, gp, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y, a.w.conv_w, gin,
-        cells);
-    wgrad_reduce<C, H, TAPS><<<(WG<C, H, TAPS>::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(
-        partial, cblocks, g);
+    enqueue_bwd_cell<NDIM, NIN, C, H>(a, gr, src, gout, nullptr, gpart, gp, partial, false,
+                                      stream);
+    enqueue_tail<NDIM, C, H>(a, gr, gpart, gp, gin, partial, g, stream);
+    return hipGetLastError();
+}
+
+// All steps of a level, last step first: each bwd_cell after the first takes
+// G' from the previous one's (G' + gS, gP) with the transposed convolution
+// fused, the weight-gradient sums accumulate in the blocks' partial rows, and
+// one bwd_conv_t and one wgrad_reduce finish the level.
+template <int NDIM, int NIN, int C, int H>
+hipError_t launch_bwd_level(const StepArgs &a0, int32_t steps, const float *states,
+                            const float *gout, float *gin, LevelGradsDev g, float *ws,
+                            hipStream_t stream) {
+    const int64_t cells = a0.ext.cells();
+    if (cells == 0 || steps <= 0) return hipSuccess;
+    const BwdGrid<NDIM> gr(a0.ext);
+    float *gpart[2] = {ws, ws + cells * C};
+    float *gp[2] = {ws + 2 * cells * C, ws + 3 * cells * C};
+    float *partial = ws + 4 * cells * C;
+    StepArgs a = a0;
+    int cur = 0;
+    for (int32_t t = steps - 1; t >= 0; --t) {
+        a.step = (uint32_t)t;
+        const bool first = t == steps - 1;
+        enqueue_bwd_cell<NDIM, NIN, C, H>(a, gr, states + (size_t)t * cells * C,
+                                          first ? gout : gpart[cur ^ 1],
+                                          first ? nullptr : gp[cur ^ 1], gpart[cur], gp[cur],
+                                          partial, !first, stream);
+        cur ^= 1;
+    }
+    enqueue_tail<NDIM, C, H>(a, gr, gpart[cur ^ 1], gp[cur ^ 1], gin, partial, g, stream);
     return hipGetLastError();
 }
 
 template <int NDIM, int C, int H>
 hipError_t bwd_nin(const StepArgs &a, const float *src, const float *gout, float *gin,
-                   LevelGradsDev g, float *ws, hipStream_t stream) {
+                   LevelGradsDev g, float *ws, hipStream_t stream, int32_t level_steps) {
+    if (level_steps >= 0) {
+        if (a.n_in == 1)
+            return launch_bwd_level<NDIM, 1, C, H>(a, level_steps, src, gout, gin, g, ws, stream);
+        if (a.n_in == 3)
+            return launch_bwd_level<NDIM, 3, C, H>(a, level_steps, src, gout, gin, g, ws, stream);
+        return hipErrorInvalidValue;
+    }
     if (a.n_in == 1) return launch_bwd<NDIM, 1, C, H>(a, src, gout, gin, g, ws, stream);
     if (a.n_in == 3) return launch_bwd<NDIM, 3, C, H>(a, src, gout, gin, g, ws, stream);
     return hipErrorInvalidValue;
@@ -411,11 +538,13 @@ hipError_t bwd_nin(const StepArgs &a, const float *src, const float *gout, float
 
 template <int NDIM>
 hipError_t bwd_size(const StepArgs &a, const float *src, const float *gout, float *gin,
-                    LevelGradsDev g, float *ws, hipStream_t stream) {
-    if (a.channels == 16 && a.hidden == 64) return bwd_nin<NDIM, 16, 64>(a, src, gout, gin, g, ws, stream);
-    if (a.channels == 12 && a.hidden == 48) return bwd_nin<NDIM, 12, 48>(a, src, gout, gin, g, ws, stream);
+                    LevelGradsDev g, float *ws, hipStream_t stream, int32_t level_steps) {
+    if (a.channels == 16 && a.hidden == 64)
+        return bwd_nin<NDIM, 16, 64>(a, src, gout, gin, g, ws, stream, level_steps);
+    if (a.channels == 12 && a.hidden == 48)
+        return bwd_nin<NDIM, 12, 48>(a, src, gout, gin, g, ws, stream, level_steps);
     if (a.channels == 20 && a.hidden == 100)
-        return bwd_nin<NDIM, 20, 100>(a, src, gout, gin, g, ws, stream);
+        return bwd_nin<NDIM, 20, 100>(a, src, gout, gin, g, ws, stream, level_steps);
     return hipErrorInvalidValue;
 }
 
@@ -494,10 +623,25 @@ size_t step_backward_workspace_floats(int ndim, int channels, int hidden, Extent
     return (size_t)(2 * cells * channels + cblocks * wg_n);
 }
 
+size_t level_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 e) {
+    // two more cell-sized buffers than one step: (G' + gS, gP) of the step
+    // read and of the step written
+    return step_backward_workspace_floats(ndim, channels, hidden, e) +
+           (size_t)(2 * e.cells() * channels);
+}
+
 hipError_t launch_step_backward(const StepArgs &a, const float *src, const float *gout,
                                 float *gin, LevelGradsDev g, float *ws, hipStream_t stream) {
-    return a.ndim == 2 ? bwd_size<2>(a, src, gout, gin, g, ws, stream)
-                       : bwd_size<3>(a, src, gout, gin, g, ws, stream);
+    return a.ndim == 2 ? bwd_size<2>(a, src, gout, gin, g, ws, stream, -1)
+                       : bwd_size<3>(a, src, gout, gin, g, ws, stream, -1);
+}
+
+hipError_t launch_level_backward(const StepArgs &a, int32_t steps, const float *states,
+                                 const float *gout, float *gin, LevelGradsDev g, float *ws,
+                                 hipStream_t stream) {
+    if (steps <= 0) return hipSuccess;
+    return a.ndim == 2 ? bwd_size<2>(a, states, gout, gin, g, ws, stream, steps)
+                       : bwd_size<3>(a, states, gout, gin, g, ws, stream, steps);
 }
 
 hipError_t launch_upsample_adjoint(const float *gfine, Extent3 coarse, int fz, int fy, int fx,

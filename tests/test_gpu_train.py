@@ -157,6 +157,10 @@ TRAIN_CASES = [
     ("2d-3lvl", 2, 3, (1, 32, 48), ((1, 2, 2), (1, 2, 2)), (3, 2, 4)),
     ("3d-2lvl", 3, 1, (4, 16, 24), ((2, 2, 2),), (2, 3)),
     ("2dt-2lvl", 3, 3, (6, 8, 20), ((1, 2, 2),), (3, 1)),
+    # a level without steps between two with several (its gradient passes
+    # straight to the upsample's adjoint); ragged backward tiles
+    ("2d-zero-steps", 2, 3, (1, 36, 68), ((1, 2, 2), (1, 3, 2)), (4, 0, 3)),
+    ("2d-5steps", 2, 1, (1, 70, 40), ((1, 2, 2),), (5, 2)),
 ]
 
 
