@@ -356,6 +356,294 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_cell(
     }, partial + (int64_t)blockIdx.x * WG<C, H, TAPS>::N, accumulate != 0);
 }
 
+// bwd_cell on the matrix cores, for C = 16, H = 64: the same results as
+// bwd_cell (fp32 products, fp32 sums), with every contraction on
+// v_mfma_f32_16x16x4_f32.  A wave takes 16 cells of the block's 64 (lane l:
+// cell n = l % 16, lane group g = l / 16, which owns channel quad g), in the
+// lane layout of the forward step kernels:
+//   * features: the lane's 8 K slots are state channels 4g..4g+3 and
+//     perception channels 4g..4g+3 of its cell; layer 1 recomputed as 4
+//     hidden tiles x 8 K chunks, leaving a = W1 f + b1 of hidden unit
+//     16 t + 4 g + i in register i of tile t;
+//   * gh = W2^T gu: K chunk i holds channel 4 g + i in lane group g, which is
+//     the lane's own G' value i, so 4 tiles x 4 chunks with A = W2 gathered;
+//     gh lands in the layout of a, and ga = gh [a > 0] is elementwise;
+//   * W1^T ga: K chunk (t, i) holds hidden unit 16 t + 4 g + i in lane group
+//     g (the lane's own ga), 2 output tiles of 16 features x 16 chunks; tile
+//     0 gives gS and tile 1 gP of channels 4g..4g+3: the lane's own quad, so
+//     G' + gS and gP are stored without exchange;
+//   * the block's outer-product sums dW1 = sum ga f^T and dW2 = sum gu h^T
+//     take the cells as K: the cells' records [f | h | ga | gu | gP] go to
+//     LDS, and each wave reads them back as MFMA operands (4 cells per K
+//     chunk, 16 chunks per output tile; wave w takes dW1 tiles 2w, 2w+1 and
+//     dW2 tile w); db1, dconv_b and dconv_w are summed on the VALU.
+// Record rows are padded so that the 4 rows a wave reads at once start 16
+// banks apart.
+template <int NDIM, int NIN>
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
+    const float *__restrict__ src, const float *__restrict__ gout,
+    const float *__restrict__ gp_prev, int dd, int dh, int dw, int tiles_x, int tiles_y,
+    const float *__restrict__ conv_w, const float *__restrict__ conv_b,
+    const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
+    uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
+    float *__restrict__ gpart, float *__restrict__ gp, float *__restrict__ partial,
+    int64_t cells, int accumulate) {
+    constexpr int C = 16, H = 64;
+    using T = BwdCellTile<NDIM>;
+    using G = WG<C, H, NDIM == 3 ? 27 : 9>;
+    constexpr int HZ = NDIM == 3 ? T::TZ + 2 : 1, HY = T::TY + 2, HX = T::TX + 2;
+    constexpr int NCELL = HZ * HY * HX;
+    constexpr int TAPS = NDIM == 3 ? 27 : 9;
+    constexpr int SF = 48, SH = 80, SQ = 16;   // record row strides (floats)
+    static_assert(T::TZ * T::TY * T::TX == kWgCells, "64 cells per block");
+    typedef float v4 __attribute__((ext_vector_type(4)));
+
+    __shared__ float4 tile[4][NCELL];       // S, channel quads
+    // records: f [64][SF], h and ga [64][SH], gu and gP [64][SQ]; the gp_prev
+    // tile (fused G') lives in the same space before the records are written
+    __shared__ __align__(16) float recs[kWgCells * (SF + 2 * SH + 2 * SQ)];
+    float *const rf = recs;
+    float *const rh = rf + kWgCells * SF;
+    float *const rga = rh + kWgCells * SH;
+    float *const rgu = rga + kWgCells * SH;
+    float *const rgp = rgu + kWgCells * SQ;
+    float4 *const gtile = reinterpret_cast<float4 *>(recs);   // [4][NCELL]
+    static_assert(4 * NCELL * 4 <= kWgCells * (SF + 2 * SH + 2 * SQ), "gp_prev tile fits");
+
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n = lane & 15, g = lane >> 4;
+    int b = blockIdx.x;
+    const int bx = b % tiles_x;
+    b /= tiles_x;
+    const int by = b % tiles_y;
+    const int bz = b / tiles_y;
+    const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
+
+    // S (and gp_prev) tiles with a one-cell halo, zero outside the grid
+    auto halo_cell = [&](int cell, int64_t &gidx) {
+        const int lx = cell % HX, ly = (cell / HX) % HY, lz = cell / (HX * HY);
+        const int gx = x0 + lx - 1, gy = y0 + ly - 1, gz = NDIM == 3 ? z0 + lz - 1 : 0;
+        gidx = ((int64_t)gz * dh + gy) * dw + gx;
+        return gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
+    };
+    for (int i = threadIdx.x; i < 4 * NCELL; i += kBwdThreads) {
+        const int q = i % 4, cell = i / 4;
+        int64_t gi;
+        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (halo_cell(cell, gi)) v = *reinterpret_cast<const float4 *>(src + gi * C + 4 * q);
+        tile[q][cell] = v;
+    }
+    if (gp_prev != nullptr)
+        for (int i = threadIdx.x; i < 4 * NCELL; i += kBwdThreads) {
+            const int cell = i % NCELL, q = i / NCELL;
+            int64_t gi;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (halo_cell(cell, gi))
+                v = make_float4(gp_prev[(4 * q + 0) * cells + gi], gp_prev[(4 * q + 1) * cells + gi],
+                                gp_prev[(4 * q + 2) * cells + gi], gp_prev[(4 * q + 3) * cells + gi]);
+            gtile[q * NCELL + cell] = v;
+        }
+    // weights in the lane's operand layouts
+    float w1a[4][8];    // [t][kc] = W1[16t + n][feature(kc, g)]
+    float w1t[2][4][4]; // [ft][t][i] = W1[16t + 4g + i][16 ft + n]
+    float w2t[4][4];    // [t][i] = W2[4g + i][16t + n] (0 for input channels)
+    v4 bias[4];         // [t][i] = b1[16t + 4g + i]
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+        for (int kc = 0; kc < 8; ++kc)
+            w1a[t][kc] = w1[(16 * t + n) * 2 * C + (kc < 4 ? 4 * g + kc : C + 4 * g + kc - 4)];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            w1t[0][t][i] = w1[(16 * t + 4 * g + i) * 2 * C + n];
+            w1t[1][t][i] = w1[(16 * t + 4 * g + i) * 2 * C + C + n];
+            w2t[t][i] = 4 * g + i < NIN ? 0.f : w2[(4 * g + i) * H + 16 * t + n];
+            bias[t][i] = b1[16 * t + 4 * g + i];
+        }
+    }
+    __syncthreads();
+
+    // ---- the wave's 16 cells ----
+    const int cl = 16 * wave + n;
+    const int tx = cl % T::TX, ty = (cl / T::TX) % T::TY, tz = cl / (T::TX * T::TY);
+    const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
+    const bool valid = x < dw && y < dh && z < dd;
+    const int centre = ((tz + (NDIM == 3 ? 1 : 0)) * HY + ty + 1) * HX + tx + 1;
+    const int64_t idx = ((int64_t)min(z, dd - 1) * dh + min(y, dh - 1)) * dw + min(x, dw - 1);
+
+    const float4 sq = tile[g][centre];
+    float f[8] = {sq.x, sq.y, sq.z, sq.w};
+    {
+        float pc[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pc[i] = conv_b[4 * g + i];
+#pragma unroll
+        for (int t = 0; t < TAPS; ++t) {
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            const float4 v = tile[g][centre + (dz * HY + dy) * HX + dx];
+            pc[0] = fmaf(conv_w[(4 * g + 0) * TAPS + t], v.x, pc[0]);
+            pc[1] = fmaf(conv_w[(4 * g + 1) * TAPS + t], v.y, pc[1]);
+            pc[2] = fmaf(conv_w[(4 * g + 2) * TAPS + t], v.z, pc[2]);
+            pc[3] = fmaf(conv_w[(4 * g + 3) * TAPS + t], v.w, pc[3]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f[4 + i] = pc[i];
+    }
+    // layer 1, recomputed
+    v4 a[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) a[t] = bias[t];
+#pragma unroll
+    for (int kc = 0; kc < 8; ++kc)
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            a[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1a[t][kc], f[kc], a[t], 0, 0, 0);
+    // G' of channels 4g..4g+3 of the cell
+    float gq[4];
+    {
+        const float4 go = *reinterpret_cast<const float4 *>(gout + idx * C + 4 * g);
+        gq[0] = go.x; gq[1] = go.y; gq[2] = go.z; gq[3] = go.w;
+    }
+    if (gp_prev != nullptr) {
+        // cell p receives K[c][t] gP[p - o_t] from each tap t
+#pragma unroll
+        for (int t = 0; t < TAPS; ++t) {
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            const float4 v = gtile[g * NCELL + centre - (dz * HY + dy) * HX - dx];
+            gq[0] = fmaf(conv_w[(4 * g + 0) * TAPS + t], v.x, gq[0]);
+            gq[1] = fmaf(conv_w[(4 * g + 1) * TAPS + t], v.y, gq[1]);
+            gq[2] = fmaf(conv_w[(4 * g + 2) * TAPS + t], v.z, gq[2]);
+            gq[3] = fmaf(conv_w[(4 * g + 3) * TAPS + t], v.w, gq[3]);
+        }
+    }
+    const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
+    float gu[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) gu[i] = (4 * g + i >= NIN && fire) ? gq[i] : 0.f;
+    // gh = W2^T gu, ga = gh [a > 0]
+    v4 ga[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        ga[t] = v4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            ga[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(w2t[t][i], gu[i], ga[t], 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) ga[t][i] = a[t][i] > 0.f ? ga[t][i] : 0.f;
+    // [gS, gP] = W1^T ga
+    v4 gsp[2];
+#pragma unroll
+    for (int ft = 0; ft < 2; ++ft) {
+        gsp[ft] = v4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                gsp[ft] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1t[ft][t][i], ga[t][i], gsp[ft], 0, 0, 0);
+    }
+    if (valid) {
+        *reinterpret_cast<float4 *>(gpart + idx * C + 4 * g) =
+            make_float4(gq[0] + gsp[0][0], gq[1] + gsp[0][1], gq[2] + gsp[0][2], gq[3] + gsp[0][3]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) gp[(4 * g + i) * cells + idx] = gsp[1][i];
+    }
+    if (gp_prev != nullptr) __syncthreads();   // every lane has read gtile
+    // records (zero for cells outside the grid: they add nothing to the sums)
+    const float vm = valid ? 1.f : 0.f;
+    *reinterpret_cast<float4 *>(rf + cl * SF + 4 * g) =
+        make_float4(vm * f[0], vm * f[1], vm * f[2], vm * f[3]);
+    *reinterpret_cast<float4 *>(rf + cl * SF + C + 4 * g) =
+        make_float4(vm * f[4], vm * f[5], vm * f[6], vm * f[7]);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        *reinterpret_cast<float4 *>(rh + cl * SH + 16 * t + 4 * g) =
+            make_float4(vm * fmaxf(a[t][0], 0.f), vm * fmaxf(a[t][1], 0.f), vm * fmaxf(a[t][2], 0.f),
+                        vm * fmaxf(a[t][3], 0.f));
+        *reinterpret_cast<float4 *>(rga + cl * SH + 16 * t + 4 * g) =
+            make_float4(vm * ga[t][0], vm * ga[t][1], vm * ga[t][2], vm * ga[t][3]);
+    }
+    *reinterpret_cast<float4 *>(rgu + cl * SQ + 4 * g) =
+        make_float4(vm * gu[0], vm * gu[1], vm * gu[2], vm * gu[3]);
+    *reinterpret_cast<float4 *>(rgp + cl * SQ + 4 * g) =
+        make_float4(vm * gsp[1][0], vm * gsp[1][1], vm * gsp[1][2], vm * gsp[1][3]);
+    __syncthreads();
+
+    // ---- the block's weight-gradient sums ----
+    float *out = partial + (int64_t)blockIdx.x * G::N;
+    auto start = [&](int o) { return accumulate ? out[o] : 0.f; };
+    // dW1 tiles (t, ft) = (wave, 0), (wave, 1): D[i][j] = sum_cells ga[16t + i] f[16ft + j]
+#pragma unroll
+    for (int ft = 0; ft < 2; ++ft) {
+        const int t = wave;
+        v4 acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = start(G::W1 + (16 * t + 4 * g + i) * 2 * C + 16 * ft + n);
+#pragma unroll 4
+        for (int k4 = 0; k4 < kWgCells / 4; ++k4) {
+            const int c = 4 * k4 + g;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(rga[c * SH + 16 * t + n], rf[c * SF + 16 * ft + n],
+                                                       acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[G::W1 + (16 * t + 4 * g + i) * 2 * C + 16 * ft + n] = acc[i];
+    }
+    // dW2 tile t = wave: D[c][j] = sum_cells gu[c] h[16t + j]
+    {
+        const int t = wave;
+        v4 acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = start(G::W2 + (4 * g + i) * H + 16 * t + n);
+#pragma unroll 4
+        for (int k4 = 0; k4 < kWgCells / 4; ++k4) {
+            const int c = 4 * k4 + g;
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(rgu[c * SQ + n], rh[c * SH + 16 * t + n], acc,
+                                                       0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[G::W2 + (4 * g + i) * H + 16 * t + n] = acc[i];
+    }
+    // db1, dconv_b (a quad of entries per job) and dconv_w (a channel quad of one tap)
+    constexpr int JB = H / 4, JC = C / 4, JK = (C / 4) * TAPS;
+    for (int job = threadIdx.x; job < JB + JC + JK; job += kBwdThreads) {
+        if (job < JB + JC) {
+            const bool isb = job < JB;
+            const float *src4 = isb ? rga + 4 * job : rgp + 4 * (job - JB);
+            const int stride = isb ? SH : SQ;
+            const int o0 = isb ? G::B1 + 4 * job : G::CB + 4 * (job - JB);
+            float sum[4] = {start(o0), start(o0 + 1), start(o0 + 2), start(o0 + 3)};
+            for (int c = 0; c < kWgCells; ++c) {
+                const float4 v = *reinterpret_cast<const float4 *>(src4 + c * stride);
+                sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[o0 + r] = sum[r];
+        } else {
+            const int jj = job - JB - JC;
+            const int cq = jj / TAPS, t = jj % TAPS;
+            const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
+            float sum[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sum[r] = start(G::CW + (4 * cq + r) * TAPS + t);
+#pragma unroll 4
+            for (int c = 0; c < kWgCells; ++c) {
+                const int px = c % T::TX, py = (c / T::TX) % T::TY, pz = c / (T::TX * T::TY);
+                const int nb = ((pz + (NDIM == 3 ? 1 : 0) + dz) * HY + py + 1 + dy) * HX + px + 1 + dx;
+                const float4 gpv = *reinterpret_cast<const float4 *>(rgp + c * SQ + 4 * cq);
+                const float4 sv = tile[cq][nb];
+                sum[0] = fmaf(gpv.x, sv.x, sum[0]);
+                sum[1] = fmaf(gpv.y, sv.y, sum[1]);
+                sum[2] = fmaf(gpv.z, sv.z, sum[2]);
+                sum[3] = fmaf(gpv.w, sv.w, sum[3]);
+            }
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[G::CW + (4 * cq + r) * TAPS + t] = sum[r];
+        }
+    }
+}
+
 template <int NDIM, int C, int H>
 __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
     const float *__restrict__ gpart, const float *__restrict__ gp, int dd, int dh, int dw,
@@ -459,6 +747,13 @@ template <int NDIM, int NIN, int C, int H>
 void enqueue_bwd_cell(const StepArgs &a, const BwdGrid<NDIM> &gr, const float *src,
                       const float *gout, const float *gp_prev, float *gpart, float *gp,
                       float *partial, bool accumulate, hipStream_t stream) {
+    if constexpr (C == 16 && H == 64) {
+        bwd_cell_mfma<NDIM, NIN><<<(unsigned)gr.cblocks, kBwdThreads, 0, stream>>>(
+            src, gout, gp_prev, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, gr.ctiles_x,
+            gr.ctiles_y, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
+            a.seed, a.threshold, gpart, gp, partial, a.ext.cells(), accumulate ? 1 : 0);
+        return;
+    }
     bwd_cell<NDIM, NIN, C, H><<<(unsigned)gr.cblocks, kBwdThreads, 0, stream>>>(
         src, gout, gp_prev, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, gr.ctiles_x, gr.ctiles_y,
         a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
