@@ -107,8 +107,9 @@ typedef enum {
  * default arithmetic) or OCTNCA_MLP_VALU only.  Combinations that no kernel
  * implements (OCTNCA_MLP_F16 with fp32 states, OCTNCA_MLP_F16S with
  * fp16 states) give OCTNCA_EUNSUPPORTED; values outside the enums give
- * OCTNCA_EINVAL.  The training entry points always use fp32 MLP operands
- * and ignore these three fields. */
+ * OCTNCA_EINVAL.  The training entry points choose their own arithmetic
+ * (split-bf16 MLP operands in the forward, fp32 in the backward) and ignore
+ * these three fields. */
 typedef struct {
     int32_t ndim;        /* 2: 3x3 taps, d must be 1; 3: 3x3x3 taps */
     int32_t channels;    /* C: state channels per cell */
@@ -387,7 +388,8 @@ size_t octree_nca_train_workspace_bytes(const octnca_model *model, octnca_extent
                                         const int32_t *steps);
 
 /* One fused training step: the inference of octree_nca_infer (same arguments,
- * fp32 MLP operands) keeping every state, the readout MSE against `target`,
+ * split-bf16 MLP operands, products to about 2^-16) keeping every state,
+ * the readout MSE against `target`,
  * and the backward through all steps and levels (finest first, the upsample's
  * adjoint between levels).
  *   grads   host array of `levels` gradient sets (index = level), OVERWRITTEN;

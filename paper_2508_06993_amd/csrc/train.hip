@@ -578,57 +578,70 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
 #pragma unroll
     for (int ft = 0; ft < 2; ++ft) {
         const int t = wave;
-        v4 acc;
+        // two interleaved chains (even and odd K chunks), added at the end
+        v4 acc, acc2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] = start(G::W1 + (16 * t + 4 * g + i) * 2 * C + 16 * ft + n);
 #pragma unroll 4
-        for (int k4 = 0; k4 < kWgCells / 4; ++k4) {
+        for (int k4 = 0; k4 < kWgCells / 4; k4 += 2) {
             const int c = 4 * k4 + g;
             acc = __builtin_amdgcn_mfma_f32_16x16x4f32(rga[c * SH + 16 * t + n], rf[c * SF + 16 * ft + n],
                                                        acc, 0, 0, 0);
+            acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(rga[(c + 4) * SH + 16 * t + n],
+                                                        rf[(c + 4) * SF + 16 * ft + n], acc2, 0, 0, 0);
         }
+        acc += acc2;
 #pragma unroll
         for (int i = 0; i < 4; ++i) out[G::W1 + (16 * t + 4 * g + i) * 2 * C + 16 * ft + n] = acc[i];
     }
     // dW2 tile t = wave: D[c][j] = sum_cells gu[c] h[16t + j]
     {
         const int t = wave;
-        v4 acc;
+        v4 acc, acc2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[i] = start(G::W2 + (4 * g + i) * H + 16 * t + n);
 #pragma unroll 4
-        for (int k4 = 0; k4 < kWgCells / 4; ++k4) {
+        for (int k4 = 0; k4 < kWgCells / 4; k4 += 2) {
             const int c = 4 * k4 + g;
             acc = __builtin_amdgcn_mfma_f32_16x16x4f32(rgu[c * SQ + n], rh[c * SH + 16 * t + n], acc,
                                                        0, 0, 0);
+            acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(rgu[(c + 4) * SQ + n],
+                                                        rh[(c + 4) * SH + 16 * t + n], acc2, 0, 0, 0);
         }
+        acc += acc2;
 #pragma unroll
         for (int i = 0; i < 4; ++i) out[G::W2 + (4 * g + i) * H + 16 * t + n] = acc[i];
     }
-    // db1, dconv_b (a quad of entries per job) and dconv_w (a channel quad of one tap)
+    // db1, dconv_b (a quad of entries per job) and dconv_w (a channel quad of
+    // one tap): four consecutive lanes per job, each summing a quarter of the
+    // cells, then the quarters added across the four lanes
     constexpr int JB = H / 4, JC = C / 4, JK = (C / 4) * TAPS;
-    for (int job = threadIdx.x; job < JB + JC + JK; job += kBwdThreads) {
+    constexpr int NJ = JB + JC + JK;
+    constexpr int QC = kWgCells / 4;
+    for (int base = 0; base < 4 * NJ; base += kBwdThreads) {
+        const int slot = base + (int)threadIdx.x;
+        const int job = min(slot / 4, NJ - 1), qtr = slot % 4;
+        float sum[4] = {0.f, 0.f, 0.f, 0.f};
+        int o[4];
         if (job < JB + JC) {
             const bool isb = job < JB;
             const float *src4 = isb ? rga + 4 * job : rgp + 4 * (job - JB);
             const int stride = isb ? SH : SQ;
             const int o0 = isb ? G::B1 + 4 * job : G::CB + 4 * (job - JB);
-            float sum[4] = {start(o0), start(o0 + 1), start(o0 + 2), start(o0 + 3)};
-            for (int c = 0; c < kWgCells; ++c) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r) o[r] = o0 + r;
+            for (int c = qtr * QC; c < (qtr + 1) * QC; ++c) {
                 const float4 v = *reinterpret_cast<const float4 *>(src4 + c * stride);
                 sum[0] += v.x; sum[1] += v.y; sum[2] += v.z; sum[3] += v.w;
             }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) out[o0 + r] = sum[r];
         } else {
             const int jj = job - JB - JC;
             const int cq = jj / TAPS, t = jj % TAPS;
             const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
-            float sum[4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) sum[r] = start(G::CW + (4 * cq + r) * TAPS + t);
+            for (int r = 0; r < 4; ++r) o[r] = G::CW + (4 * cq + r) * TAPS + t;
 #pragma unroll 4
-            for (int c = 0; c < kWgCells; ++c) {
+            for (int c = qtr * QC; c < (qtr + 1) * QC; ++c) {
                 const int px = c % T::TX, py = (c / T::TX) % T::TY, pz = c / (T::TX * T::TY);
                 const int nb = ((pz + (NDIM == 3 ? 1 : 0) + dz) * HY + py + 1 + dy) * HX + px + 1 + dx;
                 const float4 gpv = *reinterpret_cast<const float4 *>(rgp + c * SQ + 4 * cq);
@@ -638,9 +651,15 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
                 sum[2] = fmaf(gpv.z, sv.z, sum[2]);
                 sum[3] = fmaf(gpv.w, sv.w, sum[3]);
             }
-#pragma unroll
-            for (int r = 0; r < 4; ++r) out[G::CW + (4 * cq + r) * TAPS + t] = sum[r];
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            sum[r] += __shfl_xor(sum[r], 1);
+            sum[r] += __shfl_xor(sum[r], 2);
+        }
+        if (qtr == 0 && slot / 4 < NJ)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) out[o[r]] = start(o[r]) + sum[r];
     }
 }
 

@@ -7,9 +7,10 @@ Bounds (max |g - o| / max |o|): the GPU computes in fp32 what the oracle
 computes in fp64 from the same fp32 inputs.  A state gradient is a sum of a
 few dozen fp32 products per cell: 2e-5.  A weight gradient sums one product
 per cell over every cell (fp32 within chunks of 32 cells, fp64 across
-chunks): 1e-4.  The training step also differs in its forward states (fp32
-matrix-core MLP against the oracle's fp64 arithmetic rounded to fp32 per
-step), which the steps carry along: 1e-3."""
+chunks): 1e-4.  The training step also differs in its forward states (the
+matrix-core MLP with split-bf16 operands, products to about 2^-16, against
+the oracle's fp64 arithmetic rounded to fp32 per step), which the steps
+carry along: 1e-3."""
 import numpy as np
 import pytest
 import torch
