@@ -363,16 +363,25 @@ def test_fused_readout_equals_readout_of_final_state(gpu, kernel, steps):
 
 
 @pytest.mark.parametrize("steps", [(3, 2), (1, 2), (2, 3)], ids=lambda s: "s" + "-".join(map(str, s)))
-def test_fused_readout_fp16_3d(gpu, steps):
+@pytest.mark.parametrize("extent,factor", [((12, 24, 40), (1, 2, 2)), ((7, 21, 37), (1, 3, 1)),
+                                           ((5, 13, 44), (5, 1, 2)), ((9, 10, 30), (3, 2, 3))],
+                         ids=["12x24x40", "7x21x37", "5x13x44", "9x10x30"])
+def test_fused_readout_fp16_3d(gpu, steps, extent, factor):
     """fp16 3D (2D+t): the finest level's last single-step launch writes the
     readout (when it is not the level's first, upsample-fused step); it must
-    equal the readout kernel applied to the final state, byte for byte."""
-    wl = Workload(name="fused_readout_f16", ndim=3, extent=(12, 24, 40), n_in=3,
-                  factors=((1, 2, 2),), steps=steps, dtype="f16", image_kind="uniform")
-    print(f"fused readout fp16 3D steps={steps}", flush=True)
-    state, seg = gpu_infer(wl, make_image(wl), make_weights(wl))
+    equal the readout kernel applied to the final state, byte for byte.  Rows
+    of a width that is not a multiple of 8 take the unaligned kernel variant,
+    and heights that are not a multiple of 8 leave partial 8-row tiles whose
+    readout stores are clipped."""
+    wl = Workload(name="fused_readout_f16", ndim=3, extent=extent, n_in=3,
+                  factors=(factor,), steps=steps, dtype="f16", image_kind="uniform")
+    print(f"fused readout fp16 3D extent={extent} steps={steps}", flush=True)
+    image, weights = make_image(wl), make_weights(wl)
+    state, seg = gpu_infer(wl, image, weights)
     model = octnca.Model(ndim=3, n_in=3, dtype="f16")
     want = torch.empty_like(seg)
     octnca.octree_nca_readout(model, state, want)
     torch.cuda.synchronize()
     assert torch.equal(seg, want)
+    want_state, _ = oracle_infer(wl, image, weights)
+    assert_state_close(to_np(state), want_state, wl.dtype)
