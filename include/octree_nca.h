@@ -139,7 +139,8 @@ typedef struct {
                             column C + k multiplies perception channel k */
     const float *b1;     /* [H] */
     const float *w2;     /* [C][H]: row c gives the update of channel c; rows c < n_in
-                            are never read (input channels are not updated) */
+                            must be allocated but their values are ignored (read,
+                            then replaced by 0: input channels are not updated) */
 } octnca_level_weights;
 
 /* Image pyramid by node averaging (Sec. 3.2; supplement S7 table).

@@ -165,7 +165,10 @@ __global__ __launch_bounds__(kGenThreads, (kGenBlocksPerCu<NDIM, C>)) void nca_s
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
             const int f = gen_feature<C>(k, lg, s);
-            x[s] = (row < H && f >= 0) ? w1[row * 2 * C + f] : 0.f;
+            // load a valid element for every slot, then zero the padding (a
+            // load behind the condition costs a branch and a memory wait)
+            const float v = w1[min(row, H - 1) * 2 * C + max(f, 0)];
+            x[s] = (row < H && f >= 0) ? v : 0.f;
         }
         WPair wp;
         wp.hi = __builtin_convertvector(x, v8h);
@@ -178,7 +181,8 @@ __global__ __launch_bounds__(kGenThreads, (kGenBlocksPerCu<NDIM, C>)) void nca_s
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             const int j = 16 * t + 4 * lg + r;
-            b[r] = j < H ? kScale * b1[j] : 0.f;
+            const float v = b1[min(j, H - 1)];
+            b[r] = j < H ? kScale * v : 0.f;
         }
         b1s[t][lg] = make_float4(b[0], b[1], b[2], b[3]);
     }
@@ -189,7 +193,8 @@ __global__ __launch_bounds__(kGenThreads, (kGenBlocksPerCu<NDIM, C>)) void nca_s
 #pragma unroll
         for (int s = 0; s < 8; ++s) {
             const int j = gen_hidden(p, lg, s);
-            x[s] = (ch >= NIN && ch < C && j < H) ? w2[ch * H + j] * (1.f / kScale) : 0.f;
+            const float v = w2[min(ch, C - 1) * H + min(j, H - 1)];
+            x[s] = (ch >= NIN && ch < C && j < H) ? v * (1.f / kScale) : 0.f;
         }
         WPair wp;
         wp.hi = __builtin_convertvector(x, v8h);

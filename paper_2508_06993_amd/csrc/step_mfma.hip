@@ -74,8 +74,11 @@ __device__ __forceinline__ void pin(V &x) {
 // accumulate in fp32.  The second layer has outputs for the hidden channels
 // only (Sec. 3.1): load() gathers the W2 rows of the nin input channels as
 // zeros, so their update is exactly +0 and the residual needs no per-channel
-// mask.  kPerceptionScale: the factor the kernel applies to the perception
-// weights and bias (features 4..7 arrive multiplied by it).
+// mask.  Those rows are loaded like the others and then replaced by zero: a
+// load behind the lane condition became a branch and a full memory wait per
+// element (16 round trips, about 5 us per launch, measured).
+// kPerceptionScale: the factor the kernel applies to the perception weights
+// and bias (features 4..7 arrive multiplied by it).
 // ---------------------------------------------------------------------------
 
 // ReLU as an integer max on the float's bits: negative floats (sign bit set)
@@ -111,7 +114,8 @@ struct MlpF32 {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 b1[jt][i] = B1[jt * 16 + 4 * g + i];
-                w2[jt][i] = n < nin ? 0.f : W2[n * kH + jt * 16 + 4 * g + i];
+                const float v = W2[n * kH + jt * 16 + 4 * g + i];   // loaded for every n
+                w2[jt][i] = n < nin ? 0.f : v;
             }
         }
     }
@@ -213,7 +217,10 @@ struct MlpBf16x3 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = n < nin ? 0.f : W2[n * kH + hidden_of(p, s, g)];
+            for (int s = 0; s < 8; ++s) {
+                const float v = W2[n * kH + hidden_of(p, s, g)];   // loaded for every n
+                x[s] = n < nin ? 0.f : v;
+            }
             split_bf16(x, w2h[p], w2l[p]);
         }
     }
@@ -292,8 +299,10 @@ struct MlpF16 {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                x[s] = n < nin ? 0.f : W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];
+            for (int s = 0; s < 8; ++s) {
+                const float v = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];   // loaded for every n
+                x[s] = n < nin ? 0.f : v;
+            }
             w2[p] = __builtin_convertvector(x, v8h);
         }
     }
@@ -379,8 +388,10 @@ struct MlpF16S {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s)
-                x[s] = n < nin ? 0.f : W2[n * kH + MlpBf16x3::hidden_of(p, s, g)] * (1.f / kF16ActScale);
+            for (int s = 0; s < 8; ++s) {
+                const float v = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];   // loaded for every n
+                x[s] = n < nin ? 0.f : v * (1.f / kF16ActScale);
+            }
             split(x, w2h[p], w2l[p]);
         }
     }

@@ -457,7 +457,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
         for (int i = 0; i < 4; ++i) {
             w1t[0][t][i] = w1[(16 * t + 4 * g + i) * 2 * C + n];
             w1t[1][t][i] = w1[(16 * t + 4 * g + i) * 2 * C + C + n];
-            w2t[t][i] = 4 * g + i < NIN ? 0.f : w2[(4 * g + i) * H + 16 * t + n];
+            const float v2 = w2[(4 * g + i) * H + 16 * t + n];   // loaded for every row
+            w2t[t][i] = 4 * g + i < NIN ? 0.f : v2;
             bias[t][i] = b1[16 * t + 4 * g + i];
         }
     }

@@ -313,6 +313,42 @@ def test_fire_rate_zero_and_zero_w2_are_identity(gpu, step_kernel, ndim):
     np.testing.assert_array_equal(got, s)
 
 
+@pytest.mark.parametrize("dt,ndim,n_in,shape", [("f32", 2, 3, (1, 30, 70)),
+                                                ("f32", 3, 1, (6, 20, 40)),
+                                                ("f16", 3, 3, (8, 12, 40)),
+                                                ("f16", 2, 1, (1, 20, 50))])
+def test_input_rows_of_w2_are_ignored(gpu, step_kernel, dt, ndim, n_in, shape):
+    """The W2 rows of the input channels are part of the [C][H] array but
+    their values never reach the state: the kernels read them and replace them
+    by zero, so NaN there gives the same bits as zeros."""
+    rng = np.random.default_rng(21)
+    w = rand_weights(rng, ndim)
+    s = rng.normal(0, 1, shape + (C,)).astype(NP_DT[dt])
+    m = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, kernel=step_kernel)
+    w.w2[:n_in] = 0
+    ref, _ = run_level_gpu(m, s, w, 1, 3, 0.5, 8)
+    w.w2[:n_in] = np.nan
+    got, _ = run_level_gpu(m, s, w, 1, 3, 0.5, 8)
+    np.testing.assert_array_equal(got, ref)
+    assert np.isfinite(got).all()
+
+
+@pytest.mark.parametrize("kernel", ["mfma", "valu"])
+@pytest.mark.parametrize("dt,ndim,n_in,c,h", [("f32", 2, 3, 12, 48), ("f16", 3, 1, 20, 100)])
+def test_input_rows_of_w2_are_ignored_other_sizes(gpu, kernel, dt, ndim, n_in, c, h):
+    rng = np.random.default_rng(22)
+    w = rand_weights(rng, ndim, c=c, h=h)
+    shape = (1, 19, 40) if ndim == 2 else (5, 9, 36)
+    s = rng.normal(0, 1, shape + (c,)).astype(NP_DT[dt])
+    m = octnca.Model(ndim=ndim, n_in=n_in, dtype=dt, channels=c, hidden=h, kernel=kernel)
+    w.w2[:n_in] = 0
+    ref, _ = run_level_gpu(m, s, w, 1, 3, 0.5, 8)
+    w.w2[:n_in] = np.nan
+    got, _ = run_level_gpu(m, s, w, 1, 3, 0.5, 8)
+    np.testing.assert_array_equal(got, ref)
+    assert np.isfinite(got).all()
+
+
 def test_translation_equivariance_on_gpu(gpu, step_kernel):
     """With every cell firing, shifting the input shifts the output (cells far
     enough from the border)."""
