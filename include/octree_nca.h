@@ -91,9 +91,11 @@ typedef enum {
 /* Work layout of the 2D matrix-core step (octnca_model.layout2d); results do
  * not depend on it.  3D steps ignore it. */
 typedef enum {
-    OCTNCA_LAYOUT_AUTO = 0,  /* row streaming on levels of >= 2048 work items, tiles below */
-    OCTNCA_LAYOUT_ROWS = 1,  /* strips of 32 (30 for two steps) cells streamed over 128-row runs */
-    OCTNCA_LAYOUT_TILES = 2  /* 16 x 32 cell tiles */
+    OCTNCA_LAYOUT_AUTO = 0,  /* strips of 32 cells streamed over runs of 128 rows, shorter runs
+                                (down to 2 rows) on levels with fewer than 2048 such runs; two
+                                steps per launch (strips of 30) on levels with >= 2048 of those */
+    OCTNCA_LAYOUT_ROWS = 1,  /* as AUTO, with two steps per launch wherever that kernel applies */
+    OCTNCA_LAYOUT_TILES = 2  /* 16 x 32 cell tiles, one step per launch */
 } octnca_layout;
 
 /* Architecture of one NCA (all levels share it; supplement S3 fixes C and H

@@ -2140,17 +2140,23 @@ int device_cus() {
 
 constexpr int kBlocksPerCu = 2;
 
-// Work layout of a 2D level.  Large levels: row streaming over strips of 32
-// cells and runs of k2RunRows rows, once there is at least one run per wave
-// slot of a full MI355X (256 CUs x 4 SIMDs x 2 waves).  Small levels: 16 x 32
-// tiles, where the per-run start-up of the row kernel (two rows loaded and
-// waited for) would not be amortised.  The choice uses that fixed slot count,
-// not the device's, so the launch sequence (and with it the buffer that holds
-// a result) is the same on every device; only grid sizes follow the device.
+// Work layout of a 2D level: row streaming over strips of 32 cells (the 16 x
+// 32 tile kernel only when asked for).  A work item is a run of k2RunRows
+// rows where the level has at least one such run per wave slot of a full
+// MI355X (256 CUs x 4 SIMDs x 2 waves); smaller levels take shorter runs (down
+// to 2 rows) so that they still spread over about that many waves: they are
+// bound by the latency of a wave's rows, not by throughput, and the extra halo
+// rows of short runs cost less than idle SIMDs (measured: medium 2D pass 1.43
+// -> 1.35 ms, tiny 2D 0.285 -> 0.223 ms against 16 x 32 tiles; the row kernel
+// sums the taps in the tile kernel's order, so the results are the same bits).
+// The plan uses that fixed slot count, not the device's, so the launch
+// sequence (and with it the buffer that holds a result) is the same on every
+// device; only grid sizes follow the device.
 constexpr int64_t kPlanSlots = 256 * 4 * k2WavesPerSimd;
 
 struct RowsPlan {
     int tiles_x;
+    int run;                      // rows per work item
     int64_t runs, items, slots;   // slots: wave slots of this device (grid size)
 };
 
@@ -2158,15 +2164,14 @@ RowsPlan rows_plan(const StepArgs &a) {
     RowsPlan r;
     r.tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     r.slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
-    r.runs = (a.ext.h + k2RunRows - 1) / k2RunRows;
+    r.run = (int)std::min<int64_t>(
+        k2RunRows, std::max<int64_t>(2, (a.ext.h * r.tiles_x + kPlanSlots - 1) / kPlanSlots));
+    r.runs = (a.ext.h + r.run - 1) / r.run;
     r.items = (int64_t)r.tiles_x * r.runs;
     return r;
 }
 
-bool uses_rows(const StepArgs &a, Layout2d layout) {
-    return layout == Layout2d::Rows ||
-           (layout == Layout2d::Auto && rows_plan(a).items >= kPlanSlots);
-}
+bool uses_rows(const StepArgs &, Layout2d layout) { return layout != Layout2d::Tiles; }
 
 // Row kernel launch; UP: the first step of a level fused with the upsample
 // from the coarse state src (width cdw) by (fy, fx) and the image img.
@@ -2180,7 +2185,7 @@ hipError_t launch_rows(const StepArgs &a, const void *src, void *dst, const void
     auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_2d_rows<T, NIN, Mlp, true, UP>
                                  : nca_step_mfma_2d_rows<T, NIN, Mlp, false, UP>;
     kern<<<grid, 64, 0, stream>>>(
-        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, (int)r.runs, k2RunRows,
+        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, (int)r.runs, r.run,
         (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
         a.seed, a.threshold, (const T *)img, cdw, fy, fx);
     return hipGetLastError();
