@@ -848,9 +848,11 @@ int octree_nca_train_step(const octnca_model *model, const void *image, octnca_e
         !ok(hipMemcpyAsync(final_state, final_fine, state_bytes, hipMemcpyDeviceToDevice, s)))
         return OCTNCA_EHIP;
 
-    // backward, finest level first
+    // backward, finest level first; a level's backward writes its weight
+    // gradients, so only levels without steps are cleared here
     const int taps = model->ndim == 3 ? 27 : 9;
     for (int l = 0; l < levels; ++l) {
+        if (steps[l] > 0) continue;
         const int64_t c = model->channels, h = model->hidden;
         const octnca_level_grads &gr = grads[l];
         if (!ok(launch_fill_zero(gr.conv_w, c * taps, s)) || !ok(launch_fill_zero(gr.conv_b, c, s)) ||

@@ -102,9 +102,10 @@ hipError_t launch_step_backward(const StepArgs &a, const float *src, const float
 // Backward of all `steps` steps of a level (a.step unused): states holds the
 // level's states before steps 0 .. steps-1 (state t at states + t * cells * C),
 // gout = dL/dS after the last step; gin receives dL/dS of the level's first
-// state (must not alias gout or states) and the weight gradients are added to
-// g.  ws holds level_backward_workspace_floats floats.  steps = 0 enqueues
-// nothing (gin is not written).
+// state (must not alias gout or states) and g receives the level's weight
+// gradients (written, not added: the buffers need no clearing).  ws holds
+// level_backward_workspace_floats floats.  steps = 0 enqueues nothing (neither
+// gin nor g is written).
 size_t level_backward_workspace_floats(int ndim, int channels, int hidden, Extent3 extent);
 hipError_t launch_level_backward(const StepArgs &a, int32_t steps, const float *states,
                                  const float *gout, float *gin, LevelGradsDev g, float *ws,

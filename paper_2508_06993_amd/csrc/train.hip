@@ -722,7 +722,8 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_conv_t(
 constexpr int kRedWaves = 16;
 template <int C, int H, int TAPS>
 __global__ __launch_bounds__(64 * kRedWaves) void wgrad_reduce(const float *__restrict__ partial,
-                                                               int64_t blocks, LevelGradsDev g) {
+                                                               int64_t blocks, LevelGradsDev g,
+                                                               int overwrite) {
     using G = WG<C, H, TAPS>;
     __shared__ double red[kRedWaves][64];
     const int lane = threadIdx.x & 63, w = (int)(threadIdx.x >> 6);
@@ -743,7 +744,7 @@ __global__ __launch_bounds__(64 * kRedWaves) void wgrad_reduce(const float *__re
     else if (o < G::CB) dst = g.b1 + (o - G::B1);
     else if (o < G::CW) dst = g.conv_b + (o - G::CB);
     else dst = g.conv_w + (o - G::CW);
-    *dst = (float)((double)*dst + t);
+    *dst = overwrite ? (float)t : (float)((double)*dst + t);
 }
 
 // Block counts of the two backward tilings of a level.
@@ -782,13 +783,14 @@ void enqueue_bwd_cell(const StepArgs &a, const BwdGrid<NDIM> &gr, const float *s
 
 template <int NDIM, int C, int H>
 void enqueue_tail(const StepArgs &a, const BwdGrid<NDIM> &gr, const float *gpart, const float *gp,
-                  float *gin, const float *partial, LevelGradsDev g, hipStream_t stream) {
+                  float *gin, const float *partial, LevelGradsDev g, bool overwrite,
+                  hipStream_t stream) {
     constexpr int TAPS = NDIM == 3 ? 27 : 9;
     bwd_conv_t<NDIM, C, H><<<(unsigned)gr.blocks, kBwdThreads, 0, stream>>>(
         gpart, gp, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, gr.tiles_x, gr.tiles_y, a.w.conv_w,
         gin, a.ext.cells());
     wgrad_reduce<C, H, TAPS><<<(WG<C, H, TAPS>::N + 63) / 64, 64 * kRedWaves, 0, stream>>>(
-        partial, gr.cblocks, g);
+        partial, gr.cblocks, g, overwrite ? 1 : 0);
 }
 
 // One step: bwd_cell, bwd_conv_t, wgrad_reduce.
@@ -803,7 +805,7 @@ hipError_t launch_bwd(const StepArgs &a, const float *src, const float *gout, fl
     float *partial = gp + cells * C;   // [cblocks][entries]
     enqueue_bwd_cell<NDIM, NIN, C, H>(a, gr, src, gout, nullptr, gpart, gp, partial, false,
                                       stream);
-    enqueue_tail<NDIM, C, H>(a, gr, gpart, gp, gin, partial, g, stream);
+    enqueue_tail<NDIM, C, H>(a, gr, gpart, gp, gin, partial, g, false, stream);
     return hipGetLastError();
 }
 
@@ -832,7 +834,7 @@ hipError_t launch_bwd_level(const StepArgs &a0, int32_t steps, const float *stat
                                           partial, !first, stream);
         cur ^= 1;
     }
-    enqueue_tail<NDIM, C, H>(a, gr, gpart[cur ^ 1], gp[cur ^ 1], gin, partial, g, stream);
+    enqueue_tail<NDIM, C, H>(a, gr, gpart[cur ^ 1], gp[cur ^ 1], gin, partial, g, true, stream);
     return hipGetLastError();
 }
 
@@ -912,12 +914,20 @@ __global__ __launch_bounds__(256) void mse_grad(const float *__restrict__ state,
     if (threadIdx.x == 0) block_loss[blockIdx.x] = part[0];
 }
 
-__global__ __launch_bounds__(64) void sum_losses(const double *__restrict__ block_loss,
-                                                 int64_t blocks, double *__restrict__ loss) {
-    if (threadIdx.x != 0) return;
+// Sum of the block partials in a fixed order (thread t sums partials t,
+// t + 256, ...; then a tree over the threads), so the loss is deterministic.
+__global__ __launch_bounds__(256) void sum_losses(const double *__restrict__ block_loss,
+                                                  int64_t blocks, double *__restrict__ loss) {
+    __shared__ double part[256];
     double s = 0.0;
-    for (int64_t b = 0; b < blocks; ++b) s += block_loss[b];
-    *loss = s;
+    for (int64_t b = threadIdx.x; b < blocks; b += 256) s += block_loss[b];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int k = 128; k > 0; k >>= 1) {
+        if ((int)threadIdx.x < k) part[threadIdx.x] += part[threadIdx.x + k];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) *loss = part[0];
 }
 
 __global__ __launch_bounds__(256) void fill_zero(float *__restrict__ p, int64_t n) {
@@ -975,7 +985,7 @@ hipError_t launch_readout_mse(const float *state, const float *target, int64_t c
     const int64_t blocks = (cells + 255) / 256;
     if (blocks > 0)
         mse_grad<<<(unsigned)blocks, 256, 0, stream>>>(state, target, cells, channels, grad, ws);
-    sum_losses<<<1, 64, 0, stream>>>(ws, blocks, loss);
+    sum_losses<<<1, 256, 0, stream>>>(ws, blocks, loss);
     return hipGetLastError();
 }
 
