@@ -92,7 +92,7 @@ typedef enum {
  * not depend on it.  3D steps ignore it. */
 typedef enum {
     OCTNCA_LAYOUT_AUTO = 0,  /* strips of 32 cells streamed over runs of 128 rows, shorter runs
-                                (down to 2 rows) on levels with fewer than 2048 such runs; two
+                                (down to 2 rows) on levels with fewer than 1024 such runs; two
                                 steps per launch (strips of 30) on levels with >= 2048 of those */
     OCTNCA_LAYOUT_ROWS = 1,  /* as AUTO, with two steps per launch wherever that kernel applies */
     OCTNCA_LAYOUT_TILES = 2  /* 16 x 32 cell tiles, one step per launch */

@@ -2142,17 +2142,21 @@ constexpr int kBlocksPerCu = 2;
 
 // Work layout of a 2D level: row streaming over strips of 32 cells (the 16 x
 // 32 tile kernel only when asked for).  A work item is a run of k2RunRows
-// rows where the level has at least one such run per wave slot of a full
-// MI355X (256 CUs x 4 SIMDs x 2 waves); smaller levels take shorter runs (down
-// to 2 rows) so that they still spread over about that many waves: they are
-// bound by the latency of a wave's rows, not by throughput, and the extra halo
-// rows of short runs cost less than idle SIMDs (measured: medium 2D pass 1.43
-// -> 1.35 ms, tiny 2D 0.285 -> 0.223 ms against 16 x 32 tiles; the row kernel
-// sums the taps in the tile kernel's order, so the results are the same bits).
-// The plan uses that fixed slot count, not the device's, so the launch
-// sequence (and with it the buffer that holds a result) is the same on every
-// device; only grid sizes follow the device.
+// rows where the level has at least one such run per SIMD of a full MI355X
+// (256 CUs x 4 SIMDs); smaller levels take shorter runs (down to 2 rows) so
+// that they still spread over about that many waves: they are bound by the
+// latency of a wave's rows, not by throughput, and the extra halo rows of
+// short runs cost less than idle SIMDs.  Measured against 16 x 32 tiles:
+// medium 2D pass 1.43 -> 1.25 ms, tiny 2D 0.285 -> 0.22 ms, training step
+// 3.20 -> 3.07 ms; aiming at one run per wave slot (2 per SIMD) or at half a
+// run per SIMD was slower.  The row kernel sums the taps in the tile
+// kernel's order, so the results are the same bits.  Two steps per launch
+// need at least one two-step run per wave slot (kPlanSlots).  Both counts are
+// those of a full MI355X, not the device's, so the launch sequence (and with
+// it the buffer that holds a result) is the same on every device; only grid
+// sizes follow the device.
 constexpr int64_t kPlanSlots = 256 * 4 * k2WavesPerSimd;
+constexpr int64_t kRowRuns = 256 * 4;
 
 struct RowsPlan {
     int tiles_x;
@@ -2165,7 +2169,7 @@ RowsPlan rows_plan(const StepArgs &a) {
     r.tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     r.slots = (int64_t)device_cus() * 4 * k2WavesPerSimd;
     r.run = (int)std::min<int64_t>(
-        k2RunRows, std::max<int64_t>(2, (a.ext.h * r.tiles_x + kPlanSlots - 1) / kPlanSlots));
+        k2RunRows, std::max<int64_t>(2, (a.ext.h * r.tiles_x + kRowRuns - 1) / kRowRuns));
     r.runs = (a.ext.h + r.run - 1) / r.run;
     r.items = (int64_t)r.tiles_x * r.runs;
     return r;
