@@ -399,6 +399,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
     typedef float v4 __attribute__((ext_vector_type(4)));
 
     __shared__ float4 tile[4][NCELL];       // S, channel quads
+    __shared__ float4 kw[TAPS][4];          // [tap][quad] conv weights of channels 4q..4q+3
+    __shared__ float4 kb[4];                // conv bias of channel quad q
     // records: f [64][SF], h and ga [64][SH], gu and gP [64][SQ]; the gp_prev
     // tile (fused G') lives in the same space before the records are written
     __shared__ __align__(16) float recs[kWgCells * (SF + 2 * SH + 2 * SQ)];
@@ -418,6 +420,18 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
     const int by = b % tiles_y;
     const int bz = b / tiles_y;
     const int x0 = bx * T::TX, y0 = by * T::TY, z0 = bz * T::TZ;
+
+    // The wave's 16 cells (one per lane n; lane group g owns channels
+    // 4g..4g+3).  Their G' entries and fire bits do not depend on the tiles
+    // below: the load is issued and the fire bit computed first, so both
+    // overlap the tile loads instead of stalling the cell's chain later.
+    const int cl = 16 * wave + n;
+    const int tx = cl % T::TX, ty = (cl / T::TX) % T::TY, tz = cl / (T::TX * T::TY);
+    const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
+    const bool valid = x < dw && y < dh && z < dd;
+    const int64_t idx = ((int64_t)min(z, dd - 1) * dh + min(y, dh - 1)) * dw + min(x, dw - 1);
+    const float4 go = *reinterpret_cast<const float4 *>(gout + idx * C + 4 * g);
+    const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
 
     // S (and gp_prev) tiles with a one-cell halo, zero outside the grid
     auto halo_cell = [&](int cell, int64_t &gidx) {
@@ -443,6 +457,16 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
                                 gp_prev[(4 * q + 2) * cells + gi], gp_prev[(4 * q + 3) * cells + gi]);
             gtile[q * NCELL + cell] = v;
         }
+    // conv weights and bias into LDS (a tap's weights are one 16-byte read
+    // per lane there, instead of four global reads inside the tap loops)
+    for (int i = threadIdx.x; i < TAPS * 4; i += kBwdThreads) {
+        const int t = i / 4, q = i % 4;
+        kw[t][q] = make_float4(conv_w[(4 * q + 0) * TAPS + t], conv_w[(4 * q + 1) * TAPS + t],
+                               conv_w[(4 * q + 2) * TAPS + t], conv_w[(4 * q + 3) * TAPS + t]);
+    }
+    if (threadIdx.x < 4)
+        kb[threadIdx.x] = make_float4(conv_b[4 * threadIdx.x + 0], conv_b[4 * threadIdx.x + 1],
+                                      conv_b[4 * threadIdx.x + 2], conv_b[4 * threadIdx.x + 3]);
     // weights in the lane's operand layouts
     float w1a[4][8];    // [t][kc] = W1[16t + n][feature(kc, g)]
     float w1t[2][4][4]; // [ft][t][i] = W1[16t + 4g + i][16 ft + n]
@@ -465,27 +489,22 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
     __syncthreads();
 
     // ---- the wave's 16 cells ----
-    const int cl = 16 * wave + n;
-    const int tx = cl % T::TX, ty = (cl / T::TX) % T::TY, tz = cl / (T::TX * T::TY);
-    const int x = x0 + tx, y = y0 + ty, z = z0 + tz;
-    const bool valid = x < dw && y < dh && z < dd;
     const int centre = ((tz + (NDIM == 3 ? 1 : 0)) * HY + ty + 1) * HX + tx + 1;
-    const int64_t idx = ((int64_t)min(z, dd - 1) * dh + min(y, dh - 1)) * dw + min(x, dw - 1);
 
     const float4 sq = tile[g][centre];
     float f[8] = {sq.x, sq.y, sq.z, sq.w};
     {
-        float pc[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) pc[i] = conv_b[4 * g + i];
+        const float4 cb = kb[g];
+        float pc[4] = {cb.x, cb.y, cb.z, cb.w};
 #pragma unroll
         for (int t = 0; t < TAPS; ++t) {
             const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
             const float4 v = tile[g][centre + (dz * HY + dy) * HX + dx];
-            pc[0] = fmaf(conv_w[(4 * g + 0) * TAPS + t], v.x, pc[0]);
-            pc[1] = fmaf(conv_w[(4 * g + 1) * TAPS + t], v.y, pc[1]);
-            pc[2] = fmaf(conv_w[(4 * g + 2) * TAPS + t], v.z, pc[2]);
-            pc[3] = fmaf(conv_w[(4 * g + 3) * TAPS + t], v.w, pc[3]);
+            const float4 w = kw[t][g];
+            pc[0] = fmaf(w.x, v.x, pc[0]);
+            pc[1] = fmaf(w.y, v.y, pc[1]);
+            pc[2] = fmaf(w.z, v.z, pc[2]);
+            pc[3] = fmaf(w.w, v.w, pc[3]);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) f[4 + i] = pc[i];
@@ -500,24 +519,20 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
         for (int t = 0; t < 4; ++t)
             a[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(w1a[t][kc], f[kc], a[t], 0, 0, 0);
     // G' of channels 4g..4g+3 of the cell
-    float gq[4];
-    {
-        const float4 go = *reinterpret_cast<const float4 *>(gout + idx * C + 4 * g);
-        gq[0] = go.x; gq[1] = go.y; gq[2] = go.z; gq[3] = go.w;
-    }
+    float gq[4] = {go.x, go.y, go.z, go.w};
     if (gp_prev != nullptr) {
         // cell p receives K[c][t] gP[p - o_t] from each tap t
 #pragma unroll
         for (int t = 0; t < TAPS; ++t) {
             const int dz = NDIM == 3 ? t / 9 - 1 : 0, dy = (t / 3) % 3 - 1, dx = t % 3 - 1;
             const float4 v = gtile[g * NCELL + centre - (dz * HY + dy) * HX - dx];
-            gq[0] = fmaf(conv_w[(4 * g + 0) * TAPS + t], v.x, gq[0]);
-            gq[1] = fmaf(conv_w[(4 * g + 1) * TAPS + t], v.y, gq[1]);
-            gq[2] = fmaf(conv_w[(4 * g + 2) * TAPS + t], v.z, gq[2]);
-            gq[3] = fmaf(conv_w[(4 * g + 3) * TAPS + t], v.w, gq[3]);
+            const float4 w = kw[t][g];
+            gq[0] = fmaf(w.x, v.x, gq[0]);
+            gq[1] = fmaf(w.y, v.y, gq[1]);
+            gq[2] = fmaf(w.z, v.z, gq[2]);
+            gq[3] = fmaf(w.w, v.w, gq[3]);
         }
     }
-    const bool fire = cell_fires(seed, level, step, batch, (uint64_t)idx, threshold);
     float gu[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) gu[i] = (4 * g + i >= NIN && fire) ? gq[i] : 0.f;
