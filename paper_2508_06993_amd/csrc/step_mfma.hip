@@ -1306,7 +1306,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
 // Step t + 1 folds those rows into its own rolling sums and finishes cells
 // x0 .. x0 + 31, of which x0 .. x0 + 29 are stored (the last two lack their
 // right neighbours).  Per input row q: step t folds q and finishes q - 1, then
-// step t + 1 folds q - 1 and finishes q - 2.  The state between the two steps
+// step t + 1 folds q - 1; its row q - 2, complete then, is finished in the
+// next row's body, next to step t's fold.  The state between the two steps
 // never reaches HBM, so HBM sees one read and one write of the state per two
 // steps, for 32/30 of the MLP work and 2 halo rows of step t per run; the
 // results equal two single-step launches bit for bit (the same operations in
@@ -1604,13 +1605,16 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 up_cy += ++up_ry == up_fy ? 1 : 0;
                 up_ry = up_ry == up_fy ? 0 : up_ry;
             }
-            // input row q: outputs q + 1, q, q - 1 of step t
+            // input row q: outputs q + 1, q, q - 1 of step t; next to it
+            // (independent, so the matrix cores overlap the fold's FMAs) step
+            // t + 1's row q - 3, whose sum the previous body completed (B[j]
+            // is restarted by this body's second fold)
             fold(ring[j] + g * RS::PS, A[jp], A[j], A[jm]);
+            finish_b(q - 3, B[j]);
             finish_a(q - 1, jm, A[jm]);
             __builtin_amdgcn_sched_barrier(0);
             // step t's row q - 1: outputs q, q - 1, q - 2 of step t + 1
             fold(mid[(q - 1 - base) & 1] + g * RS::PS, B[j], B[jm], B[jp]);
-            finish_b(q - 2, B[jp]);
             __builtin_amdgcn_sched_barrier(0);
             commit(ra, ia, ring[jm]);
         };
@@ -1622,11 +1626,13 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             for (int grp = 0; grp < 2; ++grp)
 #pragma unroll
                 for (int k = 0; k < 4; ++k) A[i][grp][k] = B[i][grp][k] = cb[k];
-        for (int q0 = base; q0 <= y_end + 1; q0 += 3) {
+        int q0 = base;
+        for (; q0 <= y_end + 1; q0 += 3) {
             body(q0, std::integral_constant<int, 0>{});
             body(q0 + 1, std::integral_constant<int, 1>{});
             body(q0 + 2, std::integral_constant<int, 2>{});
         }
+        finish_b(q0 - 3, B[0]);   // the last body's deferred row
     }
 }
 
