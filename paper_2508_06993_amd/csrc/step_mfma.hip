@@ -1638,7 +1638,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
 
 // ---------------------------------------------------------------------------
 // 3D: a work item is an 8 x 32 (y, x) column and a run of `zrun` output
-// planes (32, or fewer on levels with too few columns to fill the chip).  Input planes stream through a ring of three LDS plane slots
+// planes (up to k3ZRun; the launch picks it with a load model).  Input planes
+// stream through a ring of three LDS plane slots
 // (planes p - 1 and p are in use while p + 1 is written).  Each input plane p
 // is read once: its 9 in-plane taps feed three rolling perception sums, for
 // outputs p + 1 (the dz = -1 weights), p (dz = 0) and p - 1 (dz = +1).  After
@@ -1648,7 +1649,12 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
 // read once per wave and applied to all 4 groups.
 // ---------------------------------------------------------------------------
 constexpr int k3TY = 8;
-constexpr int k3ZRun = 32;    // output planes per work item (longest run)
+// Longest run of output planes per work item.  A run re-reads two halo planes,
+// so long runs on deep levels stream less; its fire words (one evaluation per
+// 4 or 8 planes) take k3ZRun / 4 x 64 B of LDS per wave.  128 keeps the fp16
+// step at 3 blocks per CU (44 KB each) and the fp32 one at 2 (78 KB); against
+// 32 it took the video pass 89.0 -> 85.3 ms (64: 86.9 ms).
+constexpr int k3ZRun = 128;
 // Work item i of a 3D step is tile (tx, ty) of z run zr, with
 // i = (zr * tiles_y + ty) * tiles_x + tx.
 
