@@ -1874,6 +1874,13 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ h2 as_h2(uint32_t u) { return __builtin_bit_cast(h2, u); }
+// (mask & a) | (~mask & b) in one instruction (the compiler builds it from
+// two ands, an and-or and the mask's complement)
+__device__ __forceinline__ uint32_t bfi(uint32_t mask, uint32_t a, uint32_t b) {
+    uint32_t r;
+    asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(r) : "v"(mask), "v"(a), "v"(b));
+    return r;
+}
 __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 
 constexpr int k3hBlocksPerCu = 3;
@@ -2073,8 +2080,9 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
             const uint2 *own = ring[jm];
-            uint64_t fw_lane = 0;
-            if constexpr (ALIGNED) fw_lane = fwe[n & 7];
+            // ALIGNED: the bits of the lane's 4 cells of this plane, at 2 grp
+            uint32_t fw_lane = 0;
+            if constexpr (ALIGNED) fw_lane = (uint32_t)(fwe[n & 7] >> (slot0 * opr + (n >> 3)));
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const uint2 sp = own[centre[grp]];
@@ -2085,16 +2093,18 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                 mlp.layer1_h(fh, acc);
                 const v4f u = mlp.layer2(acc);
                 const int r = grp >> 1;
-                bool fires;
+                // all ones when the cell fires, else zero
+                uint32_t keep_new;
                 if constexpr (ALIGNED) {
-                    // cell n of the group is cell n % 8 of block (grp & 1) * 2 + n / 8 of its row
-                    fires = (fw_lane >> ((slot0 + r) * opr + (grp & 1) * 2 + (n >> 3))) & 1;
+                    // cell n of the group is cell n % 8 of block (grp & 1) * 2 + n / 8 of its
+                    // row: bit (r * opr + (grp & 1) * 2) of fw_lane, i.e. bit 2 grp
+                    keep_new = (uint32_t)__builtin_amdgcn_sbfe((int)fw_lane, 2 * grp, 1);
                 } else {
                     const int y = y0 + 2 * wave + r, x = x0 + (grp & 1) * 16 + n;
                     const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
                     const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
                     const uint64_t fw = fwe[idx & 7];
-                    fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
+                    keep_new = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1 ? ~0u : 0u;
                 }
                 const uint32_t off = offs[grp];
                 // state + update in fp32, rounded once to fp16 (u = +0 keeps an
@@ -2105,7 +2115,7 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
                                 (_Float16)fmaf(one, u[1], (float)s01[1])};
                 const h2 n23 = {(_Float16)fmaf(one, u[2], (float)s23[0]),
                                 (_Float16)fmaf(one, u[3], (float)s23[1])};
-                const v2u out = {fires ? as_u32(n01) : sp.x, fires ? as_u32(n23) : sp.y};
+                const v2u out = {bfi(keep_new, as_u32(n01), sp.x), bfi(keep_new, as_u32(n23), sp.y)};
                 __builtin_amdgcn_raw_buffer_store_b64(out, wr, off, 0, 0);
                 if constexpr (SEG) {
                     // lanes of quad 3: out[1] holds channels 14 (low) and 15 (high)
