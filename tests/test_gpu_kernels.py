@@ -291,6 +291,52 @@ def test_other_model_sizes_match_oracle(gpu, kernel, dt, ndim, n_in, c, h, shape
     assert max_rel_err(got9, want9) <= STEP_TOL[(dt, kernel)][1]
 
 
+def oracle_window_steps(s, w, n_in, ndim, level, steps, seed, rate, dt, box):
+    """The oracle's ``steps`` steps of the cells in ``box`` ((z0, z1), (y0, y1),
+    (x0, x1)) of the level held in ``s``, from a window that adds ``steps``
+    halo cells on every side away from the level's border (light cone)."""
+    grid = s.shape[:3]
+    lo = [max(0, a - steps) for a, _ in box]
+    hi = [min(n, b + steps) for (_, b), n in zip(box, grid)]
+    win = s[lo[0]:hi[0], lo[1]:hi[1], lo[2]:hi[2]]
+    for t in range(steps):
+        win = oracle.nca_step(win, w, n_in, ndim, level, t, seed, rate, NP_DT[dt],
+                              origin=tuple(lo), grid=grid)
+    return win[tuple(slice(a - l, b - l) for (a, b), l in zip(box, lo))]
+
+
+@pytest.mark.parametrize("dt,extent", [("f16", (300, 8, 24572)), ("f16", (300, 8, 24576)),
+                                       ("f32", (300, 8, 24572))])
+def test_long_3d_runs_match_oracle_on_windows(gpu, dt, extent):
+    """Levels deep and wide enough that the 3D step streams runs of more than
+    32 output planes (the launch's load model picks about 100 planes for fp16
+    and 76 for fp32 on these extents, with 768 columns), rows on and off the
+    8-cell grid (up to 32 fire evaluations per run): three steps against the
+    oracle on windows at the grid's faces, at run boundaries of several run
+    lengths and across a strip boundary."""
+    rng = np.random.default_rng(31)
+    w = rand_weights(rng, 3)
+    n_in = 1
+    d, h, wd = extent
+    # a random block tiled over the level (cheap to build at 59 M cells)
+    block = rng.normal(0, 1, (20, h, 256, C)).astype(NP_DT[dt])
+    s = np.tile(block, (-(-d // 20), 1, -(-wd // 256), 1))[:d, :, :wd]
+    s = np.ascontiguousarray(s)
+    steps = 3
+    got, which = run_level_gpu(octnca.Model(ndim=3, n_in=n_in, dtype=dt), s, w, 1, steps, 0.5, 9)
+    assert which == steps % 2
+    zs = [(0, 3), (74, 80), (97, 104), (150, 153), (197, 203), (295, 300)]
+    xs = [(0, 36), (12270, 12322), (wd - 40, wd)]
+    tol = STEP_TOL[(dt, "mfma")][1]
+    for z in zs:
+        for x in xs:
+            box = (z, (0, h), x)
+            want = oracle_window_steps(s, w, n_in, 3, 1, steps, 9, 0.5, dt, box)
+            part = got[z[0]:z[1], :, x[0]:x[1]]
+            assert max_rel_err(part, want) <= tol, (z, x)
+            np.testing.assert_array_equal(part[..., :n_in], s[z[0]:z[1], :, x[0]:x[1], :n_in])
+
+
 def test_zero_steps_leave_state(gpu):
     rng = np.random.default_rng(1)
     s = rng.normal(0, 1, (1, 9, 9, C)).astype(np.float32)
