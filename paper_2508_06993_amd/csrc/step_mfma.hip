@@ -779,8 +779,7 @@ __device__ __forceinline__ void store_quad(__half *, Rsrc w, uint32_t off, int g
 
 template <typename T>
 __device__ __forceinline__ void update_store(T *tag, Rsrc w, uint32_t off, int g, const float f[8],
-                                             const v4f &u, bool fire) {
-    const float m = fire ? 1.f : 0.f;
+                                             const v4f &u, float m) {   // m: 1 fires, 0 keeps
     v4f out;
     out[0] = fmaf(m, u[0], f[0]);
     out[1] = fmaf(m, u[1], f[1]);
@@ -1344,6 +1343,10 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     constexpr int kEvalBlocks = (k2RunRows + 2 + kEvalRows - 1) / kEvalRows;
     constexpr int kMaskRows = kEvalBlocks * kEvalRows;
     __shared__ uint64_t fire_rows[2][kMaskRows];
+    // The same words shifted once per work item so that bit c is the draw of
+    // strip cell c (x0 - 1 + c for step t, x0 + c for step t + 1): a lane's
+    // bit is then one bit-field extract.
+    __shared__ uint32_t fire_bits[2][kMaskRows];
 
     const int lane = threadIdx.x & 63;
     const int n = lane & 15;
@@ -1389,11 +1392,12 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     };
     // Fire bit of strip cell c (c = x - xs >= 0) in row `rel` (rows from the
     // step's first row) of step s, whose row starts at canonical index rowc:
-    // bit c + ((rowc + xs) & 7) of the row's word.  2D cell indices fit 32
-    // bits (two fp32 states of 2^32 cells would need 512 GB).  Rows outside
-    // the step's range read some in-range word.
-    auto row_word = [&](int s, int rel) {
-        return fire_rows[s][min(max(rel, 0), kMaskRows - 1)];
+    // bit c + ((rowc + xs) & 7) of the row's word in fire_rows, bit c of its
+    // word in fire_bits.  2D cell indices fit 32 bits (two fp32 states of
+    // 2^32 cells would need 512 GB).  Rows outside the step's range read some
+    // in-range word.
+    auto row_bits = [&](int s, int rel) {
+        return fire_bits[s][min(max(rel, 0), kMaskRows - 1)];
     };
     constexpr int kCellBytes = RS::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
@@ -1487,6 +1491,20 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             if (y_first <= y_end - st)
                 evaluate(st, blk, step + st, y_first, st ? (uint32_t)x0 : xs1);
         }
+        // Align each row's word to the strip: step t's strip starts at x1
+        // (x1 = -1 on the first strip, whose cell 0 is outside the grid and
+        // gets bit 0, unused), step t + 1's at x0.  A word spans the 5 blocks
+        // of 8 cells that hold cells xs .. xs + 31, so bits sh .. sh + 31 with
+        // sh <= 7 are inside it.
+        for (int i = lane; i < 2 * kMaskRows; i += 64) {
+            const int s = i >= kMaskRows ? 1 : 0;
+            const int rel = i - s * kMaskRows;
+            const int yo = y_begin - 1 + s + rel;
+            const uint32_t rowc = (uint32_t)min(max(yo, 0), dh - 1) * (uint32_t)dw;
+            const int sh = s ? (int)((rowc + (uint32_t)x0) & 7u)
+                             : (int)((rowc + xs1) & 7u) + (x1 - (int)xs1);
+            fire_bits[s][rel] = (uint32_t)((fire_rows[s][rel] << 1) >> (sh + 1));
+        }
         commit(ra, ia, ring[0]);
         commit(rb, ib, ring[1]);
 
@@ -1523,9 +1541,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
         // start-up whose values are never used.
         auto finish_a = [&](int yo, int slot, const float (&p)[2][4]) {
             const bool row_in = yo >= 0 && yo < dh;
-            const uint32_t rowc = (uint32_t)min(max(yo, 0), dh - 1) * (uint32_t)dw;
-            const int sh = (int)((rowc + xs1) & 7u) + (x1 - (int)xs1);   // bit of cell x1
-            const uint64_t fw = row_word(0, yo - (y_begin - 1));
+            const uint32_t fl = row_bits(0, yo - (y_begin - 1)) >> n;   // bits 0, 16: cells n, 16 + n
             const float4 *own = ring[slot] + g * RS::PS;
             float4 *out = mid[(yo - base) & 1] + g * RS::PS;
             v4f acc[2][4];
@@ -1543,7 +1559,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x1 + grp * 16 + n;
                 const bool in = row_in && x >= 0 && x < dw;
-                const float m = (fw >> max(sh + grp * 16 + n, 0)) & 1 ? 1.f : 0.f;
+                const float m = (float)__builtin_amdgcn_ubfe(fl, grp * 16u, 1u);
                 float v[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) v[k] = in ? fmaf(m, u[k], f[grp][k]) : 0.f;
@@ -1556,9 +1572,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
         auto finish_b = [&](int yo, const float (&p)[2][4]) {
             const bool out_ok = yo >= y_begin && yo < y_end;
             const int yc = min(max(yo, 0), dh - 1);
-            const uint32_t rowc = (uint32_t)yc * (uint32_t)dw;
-            const int sh = (int)((rowc + (uint32_t)x0) & 7u);
-            const uint64_t fw = row_word(1, yo - y_begin);
+            const uint32_t fl = row_bits(1, yo - y_begin) >> n;   // bits 0, 16: cells n, 16 + n
             const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
             const float4 *own = mid[(yo - base) & 1] + g * RS::PS;
             v4f acc[2][4];
@@ -1576,9 +1590,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
                 const uint32_t off = x < x_stop ? (uint32_t)x * kCellBytes : kOut;
+                const float m = (float)__builtin_amdgcn_ubfe(fl, grp * 16u, 1u);
                 if constexpr (SEG) {
-                    const bool fires = (fw >> (sh + grp * 16 + n)) & 1;
-                    const float m = fires ? 1.f : 0.f;
                     v4f o;
 #pragma unroll
                     for (int kk = 0; kk < 4; ++kk) o[kk] = fmaf(m, u[kk], f[grp][kk]);
@@ -1588,7 +1601,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                     __builtin_amdgcn_raw_buffer_store_b8((unsigned char)(o[3] > o[2] ? 1 : 0), sr,
                                                          so, 0, 0);
                 } else {
-                    update_store(dst, wr, off, g, f[grp], u, (fw >> (sh + grp * 16 + n)) & 1);
+                    update_store(dst, wr, off, g, f[grp], u, m);
                 }
             }
         };
