@@ -18,7 +18,9 @@ Prints one JSON line with
 * peak device memory;
 * under "workloads", the same record (value, ms per pass, roofline, peak
   memory) for further workloads timed in the same run (default: the one-minute
-  2D+t video, 1800 x 240 x 432 RGB, fp16 states, 5 levels, 16 steps each).
+  2D+t video, 1800 x 240 x 432 RGB, fp16 states, 5 levels, 16 steps each; the
+  320 x 320 x 24 volume, fp32 states, 3 levels; the 1024 x 1024 2D image,
+  4 levels).
 """
 from __future__ import annotations
 
@@ -327,7 +329,7 @@ def main(argv=None):
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="pathology184mp")
-    ap.add_argument("--extra", default="video2dt",
+    ap.add_argument("--extra", default="video2dt,volume3d,medium2d",
                     help="comma-separated further workloads timed in the same run and reported "
                          "under 'workloads' in the same JSON line ('' for none)")
     ap.add_argument("--model", default="c16h64", choices=sorted(MODEL_SIZES),
