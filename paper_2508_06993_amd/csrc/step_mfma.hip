@@ -567,24 +567,23 @@ struct RowLoader {
     __device__ static __forceinline__ int body_cell(int lane) { return lane % kCellsPerBody; }
     __device__ static __forceinline__ int body_chunk(int lane) { return lane / kCellsPerBody; }
 
-    // Tile whose interior starts at (y0, x0) in plane z; cells outside the
-    // grid (or z outside [0, dd)) read as zero.  The grid must satisfy
-    // HY * dw * kCellBytes < 2^32 (checked by the launcher).
-    // With active = false nothing is read (every offset is out of range) and
-    // the registers are zero: the next-tile prefetch is issued unconditionally.
-    __device__ __forceinline__ void issue(const T *__restrict__ src, int z, int dd, int dh, int dw,
-                                          int y0, int x0, bool active = true) {
+    // Per-lane byte offsets of a tile's loads within its rows (kOut for
+    // unused slots and for cells left of x = 0, above y = 0 or right of the
+    // grid; rows below the grid fall outside the descriptor).  They depend on
+    // the tile only, so a plane loop computes them once per work item and
+    // issue_at() changes only the descriptor from plane to plane.
+    struct Offsets {
+        uint32_t o[kBodySlots + 1];
+    };
+    __device__ __forceinline__ static Offsets offsets(int dw, int y0, int x0) {
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int gy0 = y0 - 1;
         const int base_row = gy0 > 0 ? gy0 : 0;
-        const int rows =
-            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
         const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
-        const Rsrc r = make_rsrc(src + ((int64_t)max(z, 0) * dh + base_row) * dw * kC,
-                                 (uint32_t)rows * row_bytes);
         const int cell = body_cell(lane);
         const uint32_t lane_off = (uint32_t)(cell * kCellBytes + body_chunk(lane) * 16);
+        Offsets r;
 #pragma unroll
         for (int k = 0; k < kBodySlots; ++k) {
             const int J = wave + 4 * k;                       // wave-uniform
@@ -593,8 +592,7 @@ struct RowLoader {
             const bool ok = J < kBody && gy >= 0 && cx0 + cell < dw;
             const uint32_t off = (uint32_t)(gy - base_row) * row_bytes +
                                  (uint32_t)cx0 * kCellBytes + lane_off;
-            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
-            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+            r.o[k] = ok ? off : kOut;
         }
         const int s = 3 - wave;
         const int row = s * kRowsPerSide + lane / (2 * NQ);
@@ -603,8 +601,34 @@ struct RowLoader {
         const bool ok = s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw;
         const uint32_t off = (uint32_t)(gy - base_row) * row_bytes + (uint32_t)gx * kCellBytes +
                              (uint32_t)(lane % NQ) * 16;
-        const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
-        v[kBodySlots] = make_uint4(x[0], x[1], x[2], x[3]);
+        r.o[kBodySlots] = ok ? off : kOut;
+        return r;
+    }
+
+    // Tile whose interior starts at (y0, x0) in plane z (lane offsets `of`
+    // from offsets()); cells outside the grid (or z outside [0, dd)) read as
+    // zero.  The grid must satisfy HY * dw * kCellBytes < 2^32 (checked by
+    // the launcher).  With active = false nothing is read (the descriptor is
+    // empty) and the registers are zero: the next-tile prefetch is issued
+    // unconditionally.
+    __device__ __forceinline__ void issue_at(const T *__restrict__ src, const Offsets &of, int z,
+                                             int dd, int dh, int dw, int y0, bool active = true) {
+        const int gy0 = y0 - 1;
+        const int base_row = gy0 > 0 ? gy0 : 0;
+        const int rows =
+            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
+        const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
+        const Rsrc r = make_rsrc(src + ((int64_t)max(z, 0) * dh + base_row) * dw * kC,
+                                 (uint32_t)rows * row_bytes);
+#pragma unroll
+        for (int k = 0; k <= kBodySlots; ++k) {
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, of.o[k], 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+    }
+    __device__ __forceinline__ void issue(const T *__restrict__ src, int z, int dd, int dh, int dw,
+                                          int y0, int x0, bool active = true) {
+        issue_at(src, offsets(dw, y0, x0), z, dd, dh, dw, y0, active);
     }
 
 __device__ __forceinline__ static void put(float4 *planes, int q, int cell, const uint4 &c) {
@@ -1757,7 +1781,8 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 for (int k = 0; k < 4; ++k) A[i][grp][k] = cb[k];
 
         __syncthreads();   // the previous item's readers are done with the ring
-        ld.issue(src, z_begin - 1, dd, dh, dw, y0, x0);
+        const typename Loader::Offsets lofs = Loader::offsets(dw, y0, x0);
+        ld.issue_at(src, lofs, z_begin - 1, dd, dh, dw, y0);
         // All fire evaluations of the work item, before the plane loop:
         // evaluation e covers output planes z_begin + e * planes_per_eval onwards.
         for (int e = 0; z_begin + e * planes_per_eval < z_end; ++e) {
@@ -1773,7 +1798,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
             fire_words[wave][e][lane & 7] = word;   // 8 lanes per address, same value
         }
         ld.commit(ring[0]);
-        ld.issue(src, z_begin, dd, dh, dw, y0, x0);
+        ld.issue_at(src, lofs, z_begin, dd, dh, dw, y0);
         __syncthreads();
 
         // Plane p (j = (p - z_begin + 1) % 3) is in ring slot j, plane p - 1 in
@@ -1864,7 +1889,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
 
             // plane p + 1 into the free slot, then start loading p + 2
             ld.commit(ring[jp]);
-            ld.issue(src, p + 2, dd, dh, dw, y0, x0, p + 2 <= z_end);
+            ld.issue_at(src, lofs, p + 2, dd, dh, dw, y0, p + 2 <= z_end);
             __syncthreads();
         };
         for (int p0 = z_begin - 1; p0 <= z_end; p0 += 3) {
@@ -1955,6 +1980,7 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     int y0_cur = 0, x0_cur = 0;   // the current item's tile origin (for the loads)
+    typename Loader::Offsets lofs;  // and its lane offsets (plain loads)
     Loader ld;
     typename Loader::template Image<NIN> im;   // used by UP only
     auto issue = [&](int z, bool active) {
@@ -1962,7 +1988,7 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
             ld.template issue_up<NIN>(src, up_cdh, up_cdw, up_fz, up_fy, up_fx, up_img, im, z,
                                       dd, dh, dw, y0_cur, x0_cur, active);
         else
-            ld.issue(src, z, dd, dh, dw, y0_cur, x0_cur, active);
+            ld.issue_at(src, lofs, z, dd, dh, dw, y0_cur, active);
     };
     auto commit = [&](uint2 *slot) {
         if constexpr (UP)
@@ -1987,6 +2013,7 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
         const int y0 = ty * k3TY, x0 = tx * kTileW;
         y0_cur = y0;
         x0_cur = x0;
+        if constexpr (!UP) lofs = Loader::offsets(dw, y0, x0);
         const int z_begin = zr * zrun;
         const int z_end = min(dd, z_begin + zrun);
         // store offsets of the lane's 4 cells within an output plane's tile rows
