@@ -1696,7 +1696,9 @@ constexpr int k3ZRun = 128;
 // i = (zr * tiles_y + ty) * tiles_x + tx.
 
 
-template <typename T, int NIN, class Mlp>
+// ALIGNED: rows start on an 8-cell boundary (w % 8 == 0), which makes the
+// ballot and the bit offset of a lane's cells lane constants.
+template <typename T, int NIN, class Mlp, bool ALIGNED>
 __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const T *__restrict__ src, T *__restrict__ dst, int dd, int dh, int dw, int tiles_x,
     int tiles_y, int items, int zrun, const float *__restrict__ conv_w,
@@ -1741,9 +1743,9 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     // cell reads the one it needs by address: selecting among them by a
     // per-lane value in registers makes the compiler build a private
     // (scratch) array, whose loads would be waited for with the stores.
-    const int opr = (dw & 7) == 0 ? 4 : 8;
-    const int lg_opr = opr == 4 ? 2 : 3;
-    const int planes_per_eval = 64 / (2 * opr);
+    constexpr int opr = ALIGNED ? 4 : 8;
+    constexpr int lg_opr = ALIGNED ? 2 : 3;
+    constexpr int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
     Loader ld;
@@ -1766,6 +1768,14 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
         const int y0 = ty * k3TY, x0 = tx * kTileW;
         const int z_begin = zr * zrun;
         const int z_end = min(dd, z_begin + zrun);
+        // store offsets of the lane's 4 cells within an output plane's tile rows
+        uint32_t offs[4];
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+            const int x = x0 + (grp & 1) * 16 + n;
+            offs[grp] = x < dw ? (uint32_t)(2 * wave + (grp >> 1)) * row_bytes + (uint32_t)x * kCellBytes
+                               : kOut;
+        }
 
         // Rolling perception sums (bias included): A[(r - z_begin + 1) % 3]
         // holds the sum of output plane r.  The plane loop is unrolled three
@@ -1865,6 +1875,11 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
             const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
             const float4 *own = ring[jm];
+            // ALIGNED: the bits of the lane's 4 cells of this plane, at 2 grp
+            // (cell n of group grp is cell n % 8 of block 2 (grp % 2) + n / 8
+            // of row grp / 2: bit (slot0 + grp / 2) * 4 + 2 (grp % 2) + n / 8)
+            uint32_t fw_lane = 0;
+            if constexpr (ALIGNED) fw_lane = (uint32_t)(fwe[n & 7] >> (slot0 * opr + (n >> 3)));
 #pragma unroll
             for (int grp = 0; grp < 4; ++grp) {
                 const float4 sp = own[centre[grp]];
@@ -1874,16 +1889,18 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 v4f acc[4];
                 mlp.layer1(f, acc);
                 const v4f u = mlp.layer2(acc);
-                const int r = grp >> 1;
-                const int ly = 2 * wave + r;
-                const int y = y0 + ly, x = x0 + (grp & 1) * 16 + n;
-                const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
-                const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
-                const uint32_t off =
-                    x < dw ? (uint32_t)ly * row_bytes + (uint32_t)x * kCellBytes : kOut;
-                const uint64_t fw = fwe[idx & 7];
-                const bool fires = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1;
-                update_store(dst, wr, off, g, f, u, fires);
+                float m;
+                if constexpr (ALIGNED) {
+                    m = (float)__builtin_amdgcn_ubfe(fw_lane, 2u * grp, 1u);
+                } else {
+                    const int r = grp >> 1;
+                    const int y = y0 + 2 * wave + r, x = x0 + (grp & 1) * 16 + n;
+                    const uint64_t idx = ((uint64_t)max(zo, 0) * dh + y) * dw + x;
+                    const uint64_t row_b0 = (((uint64_t)max(zo, 0) * dh + y) * dw + x0) >> 3;
+                    const uint64_t fw = fwe[idx & 7];
+                    m = (fw >> ((slot0 + r) * opr + (int)((idx >> 3) - row_b0))) & 1 ? 1.f : 0.f;
+                }
+                update_store(dst, wr, offs[grp], g, f, u, m);
                 __builtin_amdgcn_sched_barrier(0);
             }
 
@@ -2359,7 +2376,9 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
             a.step, a.batch, a.seed, a.threshold, nullptr, 0, 0, 1, 1, 1, a.seg);
     } else {
         const int grid = (int)std::min<int64_t>(items, slots);
-        nca_step_mfma_3d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
+        auto kern = a.ext.w % 8 == 0 ? nca_step_mfma_3d<T, NIN, Mlp, true>
+                                     : nca_step_mfma_3d<T, NIN, Mlp, false>;
+        kern<<<grid, kThreads, 0, stream>>>(
             (const T *)src, (T *)dst, (int)a.ext.d, (int)a.ext.h, (int)a.ext.w, tiles_x, tiles_y,
             (int)items, zrun, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step,
             a.batch, a.seed, a.threshold);
