@@ -306,7 +306,7 @@ def oracle_window_steps(s, w, n_in, ndim, level, steps, seed, rate, dt, box):
 
 
 @pytest.mark.parametrize("dt,extent", [("f16", (300, 8, 24572)), ("f16", (300, 8, 24576)),
-                                       ("f32", (300, 8, 24572))])
+                                       ("f32", (300, 8, 24572)), ("f32", (300, 8, 24576))])
 def test_long_3d_runs_match_oracle_on_windows(gpu, dt, extent):
     """Levels deep and wide enough that the 3D step streams runs of more than
     32 output planes (the launch's load model picks about 100 planes for fp16
