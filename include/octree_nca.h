@@ -296,7 +296,8 @@ int octree_nca_infer_static(const octnca_model *model, const void *image, octnca
  *   final_states [batch][finest][C] written, or NULL.
  *   segs         [batch][finest] uint8 written with the two-class readout, or NULL.
  * Outputs must not overlap the images or the workspace (EINVAL).  All images'
- * arguments are checked before anything is enqueued.
+ * arguments are checked before anything is enqueued.  A batch whose states
+ * would exceed 2^48 bytes is rejected (EINVAL).
  * Errors: EINVAL, ESHAPE, EUNSUPPORTED, ESPACE, EHIP. */
 int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_t batch,
                            octnca_extent finest, int32_t levels, const int32_t *factors,

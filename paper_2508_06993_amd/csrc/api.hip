@@ -71,7 +71,9 @@ int check_extent(const octnca_model *m, const octnca_extent &e) {
     if (e.d <= 0 || e.h <= 0 || e.w <= 0) return OCTNCA_ESHAPE;
     if (e.d > kMaxDim || e.h > kMaxDim || e.w > kMaxDim) return OCTNCA_ESHAPE;
     if (m->ndim == 2 && e.d != 1) return OCTNCA_ESHAPE;
-    if (e.d * e.h > kMaxCells || e.d * e.h * e.w > kMaxCells) return OCTNCA_ESHAPE;
+    // d * h <= 2^60 cannot overflow; the cell count is bounded by division
+    // (d * h * w itself could reach 2^90)
+    if (e.d * e.h > kMaxCells || e.w > kMaxCells / (e.d * e.h)) return OCTNCA_ESHAPE;
     return OCTNCA_OK;
 }
 
@@ -590,6 +592,8 @@ int octree_nca_infer_batch(const octnca_model *model, const void *images, int32_
     const size_t eb = elem_bytes(model);
     const size_t image_bytes = cells * model->n_in * eb;
     const size_t state_bytes = cells * model->channels * eb;
+    // the byte counts below (state_bytes * batch at most) stay far from 2^64
+    if ((uint64_t)batch > (uint64_t(1) << 48) / state_bytes) return OCTNCA_EINVAL;
     // the batch's outputs must not overlap its inputs or the workspace
     if (final_states != nullptr &&
         (overlap(final_states, state_bytes * batch, images, image_bytes * batch) ||

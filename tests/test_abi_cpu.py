@@ -108,6 +108,27 @@ def test_run_level_argument_checks(lib):
                                     None) == EINVAL
 
 
+def test_cell_count_limit_has_no_overflow(lib):
+    """2^36 cells per level at most: an extent whose cell count exceeds it is
+    rejected also where d * h * w does not fit 64 bits (64 x 2^30 x (2^28 + 1)
+    is 2^64 + 2^36 cells, which a 64-bit product wraps to exactly 2^36)."""
+    m3 = model(ndim=3, n_in=1)
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 30, (1 << 28) + 1), 1, None, 1) == 0
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 30, 1 << 30), 1, None, 1) == 0
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 30, 2), 1, None, 1) == 0
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 20, 1 << 11), 1, None, 1) == 0
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 20, 1 << 10), 1, None, 1) > 0
+    assert lib.octree_nca_workspace_bytes(m3, _Extent(64, 1 << 20, 1 << 9), 1, None, 1) > 0
+
+
+def test_batch_size_limit(lib):
+    """A batch whose states would exceed 2^48 bytes is rejected before any
+    pointer arithmetic (2^31 - 1 images of 2^20 x 2^10 cells)."""
+    assert lib.octree_nca_infer_batch(model(), FAKE, (1 << 31) - 1, _Extent(1, 1 << 20, 1 << 10),
+                                      1, None, weights(), (ctypes.c_int32 * 1)(1), 0.5, 0, FAKE2,
+                                      1 << 40, None, None, None) == EINVAL
+
+
 def test_pyramid_and_upsample_shape_checks(lib):
     f = (ctypes.c_int32 * 6)(1, 2, 2, 1, 2, 2)
     imgs = (ctypes.c_void_p * 2)(FAKE, FAKE2)
