@@ -894,9 +894,10 @@ namespace octnca {
 // caller's octnca_model); nothing here reads the environment.
 hipError_t launch_step(const StepArgs &a, const void *src, void *dst, hipStream_t stream) {
     if (a.kc.valu) return launch_step_valu(a, src, dst, stream);
-    // the specialised matrix-core kernels are built for C = 16, H = 64; the
-    // ablation's other sizes run on the generic matrix-core kernel
-    if (a.channels != kC || a.hidden != kH) return launch_step_gen(a, src, dst, stream);
+    // the specialised matrix-core kernels serve C = 16, H = 64 and the 2D
+    // fp32 row layout of C = 12, H = 48; the other steps of the ablation's
+    // sizes run on the generic matrix-core kernel
+    if (!step_mfma_serves(a, a.kc.layout)) return launch_step_gen(a, src, dst, stream);
     return launch_step_mfma(a, a.kc.mlp, a.kc.layout, src, dst, stream);
 }
 

@@ -119,6 +119,10 @@ size_t mse_workspace_doubles(int64_t cells);
 hipError_t launch_readout_mse(const float *state, const float *target, int64_t cells, int channels,
                               float *grad, double *loss, double *ws, hipStream_t stream);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t stream);
+// The specialised matrix-core steps: every step of C = 16, H = 64 models and
+// the 2D fp32 steps of C = 12, H = 48 models in the row layout (default
+// operand policy); step_mfma_serves says whether launch_step_mfma runs `a`.
+bool step_mfma_serves(const StepArgs &a, Layout2d layout);
 hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                             void *dst, hipStream_t stream);
 // The first step of a level fused with the upsample + inject from the next

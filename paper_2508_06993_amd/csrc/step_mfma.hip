@@ -89,6 +89,7 @@ __device__ __forceinline__ float relu(float x) {
 
 // fp32 operands: v_mfma_f32_16x16x4_f32, 32 + 16 MFMAs per 16 cells.
 struct MlpF32 {
+    static constexpr int kChannels = kC, kHidden = kH;
     static constexpr float kPerceptionScale = 1.f;
     float w1[4][8];   // [jt][kc] = W1[jt*16 + n][feature(kc, g)]
     v4f b1[4];        // [jt][i]  = b1[jt*16 + 4g + i]
@@ -177,6 +178,7 @@ __device__ __forceinline__ void split_bf16(const v8f &x, v8bf &hi, v8bf &lo) {
 }
 
 struct MlpBf16x3 {
+    static constexpr int kChannels = kC, kHidden = kH;
     static constexpr float kPerceptionScale = 1.f;
     v8bf w1h[4], w1l[4];   // [jt] slot s: W1[jt*16 + n][feature(s, g)]
     v4f b1[4];
@@ -269,6 +271,7 @@ struct MlpBf16x3 {
 // hidden activations rounded to fp16, products accumulated in fp32 on
 // v_mfma_f32_16x16x32_f16; 4 + 2 MFMAs per 16 cells.
 struct MlpF16 {
+    static constexpr int kChannels = kC, kHidden = kH;
     static constexpr float kPerceptionScale = 1.f;
     v8h w1[4];
     v4f b1[4];
@@ -348,15 +351,33 @@ struct MlpF16 {
 // activation split.  The activations keep fp16's 2^-12 relative rounding,
 // the weights about 2^-22.
 constexpr float kF16ActScale = 1.f / 256.f;
-struct MlpF16S {
+
+// Feature order of a model with C channels (C <= 16, a multiple of 4): slot
+// s < 4 of lane group g is state channel 4g + s, slot s >= 4 perception
+// channel 4g + s - 4; lane groups g >= C / 4 hold no channel.
+template <int C>
+__device__ __forceinline__ int feature_of_c(int slot, int g) {
+    return slot < 4 ? 4 * g + slot : C + 4 * g + (slot - 4);
+}
+
+// C / H: the model's size.  The lane layout is that of C = 16, H = 64; a
+// smaller model (C = 12, H = 48 of the paper's ablation, supplement S10)
+// leaves channel quad 3 and hidden tile 3 empty.  Their weights are gathered
+// as zeros (loaded from clamped indices and then replaced), hidden tile 3 is
+// not computed, and the update of channels >= C is +0.
+template <int C, int H>
+struct MlpF16SM {
+    static_assert(C % 4 == 0 && C <= kC && H % 16 == 0 && H <= kH, "fits the 16 / 64 lanes");
+    static constexpr int kChannels = C, kHidden = H;
+    static constexpr int NT = H / 16;   // hidden tiles computed
     static constexpr float kPerceptionScale = kF16ActScale;
-    v8h w1h[4], w1l[4];   // [jt] slot s: W1[jt*16 + n][feature(s, g)], hi + lo
-    v4f b1[4];            // b1 * 2^-8
-    v8h w2h[2], w2l[2];   // [p] slot s: 2^8 W2[n][hidden(p, s, g)], hi + lo
+    v8h w1h[NT], w1l[NT];   // [jt] slot s: W1[jt*16 + n][feature(s, g)], hi + lo
+    v4f b1[NT];             // b1 * 2^-8
+    v8h w2h[2], w2l[2];     // [p] slot s: 2^8 W2[n][hidden(p, s, g)], hi + lo
 
     __device__ __forceinline__ void pin_all() {
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
+        for (int jt = 0; jt < NT; ++jt) {
             pin(w1h[jt]);
             pin(w1l[jt]);
             pin(b1[jt]);
@@ -375,22 +396,31 @@ struct MlpF16S {
 
     __device__ __forceinline__ void load(const float *__restrict__ W1, const float *__restrict__ B1,
                                          const float *__restrict__ W2, int n, int g, int nin) {
+        const bool g_ok = g < C / 4;
+        const int gc = g_ok ? g : 0;
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt) {
+        for (int jt = 0; jt < NT; ++jt) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = W1[(jt * 16 + n) * 2 * kC + feature_of(s, g)];
+            for (int s = 0; s < 8; ++s) {
+                const float v = W1[(jt * 16 + n) * 2 * C + feature_of_c<C>(s, gc)];
+                x[s] = g_ok ? v : 0.f;
+            }
             split(x, w1h[jt], w1l[jt]);
 #pragma unroll
             for (int i = 0; i < 4; ++i) b1[jt][i] = B1[jt * 16 + 4 * g + i] * kF16ActScale;
         }
+        // rows of the input channels and of channels >= C are zero
+        const bool row_ok = n >= nin && n < C;
+        const int nc = n < C ? n : 0;
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
-                const float v = W2[n * kH + MlpBf16x3::hidden_of(p, s, g)];   // loaded for every n
-                x[s] = n < nin ? 0.f : v * (1.f / kF16ActScale);
+                const int hid = MlpBf16x3::hidden_of(p, s, g);
+                const float v = W2[nc * H + (hid < H ? hid : 0)];   // loaded for every n
+                x[s] = row_ok && hid < H ? v * (1.f / kF16ActScale) : 0.f;
             }
             split(x, w2h[p], w2l[p]);
         }
@@ -402,14 +432,15 @@ struct MlpF16S {
         for (int s = 0; s < 8; ++s) fx[s] = s < 4 ? f[s] * kF16ActScale : f[s];
         const v8h fh = __builtin_convertvector(fx, v8h);
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
+        for (int jt = 0; jt < NT; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1l[jt], fh, b1[jt], 0, 0, 0);
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
+        for (int jt = 0; jt < NT; ++jt)
             acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(w1h[jt], fh, acc[jt], 0, 0, 0);
     }
 
-    // ReLU as packed fp16 max after the rounding (as in MlpF16)
+    // ReLU as packed fp16 max after the rounding (as in MlpF16); hidden tiles
+    // that are not computed enter as zeros
     __device__ __forceinline__ v4f layer2(const v4f acc[4]) const {
         v4f u = {0.f, 0.f, 0.f, 0.f};
         const v8h zero = {};
@@ -417,7 +448,7 @@ struct MlpF16S {
         for (int p = 0; p < 2; ++p) {
             v8f x;
 #pragma unroll
-            for (int s = 0; s < 8; ++s) x[s] = acc[2 * p + s / 4][s % 4];
+            for (int s = 0; s < 8; ++s) x[s] = 2 * p + s / 4 < NT ? acc[2 * p + s / 4][s % 4] : 0.f;
             const v8h h = __builtin_elementwise_max(__builtin_convertvector(x, v8h), zero);
             u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2l[p], h, u, 0, 0, 0);
             u = __builtin_amdgcn_mfma_f32_16x16x32_f16(w2h[p], h, u, 0, 0, 0);
@@ -425,6 +456,7 @@ struct MlpF16S {
         return u;
     }
 };
+using MlpF16S = MlpF16SM<kC, kH>;
 
 // The MLP policy of fp32 states when none is asked for.
 using MlpF32State = MlpF16S;
@@ -869,6 +901,7 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     const float *__restrict__ conv_w, const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
+    static_assert(Mlp::kChannels == kC && Mlp::kHidden == kH, "built for C = 16, H = 64");
     using Loader = RowLoader<T, k2TY + 2>;
     __shared__ float4 planes[4 * Loader::PS];
     __shared__ float4 tapw[9][4];       // [tap][quad] conv weights of channels 4q..4q+3
@@ -1002,15 +1035,44 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
 constexpr int k2RunRows = 128;      // output rows per work item
 constexpr int k2WavesPerSimd = 2;   // 255 VGPRs with the split-bf16 MLP
 
+// The row kernels' conv weights: tapw[t][q] = the tap-t weights of channels
+// 4q..4q+3 and cb = the bias of the lane's channel quad, both times the MLP's
+// perception scale (Sec. 3.1: one 3x3 filter and bias per channel).  Quads
+// >= C / 4 (quad 3 of a C = 12 model) are zero; their indices are clamped and
+// the values replaced, so every lane loads.
+template <int C>
+__device__ __forceinline__ void load_conv_2d(const float *__restrict__ conv_w,
+                                             const float *__restrict__ conv_b, float ps,
+                                             float4 (*tapw)[4], float cb[4]) {
+    const int lane = threadIdx.x & 63;
+    const int i = min(lane, 9 * 4 - 1);
+    const int t = i / 4, q = i % 4;
+    const bool q_ok = q < C / 4;
+    const int qc = q_ok ? q : 0;
+    const float4 tw = make_float4(ps * conv_w[(4 * qc + 0) * 9 + t], ps * conv_w[(4 * qc + 1) * 9 + t],
+                                  ps * conv_w[(4 * qc + 2) * 9 + t], ps * conv_w[(4 * qc + 3) * 9 + t]);
+    if (lane < 9 * 4) tapw[t][q] = q_ok ? tw : make_float4(0.f, 0.f, 0.f, 0.f);
+    const int g = lane >> 4;
+    const bool g_ok = g < C / 4;
+    const int gc = g_ok ? g : 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) cb[k] = g_ok ? ps * conv_b[4 * gc + k] : 0.f;
+}
+
 // One halo row of a strip: kBody body loads (16 cells x 4 chunks in fp32,
 // 32 cells x 2 chunks in fp16, lane i -> cell i % cells-per-load, chunk
 // i / cells-per-load) and one side load whose first 2 NQ lanes take the left
 // and right halo cells.  Cells outside the grid and rows outside [0, h) read
-// as zero through an out-of-range offset or an empty descriptor.
-template <typename T>
+// as zero through an out-of-range offset or an empty descriptor.  A cell of C
+// channels fills kChunks of the NQ chunks; the others (channel quad 3 when
+// C = 12) read as zero the same way, so the ring holds the cell padded to 16
+// channels with zeros.
+template <typename T, int C = kC>
 struct RowStream {
     static constexpr int NQ = CellChunks<T>::N;
-    static constexpr int kCellBytes = kC * (int)sizeof(T);
+    static constexpr int kCellBytes = C * (int)sizeof(T);
+    static constexpr int kChunks = kCellBytes / 16;
+    static_assert(kCellBytes % 16 == 0 && kChunks <= NQ, "whole 16-byte chunks");
     static constexpr int kCellsPerBody = 64 / NQ;
     static constexpr int kBody = kTileW / kCellsPerBody;
     static constexpr int kDummy = kHaloW;                 // never-read slot
@@ -1021,19 +1083,20 @@ struct RowStream {
     __device__ __forceinline__ void issue(const T *__restrict__ src, int y, int dh, int dw, int x0) {
         const int lane = threadIdx.x & 63;
         const bool row_ok = y >= 0 && y < dh;
-        const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? y : 0) * dw * kC,
+        const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? y : 0) * dw * C,
                                  row_ok ? (uint32_t)dw * kCellBytes : 0u);
         const int cell = lane % kCellsPerBody, chunk = lane / kCellsPerBody;
 #pragma unroll
         for (int k = 0; k < kBody; ++k) {
             const int cx = x0 + k * kCellsPerBody + cell;
-            const uint32_t off =
-                cx >= 0 && cx < dw ? (uint32_t)cx * kCellBytes + (uint32_t)chunk * 16 : kOut;
+            const uint32_t off = chunk < kChunks && cx >= 0 && cx < dw
+                                     ? (uint32_t)cx * kCellBytes + (uint32_t)chunk * 16
+                                     : kOut;
             const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
             v[k] = make_uint4(x[0], x[1], x[2], x[3]);
         }
         const int cx = lane < NQ ? x0 - 1 : x0 + kTileW;
-        const bool ok = lane < 2 * NQ && cx >= 0 && cx < dw;
+        const bool ok = lane < 2 * NQ && lane % NQ < kChunks && cx >= 0 && cx < dw;
         const uint32_t off = ok ? (uint32_t)cx * kCellBytes + (uint32_t)(lane % NQ) * 16 : kOut;
         const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
         v[kBody] = make_uint4(x[0], x[1], x[2], x[3]);
@@ -1081,13 +1144,13 @@ struct RowStream {
                                              int y, int dh, int dw, int x0) {
         const int lane = threadIdx.x & 63;
         const bool row_ok = y >= 0 && y < dh;
-        const Rsrc r = make_rsrc(coarse + (int64_t)(row_ok ? y / fy : 0) * cdw * kC,
+        const Rsrc r = make_rsrc(coarse + (int64_t)(row_ok ? y / fy : 0) * cdw * C,
                                  row_ok ? (uint32_t)cdw * kCellBytes : 0u);
         const int cell = lane % kCellsPerBody, chunk = lane / kCellsPerBody;
 #pragma unroll
         for (int k = 0; k < kBody; ++k) {
             const int cx = x0 + k * kCellsPerBody + cell;
-            const uint32_t off = cx >= 0 && cx < dw
+            const uint32_t off = chunk < kChunks && cx >= 0 && cx < dw
                                      ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)chunk * 16
                                      : kOut;
             const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -1095,7 +1158,7 @@ struct RowStream {
         }
         {
             const int cx = lane < NQ ? x0 - 1 : x0 + kTileW;
-            const bool ok = lane < 2 * NQ && cx >= 0 && cx < dw;
+            const bool ok = lane < 2 * NQ && lane % NQ < kChunks && cx >= 0 && cx < dw;
             const uint32_t off =
                 ok ? (uint32_t)(cx / fx) * kCellBytes + (uint32_t)(lane % NQ) * 16 : kOut;
             const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
@@ -1145,7 +1208,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
     const float *__restrict__ w2, uint32_t level, uint32_t step, uint32_t batch, uint64_t seed,
     uint64_t threshold, const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx) {
-    using RS = RowStream<T>;
+    constexpr int C = Mlp::kChannels;
+    using RS = RowStream<T, C>;
     __shared__ float4 ring[4][RS::kSlotWords];   // row y in slot y & 3
     __shared__ float4 tapw[9][4];                // [tap][quad] conv weights of channels 4q..4q+3
 
@@ -1153,19 +1217,10 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     const int n = lane & 15;
     const int g = lane >> 4;
 
-    {
-        const int i = min(lane, 9 * 4 - 1);
-        const int t = i / 4, q = i % 4;
-        constexpr float ps = Mlp::kPerceptionScale;
-        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
-                                      ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
-        if (lane < 9 * 4) tapw[t][q] = tw;
-    }
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
+    load_conv_2d<C>(conv_w, conv_b, Mlp::kPerceptionScale, tapw, cb);
     mlp.pin_all();
 #pragma unroll
     for (int k = 0; k < 4; ++k) pin(cb[k]);
@@ -1264,7 +1319,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
                 fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
             }
             const int yc = max(yo, 0);
-            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
+            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * C, out_ok ? row_bytes : 0u);
             const float4 *own = ring[yo & 3] + g * RS::PS;
             const uint64_t row_b0 = ((uint64_t)yc * dw + x0) >> 3;
             v4f acc[2][4];
@@ -1281,7 +1336,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             for (int grp = 0; grp < 2; ++grp) {
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
-                const uint32_t off = x < dw ? (uint32_t)x * kCellBytes : kOut;
+                const uint32_t off = x < dw && g < C / 4 ? (uint32_t)x * kCellBytes : kOut;
                 bool fires;
                 if constexpr (ALIGNED) {
                     fires = (fire.mine >> (phase * 4 + 2 * grp + (n >> 3))) & 1;
@@ -1353,7 +1408,8 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold,
     const T *__restrict__ up_img, int up_cdw, int up_fy, int up_fx, uint8_t *__restrict__ seg) {
     static_assert(std::is_same_v<T, float>, "the intermediate ring holds fp32 states");
-    using RS = RowStream<T>;
+    constexpr int C = Mlp::kChannels;
+    using RS = RowStream<T, C>;
     // Row r of a work item (first input row `base`) lives in slot
     // (r - base) % 3 of the input ring and (r - base) % 2 of the ring of step
     // t's output rows.
@@ -1376,22 +1432,13 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     const int n = lane & 15;
     const int g = lane >> 4;
 
-    {
-        const int i = min(lane, 9 * 4 - 1);
-        const int t = i / 4, q = i % 4;
-        constexpr float ps = Mlp::kPerceptionScale;
-        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
-                                      ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
-        if (lane < 9 * 4) tapw[t][q] = tw;
-    }
     // Slots 32 and 33 of the step-t ring are never written: the two cells
     // per quad that step t + 1 computes but does not store read them.
     if (lane < 16) mid[lane >> 3][((lane >> 1) & 3) * RS::PS + 32 + (lane & 1)] = make_float4(0.f, 0.f, 0.f, 0.f);
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
+    load_conv_2d<C>(conv_w, conv_b, Mlp::kPerceptionScale, tapw, cb);
     mlp.pin_all();
 #pragma unroll
     for (int k = 0; k < 4; ++k) pin(cb[k]);
@@ -1440,11 +1487,11 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
 #pragma unroll
         for (int kk = 0; kk < RS::kBody; ++kk) {
             const int cx = x + kk * RS::kCellsPerBody + cell;
-            uc.body[kk] = cx >= 0 && cx < dw
+            uc.body[kk] = chunk < RS::kChunks && cx >= 0 && cx < dw
                               ? (uint32_t)(cx / up_fx) * kCellBytes + (uint32_t)chunk * 16 : kOut;
         }
         const int cx = lane < RS::NQ ? x - 1 : x + kTileW;
-        uc.side = lane < 2 * RS::NQ && cx >= 0 && cx < dw
+        uc.side = lane < 2 * RS::NQ && lane % RS::NQ < RS::kChunks && cx >= 0 && cx < dw
                       ? (uint32_t)(cx / up_fx) * kCellBytes + (uint32_t)(lane % RS::NQ) * 16 : kOut;
 #pragma unroll
         for (int j = 0; j < Img::kImg; ++j) {
@@ -1460,7 +1507,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
     auto issue = [&](RS &rs, Img &im, int y, int cy, int x) {
         if constexpr (UP) {
             const bool row_ok = y >= 0 && y < dh;
-            const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? cy : 0) * up_cdw * kC,
+            const Rsrc r = make_rsrc(src + (int64_t)(row_ok ? cy : 0) * up_cdw * C,
                                      row_ok ? (uint32_t)up_cdw * kCellBytes : 0u);
 #pragma unroll
             for (int kk = 0; kk < RS::kBody; ++kk) {
@@ -1597,7 +1644,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             const bool out_ok = yo >= y_begin && yo < y_end;
             const int yc = min(max(yo, 0), dh - 1);
             const uint32_t fl = row_bits(1, yo - y_begin) >> n;   // bits 0, 16: cells n, 16 + n
-            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * kC, out_ok ? row_bytes : 0u);
+            const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * C, out_ok ? row_bytes : 0u);
             const float4 *own = mid[(yo - base) & 1] + g * RS::PS;
             v4f acc[2][4];
             float f[2][8];
@@ -1613,7 +1660,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
             for (int grp = 0; grp < 2; ++grp) {
                 const v4f u = mlp.layer2(acc[grp]);
                 const int x = x0 + grp * 16 + n;
-                const uint32_t off = x < x_stop ? (uint32_t)x * kCellBytes : kOut;
+                const uint32_t off = x < x_stop && g < C / 4 ? (uint32_t)x * kCellBytes : kOut;
                 const float m = (float)__builtin_amdgcn_ubfe(fl, grp * 16u, 1u);
                 if constexpr (SEG) {
                     v4f o;
@@ -1621,7 +1668,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step2_mfma_2d_rows(
                     for (int kk = 0; kk < 4; ++kk) o[kk] = fmaf(m, u[kk], f[grp][kk]);
                     store_quad(dst, wr, off, g, o);
                     const Rsrc sr = make_rsrc(seg + (int64_t)yc * dw, out_ok ? (uint32_t)dw : 0u);
-                    const uint32_t so = g == 3 && x < x_stop ? (uint32_t)x : kOut;
+                    const uint32_t so = g == C / 4 - 1 && x < x_stop ? (uint32_t)x : kOut;
                     __builtin_amdgcn_raw_buffer_store_b8((unsigned char)(o[3] > o[2] ? 1 : 0), sr,
                                                          so, 0, 0);
                 } else {
@@ -1705,6 +1752,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
+    static_assert(Mlp::kChannels == kC && Mlp::kHidden == kH, "built for C = 16, H = 64");
     using Loader = RowLoader<T, k3TY + 2>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
@@ -2285,8 +2333,15 @@ RowsPlan pair_plan(const StepArgs &a) {
     return r;
 }
 
+// The ablation's C = 12, H = 48 model (supplement S10) on the row kernels:
+// 2D fp32 states, scaled fp16 MLP, the lanes of channel quad 3 and hidden
+// tile 3 idle.
+using MlpC12 = MlpF16SM<12, 48>;
+bool is_c12(const StepArgs &a) { return a.channels == 12 && a.hidden == 48; }
+bool is_c16(const StepArgs &a) { return a.channels == kC && a.hidden == kH; }
+
 bool uses_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
-    return a.ndim == 2 && a.dtype == Dtype::F32 && a.channels == kC && a.hidden == kH &&
+    return a.ndim == 2 && a.dtype == Dtype::F32 && (is_c16(a) || is_c12(a)) &&
            a.ext.h * a.ext.w < (int64_t(1) << 32) &&   // 32-bit cell indices in the kernel
            (mlp == MfmaMlp::Default || mlp == MfmaMlp::F16S) &&
            (layout == Layout2d::Rows ||
@@ -2295,15 +2350,15 @@ bool uses_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
 
 // UP: src is the coarse state (width cdw) upsampled by (fy, fx), img the
 // level's image; steps a.step and a.step + 1.
-template <int NIN, bool UP>
+template <class Mlp, int NIN, bool UP>
 hipError_t launch_rows_pair(const StepArgs &a, const void *src, void *dst, const void *img,
                             int cdw, int fy, int fx, hipStream_t stream) {
     const RowsPlan r = pair_plan(a);
     if (r.items == 0) return hipSuccess;
     if (r.items > INT32_MAX) return hipErrorInvalidValue;
     const int grid = (int)std::min<int64_t>(r.items, r.slots);
-    auto kern = a.seg != nullptr ? nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP, true>
-                                 : nca_step2_mfma_2d_rows<float, NIN, MlpF32State, UP, false>;
+    auto kern = a.seg != nullptr ? nca_step2_mfma_2d_rows<float, NIN, Mlp, UP, true>
+                                 : nca_step2_mfma_2d_rows<float, NIN, Mlp, UP, false>;
     kern<<<grid, 64, 0, stream>>>(
         (const float *)src, (float *)dst, (int)a.ext.h, (int)a.ext.w, r.tiles_x, k2RunRows,
         (int)r.items, a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch,
@@ -2321,11 +2376,16 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
     if (uses_rows(a, layout))
         return launch_rows<T, NIN, Mlp, false>(a, src, dst, nullptr, 0, 1, 1, stream);
-    const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
-    nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
-        (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles, a.w.conv_w,
-        a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed, a.threshold);
-    return hipGetLastError();
+    if constexpr (Mlp::kChannels != kC) {
+        return hipErrorInvalidValue;   // other model sizes: rows only
+    } else {
+        const int grid = (int)std::min<int64_t>(tiles, (int64_t)device_cus() * k2BlocksPerCu);
+        nca_step_mfma_2d<T, NIN, Mlp><<<grid, kThreads, 0, stream>>>(
+            (const T *)src, (T *)dst, (int)a.ext.h, (int)a.ext.w, tiles_x, (int)tiles,
+            a.w.conv_w, a.w.conv_b, a.w.w1, a.w.b1, a.w.w2, a.level, a.step, a.batch, a.seed,
+            a.threshold);
+        return hipGetLastError();
+    }
 }
 
 // Output planes per 3D work item, chosen per launch: the run length r in
@@ -2415,7 +2475,7 @@ hipError_t dispatch(const StepArgs &a, Layout2d layout, const void *src, void *d
     if (a.ndim == 2) {
         if (a.n_in == 1) return launch_2d<T, 1, Mlp>(a, layout, src, dst, stream);
         if (a.n_in == 3) return launch_2d<T, 3, Mlp>(a, layout, src, dst, stream);
-    } else {
+    } else if constexpr (Mlp::kChannels == kC) {   // 3D: C = 16, H = 64 only
         if (a.n_in == 1) return launch_3d<T, 1, Mlp>(a, src, dst, stream);
         if (a.n_in == 3) return launch_3d<T, 3, Mlp>(a, src, dst, stream);
     }
@@ -2440,28 +2500,44 @@ bool step_mfma_pairs(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
     return mfma_fits(a) && uses_pairs(a, mlp, layout);
 }
 
+template <class Mlp>
+hipError_t launch_pair_size(const StepArgs &a, const void *src, void *dst, const void *img,
+                            int cdw, int fy, int fx, bool up, hipStream_t stream) {
+    if (a.n_in == 1)
+        return up ? launch_rows_pair<Mlp, 1, true>(a, src, dst, img, cdw, fy, fx, stream)
+                  : launch_rows_pair<Mlp, 1, false>(a, src, dst, nullptr, 0, 1, 1, stream);
+    if (a.n_in == 3)
+        return up ? launch_rows_pair<Mlp, 3, true>(a, src, dst, img, cdw, fy, fx, stream)
+                  : launch_rows_pair<Mlp, 3, false>(a, src, dst, nullptr, 0, 1, 1, stream);
+    return hipErrorInvalidValue;
+}
+
 hipError_t launch_step2_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                              void *dst, hipStream_t stream) {
     if (!step_mfma_pairs(a, mlp, layout)) return hipErrorInvalidValue;
-    if (a.n_in == 1) return launch_rows_pair<1, false>(a, src, dst, nullptr, 0, 1, 1, stream);
-    if (a.n_in == 3) return launch_rows_pair<3, false>(a, src, dst, nullptr, 0, 1, 1, stream);
-    return hipErrorInvalidValue;
+    return is_c12(a) ? launch_pair_size<MlpC12>(a, src, dst, nullptr, 0, 1, 1, false, stream)
+                     : launch_pair_size<MlpF32State>(a, src, dst, nullptr, 0, 1, 1, false, stream);
 }
 
 hipError_t launch_step2_mfma_up(const StepArgs &a, MfmaMlp mlp, Layout2d layout,
                                 const void *coarse, int coarse_w, int fy, int fx, const void *img,
                                 void *dst, hipStream_t stream) {
     if (!step_mfma_pairs(a, mlp, layout)) return hipErrorInvalidValue;
-    if (a.n_in == 1)
-        return launch_rows_pair<1, true>(a, coarse, dst, img, coarse_w, fy, fx, stream);
-    if (a.n_in == 3)
-        return launch_rows_pair<3, true>(a, coarse, dst, img, coarse_w, fy, fx, stream);
-    return hipErrorInvalidValue;
+    return is_c12(a)
+               ? launch_pair_size<MlpC12>(a, coarse, dst, img, coarse_w, fy, fx, true, stream)
+               : launch_pair_size<MlpF32State>(a, coarse, dst, img, coarse_w, fy, fx, true, stream);
+}
+
+bool step_mfma_serves(const StepArgs &a, Layout2d layout) {
+    if (is_c16(a)) return true;
+    return is_c12(a) && a.ndim == 2 && a.dtype == Dtype::F32 && uses_rows(a, layout) &&
+           mfma_fits(a);
 }
 
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
-    if (a.channels != kC || a.hidden != kH || mlp != MfmaMlp::Default || !mfma_fits(a))
-        return false;
+    if (mlp != MfmaMlp::Default || !mfma_fits(a)) return false;
+    if (is_c12(a)) return step_mfma_serves(a, layout);
+    if (!is_c16(a)) return false;
     if (a.ndim == 2) return uses_rows(a, layout);
     return a.dtype == Dtype::F16;   // the fp16 3D step
 }
@@ -2477,6 +2553,15 @@ hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *c
         if (a.n_in == 3)
             return launch_3d_f16_up<3>(a, coarse, coarse_h, coarse_w, fz, fy, fx, img, dst,
                                        stream);
+        return hipErrorInvalidValue;
+    }
+    if (is_c12(a)) {
+        if (a.n_in == 1)
+            return launch_rows<float, 1, MlpC12, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                       stream);
+        if (a.n_in == 3)
+            return launch_rows<float, 3, MlpC12, true>(a, coarse, dst, img, coarse_w, fy, fx,
+                                                       stream);
         return hipErrorInvalidValue;
     }
     if (a.dtype == Dtype::F32) {
@@ -2500,6 +2585,11 @@ hipError_t launch_step_mfma_up(const StepArgs &a, Layout2d layout, const void *c
 hipError_t launch_step_mfma(const StepArgs &a, MfmaMlp mlp, Layout2d layout, const void *src,
                             void *dst, hipStream_t stream) {
     if (!mfma_fits(a)) return launch_step_valu(a, src, dst, stream);
+    if (is_c12(a)) {
+        if (!step_mfma_serves(a, layout) || mlp != MfmaMlp::Default) return hipErrorInvalidValue;
+        return dispatch<float, MlpC12>(a, layout, src, dst, stream);
+    }
+    if (!is_c16(a)) return hipErrorInvalidValue;
     if (mlp == MfmaMlp::Default)
         mlp = a.dtype == Dtype::F32 ? MfmaMlp::F16S : MfmaMlp::F16;
     if (a.dtype == Dtype::F32) {

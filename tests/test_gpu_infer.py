@@ -60,8 +60,10 @@ SMALL = [
     Workload(name="odd_steps_f16_2d", ndim=2, extent=(1, 48, 36), n_in=1,
              factors=((1, 2, 2), (1, 3, 3)), steps=(3, 1, 5), dtype="f16",
              image_kind="uniform"),
-    # the ablation's model sizes (supplement S10): the generic matrix-core
-    # kernel ("mfma" cases) and the vector kernel ("valu")
+    # the ablation's model sizes (supplement S10): 2D fp32 states of 12/48 on
+    # the row kernels ("mfma", "mfma_rows") or the generic tile kernel
+    # ("mfma_tiles"), the others on the generic matrix-core kernel, and all on
+    # the vector kernel ("valu")
     Workload(name="c12h48_2d", ndim=2, extent=(1, 64, 96), n_in=3, factors=((1, 2, 2),) * 2,
              steps=(4, 3, 5), image_kind="uniform", channels=12, hidden=48),
     Workload(name="c20h100_3d_f16", ndim=3, extent=(8, 16, 24), n_in=3,
@@ -80,7 +82,8 @@ SMALL = [
 def test_infer_matches_oracle(gpu, step_kernel, wl):
     if (wl.channels, wl.hidden) != (16, 64) and step_kernel in ("mfma_f32", "mfma_bf16x3"):
         pytest.skip("the matrix-core operand choices serve C/H = 16/64 only; the other "
-                    "sizes run on the vector kernel (the 'mfma' and 'valu' cases)")
+                    "sizes take the default arithmetic ('mfma', 'mfma_rows', 'mfma_tiles') "
+                    "or the vector kernel ('valu')")
     image = make_image(wl)
     weights = make_weights(wl)
     state, seg = gpu_infer(wl, image, weights, kernel=step_kernel)
