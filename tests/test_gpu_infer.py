@@ -12,6 +12,8 @@ oracle.
   boxes of 2 x 16 x 16 cells, evaluated exactly through their light cones
   (corners, edges, the kernels' work-item edges, random interior).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -308,14 +310,21 @@ def sampled_boxes(wl, count, size, depth=1, seed=5):
     return out
 
 
+PATHOLOGY_C12H48 = dataclasses.replace(PATHOLOGY_184MP, name="pathology184mp_c12h48",
+                                       channels=12, hidden=48)
+
+
 @pytest.mark.parametrize("wl,count,size,depth", [(PATHOLOGY_184MP, 64, 16, 1),
-                                                 (VIDEO_2DT, 16, 16, 2)],
-                         ids=["pathology184mp", "video2dt"])
+                                                 (VIDEO_2DT, 16, 16, 2),
+                                                 (PATHOLOGY_C12H48, 32, 16, 1)],
+                         ids=["pathology184mp", "video2dt", "pathology184mp_c12h48"])
 def test_full_size_sampled_boxes(gpu, wl, count, size, depth):
     """The 184.5 MP image and the one-minute video run whole on the GPU; the
     oracle evaluates sampled boxes exactly through their light cones (in
     parallel over the host's cores).  The bounds apply to all sampled cells
-    together."""
+    together.  The 184.5 MP image also runs with the ablation's C = 12,
+    H = 48 model (supplement S10), whose 2D fp32 steps take the same row
+    kernels."""
     print(f"full-size parity {wl.name} extent={wl.extent}: {count} boxes of "
           f"{depth}x{size}x{size}", flush=True)
     path = cached_image_file(wl)
