@@ -1242,11 +1242,14 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
     int gq = g;
     RS ra, rb;
     typename RS::template Image<NIN> ia, ib;   // used by UP only
+    // Rows at or beyond y_lim (the run's last input row + 1, or the grid's
+    // height) read as zero through an empty descriptor, without a memory access.
+    int y_lim = dh;
     auto issue = [&](RS &rs, typename RS::template Image<NIN> &im, int y, int x0) {
         if constexpr (UP)
-            rs.template issue_up<NIN>(src, up_cdw, up_fy, up_fx, up_img, im, y, dh, dw, x0);
+            rs.template issue_up<NIN>(src, up_cdw, up_fy, up_fx, up_img, im, y, y_lim, dw, x0);
         else
-            rs.issue(src, y, dh, dw, x0);
+            rs.issue(src, y, y_lim, dw, x0);
     };
     auto commit = [&](const RS &rs, const typename RS::template Image<NIN> &im, float4 *slot) {
         if constexpr (UP)
@@ -1261,6 +1264,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
         const int x0 = sx * kTileW;
         const int y_begin = ry * run_rows;
         const int y_end = min(dh, y_begin + run_rows);
+        y_lim = min(dh, y_end + 1);   // input rows y_begin - 1 .. y_end feed the run
 
         // rolling perception sums (bias included) of outputs q - 1, q, q + 1
         float acc_p[2][4], acc_c[2][4], acc_n[2][4];
@@ -1272,12 +1276,6 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
                 acc_c[grp][k] = cb[k];
                 acc_n[grp][k] = cb[k];
             }
-
-        // rows y_begin - 1 and y_begin into the ring
-        issue(ra, ia, y_begin - 1, x0);
-        issue(rb, ib, y_begin, x0);
-        commit(ra, ia, ring[(y_begin - 1) & 3]);
-        commit(rb, ib, ring[y_begin & 3]);
 
         // Input row q with its x taps: output q + 1 takes the dy = -1 weights,
         // q the dy = 0 ones and q - 1 the dy = +1 ones.
@@ -1304,6 +1302,18 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
                     }
                 }
             }
+        };
+
+        // The sums shift by one row: output q + 1 becomes the next to finish.
+        auto shift = [&]() {
+#pragma unroll
+            for (int grp = 0; grp < 2; ++grp)
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    acc_p[grp][k] = acc_c[grp][k];
+                    acc_c[grp][k] = acc_n[grp][k];
+                    acc_n[grp][k] = cb[k];
+                }
         };
 
         // Output row yo (complete in acc_p): MLP, fire gate and store of its
@@ -1346,19 +1356,28 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
                 }
                 update_store(dst, wr, off, g, f[grp], u, fires);
             }
-#pragma unroll
-            for (int grp = 0; grp < 2; ++grp)
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    acc_p[grp][k] = acc_c[grp][k];
-                    acc_c[grp][k] = acc_n[grp][k];
-                    acc_n[grp][k] = cb[k];
-                }
+            shift();
         };
 
-        // input rows q, q + 1 per iteration, from y_begin - 1 through y_end
+        // Rows y_begin - 1 and y_begin into the ring, y_begin + 1 and
+        // y_begin + 2 in flight while they are folded; outputs y_begin - 2 and
+        // y_begin - 1, which they complete, are outside the run (not computed).
+        issue(ra, ia, y_begin - 1, x0);
+        issue(rb, ib, y_begin, x0);
+        commit(ra, ia, ring[(y_begin - 1) & 3]);
+        commit(rb, ib, ring[y_begin & 3]);
+        issue(ra, ia, y_begin + 1, x0);
+        issue(rb, ib, y_begin + 2, x0);
+        fold_row(y_begin - 1);
+        shift();
+        fold_row(y_begin);
+        shift();
+        commit(ra, ia, ring[(y_begin + 1) & 3]);
+        commit(rb, ib, ring[(y_begin + 2) & 3]);
+
+        // input rows q, q + 1 per iteration, from y_begin + 1 through y_end
         // (plus one padding row when the count is odd)
-        for (int q = y_begin - 1; q <= y_end; q += 2) {
+        for (int q = y_begin + 1; q <= y_end; q += 2) {
             issue(ra, ia, q + 2, x0);
             issue(rb, ib, q + 3, x0);
             fold_row(q);
