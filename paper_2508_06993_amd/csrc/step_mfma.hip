@@ -1953,9 +1953,18 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
                 float f[8] = {sp.x, sp.y, sp.z, sp.w};
 #pragma unroll
                 for (int k = 0; k < 4; ++k) f[4 + k] = last[grp][k];
-                v4f acc[4];
-                mlp.layer1(f, acc);
-                const v4f u = mlp.layer2(acc);
+                // The MLP of a plane outside the run (the first two bodies of a
+                // work item and its padding) is skipped: a uniform branch with
+                // no memory operation inside, so the store below and the wait
+                // counts around it are the same on both paths.  That store is
+                // dropped, so u may hold anything there (left unspecified: no
+                // register moves to merge the two paths).
+                v4f u = __builtin_nondeterministic_value(u);
+                if (out_ok) {
+                    v4f acc[4];
+                    mlp.layer1(f, acc);
+                    u = mlp.layer2(acc);
+                }
                 float m;
                 if constexpr (ALIGNED) {
                     m = (float)__builtin_amdgcn_ubfe(fw_lane, 2u * grp, 1u);
