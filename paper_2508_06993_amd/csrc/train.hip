@@ -440,33 +440,57 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
         gidx = ((int64_t)gz * dh + gy) * dw + gx;
         return gx >= 0 && gx < dw && gy >= 0 && gy < dh && gz >= 0 && gz < dd;
     };
-    for (int i = threadIdx.x; i < 4 * NCELL; i += kBwdThreads) {
+    // Every thread loads its elements from clamped in-grid addresses and zeroes
+    // the values outside afterwards, and all tile loads are issued before the
+    // first LDS write: the tiles then cost one memory round trip (a load
+    // behind the cell's condition became a branch and a wait per element).
+    constexpr int LPT = (4 * NCELL + kBwdThreads - 1) / kBwdThreads;
+    // v with every bit cleared where m is 0 (an exact +0 whatever v holds)
+    auto masked = [](float4 v, uint32_t m) {
+        return make_float4(__uint_as_float(__float_as_uint(v.x) & m),
+                           __uint_as_float(__float_as_uint(v.y) & m),
+                           __uint_as_float(__float_as_uint(v.z) & m),
+                           __uint_as_float(__float_as_uint(v.w) & m));
+    };
+    float4 sv[LPT], gv[LPT];
+    uint32_t s_m[LPT], g_m[LPT];
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+        const int i = min((int)threadIdx.x + j * kBwdThreads, 4 * NCELL - 1);
         const int q = i % 4, cell = i / 4;
         int64_t gi;
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (halo_cell(cell, gi)) v = *reinterpret_cast<const float4 *>(src + gi * C + 4 * q);
-        tile[q][cell] = v;
+        const bool ok = halo_cell(cell, gi);
+        s_m[j] = ok ? 0xffffffffu : 0u;
+        sv[j] = *reinterpret_cast<const float4 *>(src + (ok ? gi : 0) * C + 4 * q);
     }
-    if (gp_prev != nullptr)
-        for (int i = threadIdx.x; i < 4 * NCELL; i += kBwdThreads) {
+    if (gp_prev != nullptr) {
+#pragma unroll
+        for (int j = 0; j < LPT; ++j) {
+            const int i = min((int)threadIdx.x + j * kBwdThreads, 4 * NCELL - 1);
             const int cell = i % NCELL, q = i / NCELL;
             int64_t gi;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (halo_cell(cell, gi))
-                v = make_float4(gp_prev[(4 * q + 0) * cells + gi], gp_prev[(4 * q + 1) * cells + gi],
-                                gp_prev[(4 * q + 2) * cells + gi], gp_prev[(4 * q + 3) * cells + gi]);
-            gtile[q * NCELL + cell] = v;
+            const bool ok = halo_cell(cell, gi);
+            g_m[j] = ok ? 0xffffffffu : 0u;
+            const int64_t gc = ok ? gi : 0;
+            gv[j] = make_float4(gp_prev[(4 * q + 0) * cells + gc], gp_prev[(4 * q + 1) * cells + gc],
+                                gp_prev[(4 * q + 2) * cells + gc], gp_prev[(4 * q + 3) * cells + gc]);
         }
-    // conv weights and bias into LDS (a tap's weights are one 16-byte read
-    // per lane there, instead of four global reads inside the tap loops)
-    for (int i = threadIdx.x; i < TAPS * 4; i += kBwdThreads) {
-        const int t = i / 4, q = i % 4;
-        kw[t][q] = make_float4(conv_w[(4 * q + 0) * TAPS + t], conv_w[(4 * q + 1) * TAPS + t],
-                               conv_w[(4 * q + 2) * TAPS + t], conv_w[(4 * q + 3) * TAPS + t]);
     }
-    if (threadIdx.x < 4)
-        kb[threadIdx.x] = make_float4(conv_b[4 * threadIdx.x + 0], conv_b[4 * threadIdx.x + 1],
-                                      conv_b[4 * threadIdx.x + 2], conv_b[4 * threadIdx.x + 3]);
+    // conv weights and bias for LDS (a tap's weights are one 16-byte read per
+    // lane there, instead of four global reads inside the tap loops); thread
+    // i < 4 TAPS holds [tap i / 4][quad i % 4], thread i < 4 the bias of quad
+    // i, loaded from clamped indices by every thread
+    static_assert(TAPS * 4 <= kBwdThreads, "one conv weight quad per thread");
+    float4 kwv, kbv;
+    {
+        const int i = min((int)threadIdx.x, TAPS * 4 - 1);
+        const int t = i / 4, q = i % 4;
+        kwv = make_float4(conv_w[(4 * q + 0) * TAPS + t], conv_w[(4 * q + 1) * TAPS + t],
+                          conv_w[(4 * q + 2) * TAPS + t], conv_w[(4 * q + 3) * TAPS + t]);
+        const int qb = min((int)threadIdx.x, 3);
+        kbv = make_float4(conv_b[4 * qb + 0], conv_b[4 * qb + 1], conv_b[4 * qb + 2],
+                          conv_b[4 * qb + 3]);
+    }
     // weights in the lane's operand layouts
     float w1a[4][8];    // [t][kc] = W1[16t + n][feature(kc, g)]
     float w1t[2][4][4]; // [ft][t][i] = W1[16t + 4g + i][16 ft + n]
@@ -484,6 +508,21 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_cell_mfma(
             const float v2 = w2[(4 * g + i) * H + 16 * t + n];   // loaded for every row
             w2t[t][i] = 4 * g + i < NIN ? 0.f : v2;
             bias[t][i] = b1[16 * t + 4 * g + i];
+        }
+    }
+    // LDS writes, after every load of the block's set-up has been issued
+    if (threadIdx.x < TAPS * 4) kw[threadIdx.x / 4][threadIdx.x % 4] = kwv;
+    if (threadIdx.x < 4) kb[threadIdx.x] = kbv;
+#pragma unroll
+    for (int j = 0; j < LPT; ++j) {
+        const int i = (int)threadIdx.x + j * kBwdThreads;
+        if (i < 4 * NCELL) tile[i % 4][i / 4] = masked(sv[j], s_m[j]);
+    }
+    if (gp_prev != nullptr) {
+#pragma unroll
+        for (int j = 0; j < LPT; ++j) {
+            const int i = (int)threadIdx.x + j * kBwdThreads;
+            if (i < 4 * NCELL) gtile[i] = masked(gv[j], g_m[j]);
         }
     }
     __syncthreads();
