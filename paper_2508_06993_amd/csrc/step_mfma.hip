@@ -912,12 +912,12 @@ __global__ __launch_bounds__(kThreads, k2BlocksPerCu) void nca_step_mfma_2d(
     const int g = lane >> 4;
 
     {
-        const int i = min((int)threadIdx.x, 9 * 4 - 1);
+        const int i = (int)threadIdx.x % (9 * 4);
         const int t = i / 4, q = i % 4;
         constexpr float ps = Mlp::kPerceptionScale;
         const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 9 + t], ps * conv_w[(4 * q + 1) * 9 + t],
                                       ps * conv_w[(4 * q + 2) * 9 + t], ps * conv_w[(4 * q + 3) * 9 + t]);
-        if (threadIdx.x < 9 * 4) tapw[t][q] = tw;
+        tapw[t][q] = tw;   // threads >= 36 rewrite an entry (same value): no branch
     }
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g, NIN);
@@ -1045,18 +1045,20 @@ __device__ __forceinline__ void load_conv_2d(const float *__restrict__ conv_w,
                                              const float *__restrict__ conv_b, float ps,
                                              float4 (*tapw)[4], float cb[4]) {
     const int lane = threadIdx.x & 63;
-    const int i = min(lane, 9 * 4 - 1);
+    const int i = lane % (9 * 4);
     const int t = i / 4, q = i % 4;
     const bool q_ok = q < C / 4;
     const int qc = q_ok ? q : 0;
     const float4 tw = make_float4(ps * conv_w[(4 * qc + 0) * 9 + t], ps * conv_w[(4 * qc + 1) * 9 + t],
                                   ps * conv_w[(4 * qc + 2) * 9 + t], ps * conv_w[(4 * qc + 3) * 9 + t]);
-    if (lane < 9 * 4) tapw[t][q] = q_ok ? tw : make_float4(0.f, 0.f, 0.f, 0.f);
     const int g = lane >> 4;
     const bool g_ok = g < C / 4;
     const int gc = g_ok ? g : 0;
 #pragma unroll
     for (int k = 0; k < 4; ++k) cb[k] = g_ok ? ps * conv_b[4 * gc + k] : 0.f;
+    // lanes >= 36 write an entry again with the same value: no branch, so the
+    // loads above are not sunk behind one and wait once together
+    tapw[t][q] = q_ok ? tw : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 // One halo row of a strip: kBody body loads (16 cells x 4 chunks in fp32,
