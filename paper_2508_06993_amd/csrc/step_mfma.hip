@@ -1306,6 +1306,14 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
             }
         };
 
+        // Fire bits of output rows yo .. yo + rows_per_eval - 1.
+        auto evaluate_fire = [&](int yo) {
+            const int yy = min(yo + (lane >> lg_opr), dh - 1);
+            const uint64_t b0 = ((uint64_t)yy * dw + x0) >> 3;
+            fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, batch, seed, threshold);
+            fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
+        };
+
         // The sums shift by one row: output q + 1 becomes the next to finish.
         auto shift = [&]() {
 #pragma unroll
@@ -1324,12 +1332,7 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
         auto finish_row = [&](int yo) {
             const bool out_ok = yo >= y_begin && yo < y_end;
             const int phase = (yo - y_begin) & (rows_per_eval - 1);
-            if (out_ok && phase == 0) {
-                const int yy = min(yo + (lane >> lg_opr), dh - 1);
-                const uint64_t b0 = ((uint64_t)yy * dw + x0) >> 3;
-                fire.f = fire_ballots(b0 + (lane & (fire.opr - 1)), step, level, batch, seed, threshold);
-                fire.mine = select_ballot(fire.f, (uint32_t)n & 7u);
-            }
+            if (out_ok && phase == 0 && yo != y_begin) evaluate_fire(yo);
             const int yc = max(yo, 0);
             const Rsrc wr = make_rsrc(dst + (int64_t)yc * dw * C, out_ok ? row_bytes : 0u);
             const float4 *own = ring[yo & 3] + g * RS::PS;
@@ -1364,8 +1367,10 @@ __global__ __launch_bounds__(64, k2WavesPerSimd) void nca_step_mfma_2d_rows(
         // Rows y_begin - 1 and y_begin into the ring, y_begin + 1 and
         // y_begin + 2 in flight while they are folded; outputs y_begin - 2 and
         // y_begin - 1, which they complete, are outside the run (not computed).
+        // The run's first fire evaluation runs while the first rows load.
         issue(ra, ia, y_begin - 1, x0);
         issue(rb, ib, y_begin, x0);
+        evaluate_fire(y_begin);
         commit(ra, ia, ring[(y_begin - 1) & 3]);
         commit(rb, ib, ring[y_begin & 3]);
         issue(ra, ia, y_begin + 1, x0);
