@@ -574,10 +574,15 @@ __device__ __forceinline__ int64_t xcd_item(int64_t u, int grid) {
     return (r * kXcds + b % kXcds) * (grid / kXcds) + b / kXcds;
 }
 
-template <typename T, int HY>
+// C: channels of a cell; a cell fills kChunks of the NQ 16-byte chunks, the
+// loads of the others (channel quad 3 when C = 12) take the out-of-range
+// offset and read as zero.
+template <typename T, int HY, int C = kC>
 struct RowLoader {
     static constexpr int NQ = CellChunks<T>::N;
-    static constexpr int kCellBytes = kC * (int)sizeof(T);
+    static constexpr int kCellBytes = C * (int)sizeof(T);
+    static constexpr int kChunks = kCellBytes / 16;
+    static_assert(kCellBytes % 16 == 0 && kChunks <= NQ, "whole 16-byte chunks");
     static constexpr int kCellsPerBody = 64 / NQ;            // cells per body load
     static constexpr int kBodyPerRow = kTileW / kCellsPerBody;
     static constexpr int kRowsPerSide = 64 / (2 * NQ);       // rows per side load
@@ -621,7 +626,7 @@ struct RowLoader {
             const int J = wave + 4 * k;                       // wave-uniform
             const int gy = gy0 + J / kBodyPerRow;
             const int cx0 = x0 + (J % kBodyPerRow) * kCellsPerBody;
-            const bool ok = J < kBody && gy >= 0 && cx0 + cell < dw;
+            const bool ok = J < kBody && gy >= 0 && cx0 + cell < dw && body_chunk(lane) < kChunks;
             const uint32_t off = (uint32_t)(gy - base_row) * row_bytes +
                                  (uint32_t)cx0 * kCellBytes + lane_off;
             r.o[k] = ok ? off : kOut;
@@ -630,7 +635,8 @@ struct RowLoader {
         const int row = s * kRowsPerSide + lane / (2 * NQ);
         const int gy = gy0 + row;
         const int gx = ((lane / NQ) & 1) ? x0 + kTileW : x0 - 1;
-        const bool ok = s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw;
+        const bool ok =
+            s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw && lane % NQ < kChunks;
         const uint32_t off = (uint32_t)(gy - base_row) * row_bytes + (uint32_t)gx * kCellBytes +
                              (uint32_t)(lane % NQ) * 16;
         r.o[kBodySlots] = ok ? off : kOut;
@@ -650,7 +656,7 @@ struct RowLoader {
         const int rows =
             (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
         const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
-        const Rsrc r = make_rsrc(src + ((int64_t)max(z, 0) * dh + base_row) * dw * kC,
+        const Rsrc r = make_rsrc(src + ((int64_t)max(z, 0) * dh + base_row) * dw * C,
                                  (uint32_t)rows * row_bytes);
 #pragma unroll
         for (int k = 0; k <= kBodySlots; ++k) {
@@ -729,6 +735,7 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
                                              int fz, int fy, int fx, const T *__restrict__ img,
                                              Image<NIN> &im, int z, int dd, int dh, int dw,
                                              int y0, int x0, bool active = true) {
+        static_assert(C == kC, "the fused upsample serves C = 16");
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int gy0 = y0 - 1;
@@ -1778,8 +1785,9 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     const float *__restrict__ conv_b,
     const float *__restrict__ w1, const float *__restrict__ b1, const float *__restrict__ w2,
     uint32_t level, uint32_t step, uint32_t batch, uint64_t seed, uint64_t threshold) {
-    static_assert(Mlp::kChannels == kC && Mlp::kHidden == kH, "built for C = 16, H = 64");
-    using Loader = RowLoader<T, k3TY + 2>;
+    // C = 16 (H = 64) or the ablation's C = 12 (H = 48): channel quad 3 idle
+    constexpr int C = Mlp::kChannels;
+    using Loader = RowLoader<T, k3TY + 2, C>;
     __shared__ float4 ring[3][4 * Loader::PS];
     __shared__ float4 tapw[27][4];      // [tap][quad] conv weights of channels 4q..4q+3
     // [wave][evaluation of the work item][b]: ballot b (k3ZRun / 4 evaluations
@@ -1794,16 +1802,18 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
     {
         const int i = min((int)threadIdx.x, 27 * 4 - 1);
         const int t = i / 4, q = i % 4;
+        const int qc = q < C / 4 ? q : 0;   // quads >= C / 4: zero weights
         constexpr float ps = Mlp::kPerceptionScale;
-        const float4 tw = make_float4(ps * conv_w[(4 * q + 0) * 27 + t], ps * conv_w[(4 * q + 1) * 27 + t],
-                                      ps * conv_w[(4 * q + 2) * 27 + t], ps * conv_w[(4 * q + 3) * 27 + t]);
-        if (threadIdx.x < 27 * 4) tapw[t][q] = tw;
+        const float4 tw = make_float4(ps * conv_w[(4 * qc + 0) * 27 + t], ps * conv_w[(4 * qc + 1) * 27 + t],
+                                      ps * conv_w[(4 * qc + 2) * 27 + t], ps * conv_w[(4 * qc + 3) * 27 + t]);
+        if (threadIdx.x < 27 * 4) tapw[t][q] = q < C / 4 ? tw : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     Mlp mlp;
     mlp.load(w1, b1, w2, n, g, NIN);
     float cb[4];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) cb[k] = Mlp::kPerceptionScale * conv_b[4 * g + k];
+    for (int k = 0; k < 4; ++k)
+        cb[k] = g < C / 4 ? Mlp::kPerceptionScale * conv_b[4 * (g < C / 4 ? g : 0) + k] : 0.f;
     mlp.pin_all();
 #pragma unroll
     for (int k = 0; k < 4; ++k) pin(cb[k]);
@@ -1847,8 +1857,9 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
 #pragma unroll
         for (int grp = 0; grp < 4; ++grp) {
             const int x = x0 + (grp & 1) * 16 + n;
-            offs[grp] = x < dw ? (uint32_t)(2 * wave + (grp >> 1)) * row_bytes + (uint32_t)x * kCellBytes
-                               : kOut;
+            offs[grp] = x < dw && g < C / 4
+                            ? (uint32_t)(2 * wave + (grp >> 1)) * row_bytes + (uint32_t)x * kCellBytes
+                            : kOut;
         }
 
         // Rolling perception sums (bias included): A[(r - z_begin + 1) % 3]
@@ -1946,7 +1957,7 @@ __global__ __launch_bounds__(kThreads, 2) void nca_step_mfma_3d(
             const int phase = zrel & (planes_per_eval - 1);
             const uint64_t *fwe = fire_words[wave][zrel / planes_per_eval];
             const int slot0 = 2 * phase;
-            const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * kC,
+            const Rsrc wr = make_rsrc(dst + ((int64_t)max(zo, 0) * dh + y0) * dw * C,
                                       out_ok ? (uint32_t)min(k3TY, dh - y0) * row_bytes : 0u);
             const float4 *own = ring[jm];
             // ALIGNED: the bits of the lane's 4 cells of this plane, at 2 grp
@@ -2368,9 +2379,9 @@ RowsPlan pair_plan(const StepArgs &a) {
     return r;
 }
 
-// The ablation's C = 12, H = 48 model (supplement S10) on the row kernels:
-// 2D fp32 states, scaled fp16 MLP, the lanes of channel quad 3 and hidden
-// tile 3 idle.
+// The ablation's C = 12, H = 48 model (supplement S10) on the kernels of
+// C = 16: fp32 states (the 2D row kernels and the 3D step), scaled fp16 MLP,
+// the lanes of channel quad 3 and hidden tile 3 idle.
 using MlpC12 = MlpF16SM<12, 48>;
 bool is_c12(const StepArgs &a) { return a.channels == 12 && a.hidden == 48; }
 bool is_c16(const StepArgs &a) { return a.channels == kC && a.hidden == kH; }
@@ -2510,7 +2521,8 @@ hipError_t dispatch(const StepArgs &a, Layout2d layout, const void *src, void *d
     if (a.ndim == 2) {
         if (a.n_in == 1) return launch_2d<T, 1, Mlp>(a, layout, src, dst, stream);
         if (a.n_in == 3) return launch_2d<T, 3, Mlp>(a, layout, src, dst, stream);
-    } else if constexpr (Mlp::kChannels == kC) {   // 3D: C = 16, H = 64 only
+    } else if constexpr (Mlp::kChannels == kC || std::is_same_v<T, float>) {
+        // 3D: C = 16, H = 64, or fp32 states of C = 12, H = 48
         if (a.n_in == 1) return launch_3d<T, 1, Mlp>(a, src, dst, stream);
         if (a.n_in == 3) return launch_3d<T, 3, Mlp>(a, src, dst, stream);
     }
@@ -2565,13 +2577,13 @@ hipError_t launch_step2_mfma_up(const StepArgs &a, MfmaMlp mlp, Layout2d layout,
 
 bool step_mfma_serves(const StepArgs &a, Layout2d layout) {
     if (is_c16(a)) return true;
-    return is_c12(a) && a.ndim == 2 && a.dtype == Dtype::F32 && uses_rows(a, layout) &&
+    return is_c12(a) && a.dtype == Dtype::F32 && (a.ndim == 3 || uses_rows(a, layout)) &&
            mfma_fits(a);
 }
 
 bool step_mfma_fuses_upsample(const StepArgs &a, MfmaMlp mlp, Layout2d layout) {
     if (mlp != MfmaMlp::Default || !mfma_fits(a)) return false;
-    if (is_c12(a)) return step_mfma_serves(a, layout);
+    if (is_c12(a)) return a.ndim == 2 && step_mfma_serves(a, layout);
     if (!is_c16(a)) return false;
     if (a.ndim == 2) return uses_rows(a, layout);
     return a.dtype == Dtype::F16;   // the fp16 3D step

@@ -249,11 +249,17 @@ def parity_report(wl, got, want, got_seg, want_seg, what):
           f"disagreements={int(np.sum(np.asarray(got_seg) != np.asarray(want_seg)))}", flush=True)
 
 
-@pytest.mark.parametrize("wl", [TINY_2D, MEDIUM_2D, VOLUME_3D], ids=lambda w: w.name)
+VOLUME_C12H48 = dataclasses.replace(VOLUME_3D, name="volume3d_c12h48", channels=12, hidden=48)
+
+
+@pytest.mark.parametrize("wl", [TINY_2D, MEDIUM_2D, VOLUME_3D, VOLUME_C12H48],
+                         ids=lambda w: w.name)
 def test_full_size_whole_grid(gpu, wl):
     """The three workloads the oracle finishes whole within the test (band-
     parallel over the host's cores): every cell of the final state and the
-    readout against the oracle."""
+    readout against the oracle.  The 3D volume also runs with the ablation's
+    C = 12, H = 48 model (supplement S10), whose fp32 3D steps take the same
+    kernel."""
     print(f"full-size whole-grid parity {wl.name} extent={wl.extent}", flush=True)
     image = np.ascontiguousarray(cached_image(wl))
     weights = make_weights(wl)

@@ -268,16 +268,18 @@ def test_level_steps_match_oracle(gpu, step_kernel, dt, ndim, n_in, shape):
     ("f32", 3, 3, 12, 48, (4, 10, 12)), ("f16", 2, 3, 12, 48, (1, 16, 40)),
     ("f32", 2, 3, 20, 100, (1, 19, 70)), ("f32", 2, 1, 12, 48, (1, 33, 65)),
     ("f16", 3, 1, 20, 100, (7, 9, 33)), ("f32", 3, 3, 20, 100, (3, 5, 40)),
-    ("f32", 2, 3, 12, 48, (1, 1, 1)), ("f16", 3, 3, 20, 100, (1, 1, 1))])
+    ("f32", 2, 3, 12, 48, (1, 1, 1)), ("f16", 3, 3, 20, 100, (1, 1, 1)),
+    ("f32", 3, 1, 12, 48, (9, 19, 70)), ("f32", 3, 3, 12, 48, (7, 17, 64))])
 def test_other_model_sizes_match_oracle(gpu, kernel, dt, ndim, n_in, c, h, shape):
     """The ablation's model sizes C/H = 12/48 and 20/100 (supplement S10) on
     every kernel that serves them: 2D fp32 states of 12/48 on the row kernels
     ("mfma": one step per launch on levels this small, "mfma_rows": two steps
     per launch, "mfma_1step": one) or the generic tile kernel ("mfma_tiles"),
-    the other cases on the generic matrix-core kernel ("mfma"), and all on the
-    vector kernel ("valu"): one step and nine steps against the oracle
-    (several strips or tiles, ragged tails, a single cell), input channels
-    unchanged, non-firing cells copied bit for bit."""
+    3D fp32 states of 12/48 on the 3D step of 16/64 (rows on and off the
+    8-cell grid), the other cases on the generic matrix-core kernel ("mfma"),
+    and all on the vector kernel ("valu"): one step and nine steps against the
+    oracle (several strips or tiles, ragged tails, a single cell), input
+    channels unchanged, non-firing cells copied bit for bit."""
     if kernel in ("mfma_rows", "mfma_tiles", "mfma_1step") and (dt, ndim, c) != ("f32", 2, 12):
         pytest.skip("the same generic kernel as the 'mfma' case")
     rng = np.random.default_rng(13)
