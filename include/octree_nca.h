@@ -106,11 +106,11 @@ typedef enum {
  * Step kernel: a zero-initialised tail (mlp, layout2d, steps_per_launch all
  * 0) is the library's default.  C = 16, H = 64 takes every option; the
  * other sizes take OCTNCA_MLP_AUTO (the default arithmetic on the matrix
- * cores) or OCTNCA_MLP_VALU only.  With OCTNCA_MLP_AUTO, 2D fp32 states of
- * C = 12, H = 48 run on the row kernels of C = 16, H = 64 (layout2d and
- * steps_per_launch apply as for that size; OCTNCA_LAYOUT_TILES selects
- * 8 x 32 tiles of a generic kernel); their other steps and all steps of
- * C = 20, H = 100 run on that generic kernel.  Combinations that no kernel
+ * cores) or OCTNCA_MLP_VALU only.  With OCTNCA_MLP_AUTO, fp32 states of
+ * C = 12, H = 48 run on the kernels of C = 16, H = 64 (in 2D the row kernels:
+ * layout2d and steps_per_launch apply as for that size, and
+ * OCTNCA_LAYOUT_TILES selects 8 x 32 tiles of a generic kernel); their fp16
+ * steps and all steps of C = 20, H = 100 run on that generic kernel.  Combinations that no kernel
  * implements (OCTNCA_MLP_F16 with fp32 states, OCTNCA_MLP_F16S with
  * fp16 states) give OCTNCA_EUNSUPPORTED; values outside the enums give
  * OCTNCA_EINVAL.  The training entry points choose their own arithmetic
