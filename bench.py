@@ -347,8 +347,8 @@ def main(argv=None):
     args = ap.parse_args(argv)
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
-              "octree inference of one image runs on a single MI355X. Use --gpus 1.",
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); the octree "
+              "inference of one image runs on a single MI355X. Use --gpus 1.",
               file=sys.stderr)
         return 2
 
