@@ -717,11 +717,8 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
         planes[(2 * c + 1) * PS16 + cell] = make_uint2(x.z, x.w);
     }
 
-    // Upsample + inject fused into the load (3D first step of a level; fp16
-    // planes): plane z, row gy and cell gx of the fine level come from the
-    // coarse state's plane z / fz, row gy / fy and cell gx / fx (gathered per
-    // lane); the NIN input channels from the fine image, one element per
-    // thread and load, written over channel quad 0 by commit_up_raw.
+    // Image elements of a tile's rows for the fused upsample (one per thread
+    // and load).
     static constexpr int kThreadsPerBlock = 256;
     template <int NIN>
     struct Image {
@@ -730,26 +727,29 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
         uint32_t e[kImg];
     };
 
+    // Per-lane byte offsets of the fused-upsample loads within the coarse rows
+    // and the image rows a tile may touch (kOut for unused slots and cells
+    // outside the grid): like offsets(), they depend on the tile only and are
+    // computed once per work item (the per-lane divisions by fx and fy no
+    // longer run per plane).
     template <int NIN>
-    __device__ __forceinline__ void issue_up(const T *__restrict__ coarse, int cdh, int cdw,
-                                             int fz, int fy, int fx, const T *__restrict__ img,
-                                             Image<NIN> &im, int z, int dd, int dh, int dw,
-                                             int y0, int x0, bool active = true) {
+    struct UpOffsets {
+        uint32_t o[kBodySlots + 1];
+        uint32_t img[Image<NIN>::kImg];
+    };
+    template <int NIN>
+    __device__ __forceinline__ static UpOffsets<NIN> up_offsets(int cdw, int fy, int fx, int dw,
+                                                                int y0, int x0) {
         static_assert(C == kC, "the fused upsample serves C = 16");
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int gy0 = y0 - 1;
         const int base_row = gy0 > 0 ? gy0 : 0;
-        const int rows =
-            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
-        // coarse rows base_row / fy .. (base_row + rows - 1) / fy of plane z / fz
         const int cbase = base_row / fy;
-        const int crows = rows > 0 ? (base_row + rows - 1) / fy - cbase + 1 : 0;
         const uint32_t crow_bytes = (uint32_t)cdw * kCellBytes;
-        const Rsrc r = make_rsrc(coarse + ((int64_t)(max(z, 0) / fz) * cdh + cbase) * cdw * kC,
-                                 (uint32_t)crows * crow_bytes);
         const int cell = body_cell(lane);
         const uint32_t chunk_off = (uint32_t)body_chunk(lane) * 16;
+        UpOffsets<NIN> r;
 #pragma unroll
         for (int k = 0; k < kBodySlots; ++k) {
             const int J = wave + 4 * k;
@@ -758,8 +758,7 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
             const bool ok = J < kBody && gy >= 0 && cx < dw;
             const uint32_t off = (uint32_t)(gy / fy - cbase) * crow_bytes +
                                  (uint32_t)(cx / fx) * kCellBytes + chunk_off;
-            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
-            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+            r.o[k] = ok ? off : kOut;
         }
         {
             const int s = 3 - wave;
@@ -769,12 +768,9 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
             const bool ok = s < kSide && row < HY && gy >= 0 && gx >= 0 && gx < dw;
             const uint32_t off = (uint32_t)(gy / fy - cbase) * crow_bytes +
                                  (uint32_t)(gx / fx) * kCellBytes + (uint32_t)(lane % NQ) * 16;
-            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, ok ? off : kOut, 0, 0);
-            v[kBodySlots] = make_uint4(x[0], x[1], x[2], x[3]);
+            r.o[kBodySlots] = ok ? off : kOut;
         }
         const uint32_t irow_bytes = (uint32_t)dw * NIN * (uint32_t)sizeof(T);
-        const Rsrc ri = make_rsrc(img + ((int64_t)max(z, 0) * dh + base_row) * dw * NIN,
-                                  (uint32_t)rows * irow_bytes);
 #pragma unroll
         for (int j = 0; j < Image<NIN>::kImg; ++j) {
             const int e = (int)threadIdx.x + kThreadsPerBlock * j;
@@ -785,8 +781,46 @@ __device__ __forceinline__ static void put(float4 *planes, int q, int cell, cons
             const bool ok = e < Image<NIN>::kElems && gy >= 0 && gx >= 0 && gx < dw;
             const uint32_t off = (uint32_t)(gy - base_row) * irow_bytes +
                                  (uint32_t)(gx * NIN + rem % NIN) * (uint32_t)sizeof(T);
-            im.e[j] = __builtin_amdgcn_raw_buffer_load_b16(ri, ok ? off : kOut, 0, 0);
+            r.img[j] = ok ? off : kOut;
         }
+        return r;
+    }
+
+    // Upsample + inject fused into the load (3D first step of a level; fp16
+    // planes): plane z, row gy and cell gx of the fine level come from the
+    // coarse state's plane z / fz, row gy / fy and cell gx / fx; the NIN input
+    // channels from the fine image, one element per thread and load, written
+    // over channel quad 0 by commit_up_raw.  `of` holds the lane offsets of the
+    // tile whose interior starts at (y0, x0) (from up_offsets()); rows outside
+    // the grid and z outside [0, dd) read as zero through the descriptors'
+    // ranges (the fine height is a multiple of fy, so a row below the grid
+    // maps past the coarse rows covered).
+    template <int NIN>
+    __device__ __forceinline__ void issue_up(const T *__restrict__ coarse, int cdh, int cdw,
+                                             int fz, int fy, const T *__restrict__ img,
+                                             const UpOffsets<NIN> &of, Image<NIN> &im, int z,
+                                             int dd, int dh, int dw, int y0, bool active = true) {
+        const int gy0 = y0 - 1;
+        const int base_row = gy0 > 0 ? gy0 : 0;
+        const int rows =
+            (active && z >= 0 && z < dd) ? max(0, min(gy0 + HY, dh) - base_row) : 0;
+        // coarse rows base_row / fy .. (base_row + rows - 1) / fy of plane z / fz
+        const int cbase = base_row / fy;
+        const int crows = rows > 0 ? (base_row + rows - 1) / fy - cbase + 1 : 0;
+        const uint32_t crow_bytes = (uint32_t)cdw * kCellBytes;
+        const Rsrc r = make_rsrc(coarse + ((int64_t)(max(z, 0) / fz) * cdh + cbase) * cdw * C,
+                                 (uint32_t)crows * crow_bytes);
+#pragma unroll
+        for (int k = 0; k <= kBodySlots; ++k) {
+            const v4u x = __builtin_amdgcn_raw_buffer_load_b128(r, of.o[k], 0, 0);
+            v[k] = make_uint4(x[0], x[1], x[2], x[3]);
+        }
+        const uint32_t irow_bytes = (uint32_t)dw * NIN * (uint32_t)sizeof(T);
+        const Rsrc ri = make_rsrc(img + ((int64_t)max(z, 0) * dh + base_row) * dw * NIN,
+                                  (uint32_t)rows * irow_bytes);
+#pragma unroll
+        for (int j = 0; j < Image<NIN>::kImg; ++j)
+            im.e[j] = __builtin_amdgcn_raw_buffer_load_b16(ri, of.img[j], 0, 0);
     }
 
     // Called by every thread of the block: the coarse words of a cell and its
@@ -2033,6 +2067,9 @@ __device__ __forceinline__ uint32_t bfi(uint32_t mask, uint32_t a, uint32_t b) {
 __device__ __forceinline__ uint32_t as_u32(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 
 constexpr int k3hBlocksPerCu = 3;
+// the upsample-fused variant: its extra set-up registers spill a few words
+// outside the plane loop at 3 blocks per CU
+constexpr int k3hUpBlocksPerCu = 3;
 
 // UP: the first step of a level fused with the upsample + inject: src is the
 // next coarser level's state (extent up_cdh x up_cdw per plane), upsampled by
@@ -2043,7 +2080,7 @@ constexpr int k3hBlocksPerCu = 3;
 // (channel C - 1 > channel C - 2 in the stored fp16 values, ties and NaNs 0)
 // to seg; the finest level's last launch uses it.
 template <int NIN, bool ALIGNED, bool UP, bool SEG = false>
-__global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mfma_3d_f16(
+__global__ __launch_bounds__(kThreads, UP ? k3hUpBlocksPerCu : k3hBlocksPerCu) void nca_step_mfma_3d_f16(
     const __half *__restrict__ src, __half *__restrict__ dst, int dd, int dh, int dw,
     int tiles_x, int tiles_y, int items, int zrun, const float *__restrict__ conv_w,
     const float *__restrict__ conv_b, const float *__restrict__ w1, const float *__restrict__ b1,
@@ -2090,14 +2127,15 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
     constexpr int planes_per_eval = 64 / (2 * opr);
     constexpr int kCellBytes = Loader::kCellBytes;
     const uint32_t row_bytes = (uint32_t)dw * kCellBytes;
-    int y0_cur = 0, x0_cur = 0;   // the current item's tile origin (for the loads)
+    int y0_cur = 0;   // the current item's first tile row (for the loads)
     typename Loader::Offsets lofs;  // and its lane offsets (plain loads)
+    typename Loader::template UpOffsets<NIN> uofs;   // (fused upsample loads)
     Loader ld;
     typename Loader::template Image<NIN> im;   // used by UP only
     auto issue = [&](int z, bool active) {
         if constexpr (UP)
-            ld.template issue_up<NIN>(src, up_cdh, up_cdw, up_fz, up_fy, up_fx, up_img, im, z,
-                                      dd, dh, dw, y0_cur, x0_cur, active);
+            ld.template issue_up<NIN>(src, up_cdh, up_cdw, up_fz, up_fy, up_img, uofs, im, z,
+                                      dd, dh, dw, y0_cur, active);
         else
             ld.issue_at(src, lofs, z, dd, dh, dw, y0_cur, active);
     };
@@ -2123,8 +2161,10 @@ __global__ __launch_bounds__(kThreads, UP ? 2 : k3hBlocksPerCu) void nca_step_mf
         const int ty = rest / tiles_x;
         const int y0 = ty * k3TY, x0 = tx * kTileW;
         y0_cur = y0;
-        x0_cur = x0;
-        if constexpr (!UP) lofs = Loader::offsets(dw, y0, x0);
+        if constexpr (UP)
+            uofs = Loader::template up_offsets<NIN>(up_cdw, up_fy, up_fx, dw, y0, x0);
+        else
+            lofs = Loader::offsets(dw, y0, x0);
         const int z_begin = zr * zrun;
         const int z_end = min(dd, z_begin + zrun);
         // store offsets of the lane's 4 cells within an output plane's tile rows
@@ -2499,7 +2539,7 @@ hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int 
                             int fy, int fx, const void *img, void *dst, hipStream_t stream) {
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
-    const int64_t slots = (int64_t)device_cus() * 2;
+    const int64_t slots = (int64_t)device_cus() * k3hUpBlocksPerCu;
     const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
