@@ -29,8 +29,9 @@ int check_model(const octnca_model *m) {
     if (m == nullptr) return OCTNCA_EINVAL;
     if (m->ndim != 2 && m->ndim != 3) return OCTNCA_EUNSUPPORTED;
     // C / H: the paper's 16 / 64 and the 12 / 48 and 20 / 100 of its ablation
-    // (supplement S10); the matrix-core kernels serve 16 / 64, the vector
-    // kernel all three
+    // (supplement S10); every size runs on the matrix cores (the specialised
+    // kernels for 16 / 64 and fp32 12 / 48, a generic kernel otherwise) and on
+    // the vector kernel
     const bool size_ok = (m->channels == 16 && m->hidden == 64) ||
                          (m->channels == 12 && m->hidden == 48) ||
                          (m->channels == 20 && m->hidden == 100);
