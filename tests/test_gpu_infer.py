@@ -77,6 +77,11 @@ SMALL = [
     Workload(name="c12h48_3d_nin1", ndim=3, extent=(10, 24, 40), n_in=1,
              factors=((1, 2, 2), (2, 2, 2)), steps=(4, 3, 2), image_kind="uniform",
              channels=12, hidden=48),
+    # 12/48 with a one-channel image in 2D: the upsample-fused row variants
+    # (one and two steps per launch) and the fused readout with n_in = 1
+    Workload(name="c12h48_2d_nin1", ndim=2, extent=(1, 48, 68), n_in=1,
+             factors=((1, 2, 2), (1, 2, 2)), steps=(4, 3, 2), image_kind="uniform",
+             channels=12, hidden=48),
 ]
 
 
