@@ -366,19 +366,23 @@ def test_full_size_sampled_boxes(gpu, wl, count, size, depth):
 # readout fused into the finest level's last two-step launch
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("size", [(16, 64), (12, 48)], ids=["c16h64", "c12h48"])
 @pytest.mark.parametrize("kernel", ["mfma_rows", "mfma_rows,mfma_1step", "mfma_tiles"])
 @pytest.mark.parametrize("steps", [(4, 2, 3), (5, 2, 3), (2, 2, 3), (0, 2, 3)],
                          ids=lambda s: "s" + "-".join(map(str, s)))
-def test_fused_readout_equals_readout_of_final_state(gpu, kernel, steps):
+def test_fused_readout_equals_readout_of_final_state(gpu, kernel, steps, size):
     """Where the finest level's last launch runs two steps (with the upsample
     fused into it or not), that launch writes the readout; it must equal the
     readout kernel applied to the final state, byte for byte.  Elsewhere the
-    readout kernel runs."""
+    readout kernel runs.  With C = 12 the last two channels sit in channel
+    quad 2."""
+    c, h = size
     wl = Workload(name="fused_readout", ndim=2, extent=(1, 72, 100), n_in=3,
-                  factors=((1, 2, 2), (1, 2, 2)), steps=steps, image_kind="uniform")
-    print(f"fused readout kernel={kernel} steps={steps}", flush=True)
+                  factors=((1, 2, 2), (1, 2, 2)), steps=steps, image_kind="uniform",
+                  channels=c, hidden=h)
+    print(f"fused readout kernel={kernel} steps={steps} c={c}", flush=True)
     state, seg = gpu_infer(wl, make_image(wl), make_weights(wl), kernel=kernel)
-    model = octnca.Model(ndim=2, n_in=3)
+    model = octnca.Model(ndim=2, n_in=3, channels=c, hidden=h)
     want = torch.empty_like(seg)
     octnca.octree_nca_readout(model, state, want)
     torch.cuda.synchronize()
