@@ -394,6 +394,26 @@ def test_infer_launches_counts_two_step_launches():
         octnca.octree_nca_infer_launches(m, (1, 64, 64), [(1, 2, 2)] * 2, [5, -1, 3])
 
 
+def test_infer_launches_of_the_other_model_sizes():
+    """The 12/48 model's fp32 2D steps take the row kernels of 16/64, two steps
+    per launch included; its fp16 steps, its 3D steps and the 20/100 model run
+    one step per launch (no upsample fusion in 3D fp32 and on the generic
+    kernel, so each level but the coarsest adds none)."""
+    f = [(1, 2, 2)] * 5
+    c12 = octnca.Model(ndim=2, n_in=3, channels=12, hidden=48)
+    assert octnca.octree_nca_infer_launches(c12, (1, 11264, 16384), f, [20] * 6) == \
+        [10, 10, 10, 20, 20, 20]
+    c12_1 = octnca.Model(ndim=2, n_in=3, channels=12, hidden=48, kernel="mfma_1step")
+    assert octnca.octree_nca_infer_launches(c12_1, (1, 11264, 16384), f, [20] * 6) == [20] * 6
+    c12_h = octnca.Model(ndim=2, n_in=3, dtype="f16", channels=12, hidden=48)
+    assert octnca.octree_nca_infer_launches(c12_h, (1, 4096, 1920), [], [20]) == [20]
+    c20 = octnca.Model(ndim=2, n_in=3, channels=20, hidden=100)
+    assert octnca.octree_nca_infer_launches(c20, (1, 11264, 16384), f, [20] * 6) == [20] * 6
+    c12_3 = octnca.Model(ndim=3, n_in=1, channels=12, hidden=48)
+    assert octnca.octree_nca_infer_launches(c12_3, (24, 320, 320), [(1, 2, 2)] * 2,
+                                            [20] * 3) == [20] * 3
+
+
 def test_model_kernel_fields_are_checked(lib):
     """The step-kernel fields of octnca_model: values outside their enums are
     EINVAL, combinations no kernel implements EUNSUPPORTED; checked before
