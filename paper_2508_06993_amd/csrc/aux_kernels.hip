@@ -3,6 +3,7 @@
 // export.  All are single passes over HBM with coalesced 16-byte accesses
 // where the layout allows it.
 #include <algorithm>
+#include <type_traits>
 
 #include "launch.h"
 
@@ -55,6 +56,41 @@ __global__ __launch_bounds__(kBlock) void pool_kernel(const T *__restrict__ src,
                     }
                 }
             dst[((int64_t)z * dh + y) * dw * n_in + i] = Storage<T>::from_float(acc / inv);
+        }
+    }
+}
+
+// The same for the common factors (1, 2, 2): one thread per output cell of a
+// row, whose 2 x 2 x NIN inputs are 2 NIN consecutive values in each of its
+// two input rows (fewer, wider loads than one thread per channel); the sums
+// are taken in the same (dy, dx) order, so the results are the same bits.
+template <typename T, int NIN>
+__global__ __launch_bounds__(kBlock) void pool22_kernel(const T *__restrict__ src,
+                                                        T *__restrict__ dst, int dd, int dh,
+                                                        int dw) {
+    const uint32_t x = blockIdx.x * (uint32_t)kBlock + threadIdx.x;   // output cell in the row
+    if (x >= (uint32_t)dw) return;
+    const int64_t sw = (int64_t)dw * 2 * NIN;   // values per input row
+    for (int z = blockIdx.z; z < dd; z += gridDim.z) {
+        for (int y = blockIdx.y; y < dh; y += gridDim.y) {
+            const T *r0 = src + ((int64_t)z * dh * 2 + 2 * y) * sw + (int64_t)x * 2 * NIN;
+            const T *r1 = r0 + sw;
+            float v0[2 * NIN], v1[2 * NIN];
+#pragma unroll
+            for (int k = 0; k < 2 * NIN; ++k) {
+                v0[k] = Storage<T>::to_float(r0[k]);
+                v1[k] = Storage<T>::to_float(r1[k]);
+            }
+            T *out = dst + ((int64_t)z * dh + y) * dw * NIN + (int64_t)x * NIN;
+#pragma unroll
+            for (int c = 0; c < NIN; ++c) {
+                float acc = 0.f;
+                acc += v0[c];
+                acc += v0[NIN + c];
+                acc += v1[c];
+                acc += v1[NIN + c];
+                out[c] = Storage<T>::from_float(acc / 4.f);
+            }
         }
     }
 }
@@ -152,6 +188,22 @@ __global__ __launch_bounds__(kBlock) void fire_mask_kernel(uint64_t seed, uint32
 hipError_t launch_pool(Dtype dt, const void *src, Extent3 e, void *dst, int fz, int fy, int fx,
                        int n_in, hipStream_t stream) {
     if (e.cells() == 0) return hipSuccess;
+    if (fz == 1 && fy == 2 && fx == 2 && (n_in == 1 || n_in == 3)) {
+        const dim3 g22 = row_grid(e.w, e.h, e.d);
+        auto go = [&](auto tag, auto nin) {
+            using T = decltype(tag);
+            pool22_kernel<T, decltype(nin)::value><<<g22, kBlock, 0, stream>>>(
+                (const T *)src, (T *)dst, (int)e.d, (int)e.h, (int)e.w);
+        };
+        if (dt == Dtype::F32) {
+            if (n_in == 1) go(float{}, std::integral_constant<int, 1>{});
+            else go(float{}, std::integral_constant<int, 3>{});
+        } else {
+            if (n_in == 1) go(__half{}, std::integral_constant<int, 1>{});
+            else go(__half{}, std::integral_constant<int, 3>{});
+        }
+        return hipGetLastError();
+    }
     const dim3 grid = row_grid(e.w * n_in, e.h, e.d);
     if (dt == Dtype::F32)
         pool_kernel<float><<<grid, kBlock, 0, stream>>>((const float *)src, (float *)dst,

@@ -63,7 +63,8 @@ def test_fire_mask_bit_exact(gpu, extent, seed, level, step, rate):
 POOL_CASES = [("f32", 2, (1, 64, 96), [(1, 2, 2)] * 3, 3), ("f32", 3, (8, 24, 20),
               [(2, 2, 2), (1, 2, 2)], 1), ("f16", 3, (8, 24, 20), [(2, 2, 2), (2, 2, 1)], 3),
               ("f16", 2, (1, 40, 36), [(1, 2, 2), (1, 2, 3)], 3), ("f32", 3, (6, 9, 4),
-              [(3, 3, 4)], 3)]
+              [(3, 3, 4)], 3), ("f16", 3, (4, 20, 36), [(1, 2, 2), (2, 2, 2)], 1),
+              ("f32", 2, (1, 34, 18), [(1, 2, 2)], 1)]
 
 
 @pytest.mark.parametrize("dt,ndim,extent,factors,n_in", POOL_CASES)
