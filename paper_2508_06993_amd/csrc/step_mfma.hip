@@ -1804,8 +1804,11 @@ constexpr int k3TY = 8;
 // so long runs on deep levels stream less; its fire words (one evaluation per
 // 4 or 8 planes) take k3ZRun / 4 x 64 B of LDS per wave.  128 keeps the fp16
 // step at 3 blocks per CU (44 KB each) and the fp32 one at 2 (78 KB); against
-// 32 it took the video pass 89.0 -> 85.3 ms (64: 86.9 ms).
+// 32 it took the video pass 89.0 -> 85.3 ms (64: 86.9 ms).  The fp16 step
+// takes runs of up to 256 planes (16 KB of fire words per block: 52 KB, still
+// 3 blocks per CU).
 constexpr int k3ZRun = 128;
+constexpr int k3hZRun = 256;
 // Work item i of a 3D step is tile (tx, ty) of z run zr, with
 // i = (zr * tiles_y + ty) * tiles_x + tx.
 
@@ -2090,9 +2093,9 @@ __global__ __launch_bounds__(kThreads, UP ? k3hUpBlocksPerCu : k3hBlocksPerCu) v
     using Loader = RowLoader<__half, k3TY + 2>;
     __shared__ uint2 ring[3][4 * Loader::PS16];
     __shared__ uint2 tapw[27][4];           // [tap][quad] fp16 conv weights of channels 4q..4q+3
-    // [wave][evaluation of the work item][b]: ballot b (k3ZRun / 4 evaluations
+    // [wave][evaluation of the work item][b]: ballot b (k3hZRun / 4 evaluations
     // at most: one per 4 or 8 planes)
-    __shared__ uint64_t fire_words[4][k3ZRun / 4][8];
+    __shared__ uint64_t fire_words[4][k3hZRun / 4][8];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -2264,7 +2267,7 @@ __global__ __launch_bounds__(kThreads, UP ? k3hUpBlocksPerCu : k3hBlocksPerCu) v
 
             const int zo = p - 1;
             const bool out_ok = zo >= z_begin && zo < z_end;
-            const int zrel = min(max(zo - z_begin, 0), k3ZRun - 1);   // in range for any plane
+            const int zrel = min(max(zo - z_begin, 0), k3hZRun - 1);   // in range for any plane
             const int phase = zrel & (planes_per_eval - 1);
             const uint64_t *fwe = fire_words[wave][zrel / planes_per_eval];
             const int slot0 = 2 * phase;
@@ -2475,17 +2478,17 @@ hipError_t launch_2d(const StepArgs &a, Layout2d layout, const void *src, void *
 }
 
 // Output planes per 3D work item, chosen per launch: the run length r in
-// 1 .. 32 that minimises ceil(items(r) / slots) * (planes(r) + 2), the work
+// 1 .. max_run that minimises ceil(items(r) / slots) * (planes(r) + 2), the work
 // of the most loaded block slot (grid-stride rounds times the planes a work
 // item streams, its two halo planes included); ties go to the longer run.
 // Short runs spread small levels over the chip at the cost of reading their
 // halo planes again; long runs stream large levels with little re-reading.
 // With groups of 3 (the fp16 kernel's plane loop is unrolled three times),
 // a work item streams its planes in whole groups of three.
-int pick_zrun(int64_t tiles, int64_t depth, int64_t slots, bool groups_of_3 = false) {
+int pick_zrun(int64_t tiles, int64_t depth, int64_t slots, bool groups_of_3, int max_run) {
     int best = 1;
     int64_t best_cost = INT64_MAX;
-    for (int r = 1; r <= k3ZRun; ++r) {
+    for (int r = 1; r <= max_run; ++r) {
         const int64_t items = tiles * ((depth + r - 1) / r);
         int64_t planes = std::min<int64_t>(r, depth) + 2;
         if (groups_of_3) planes = (planes + 2) / 3 * 3;
@@ -2504,7 +2507,8 @@ hipError_t launch_3d(const StepArgs &a, const void *src, void *dst, hipStream_t 
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t slots = (int64_t)device_cus() * (kF16 ? k3hBlocksPerCu : kBlocksPerCu);
-    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true);
+    const int zrun =
+        pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true, kF16 ? k3hZRun : k3ZRun);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;
@@ -2540,7 +2544,7 @@ hipError_t launch_3d_f16_up(const StepArgs &a, const void *coarse, int cdh, int 
     const int tiles_x = (int)((a.ext.w + kTileW - 1) / kTileW);
     const int tiles_y = (int)((a.ext.h + k3TY - 1) / k3TY);
     const int64_t slots = (int64_t)device_cus() * k3hUpBlocksPerCu;
-    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true);
+    const int zrun = pick_zrun((int64_t)tiles_x * tiles_y, a.ext.d, slots, true, k3hZRun);
     const int64_t zruns = (a.ext.d + zrun - 1) / zrun;
     const int64_t items = (int64_t)tiles_x * tiles_y * zruns;
     if (items == 0) return hipSuccess;

@@ -285,7 +285,7 @@ def sampled_boxes(wl, count, size, depth=1, seed=5):
     128-row run edge, boxes straddling a 32-cell tile edge and an 8-row (3D)
     or 16-row (2D) tile edge, boxes starting at the last cell of a strip and
     of a run, and uniformly random boxes; in 3D the first three kinds also
-    straddle a z-run edge (a multiple of 100 planes: the 3D step's run length
+    straddle a z-run edge (a multiple of 202 planes: the 3D step's run length
     on the video's finest level on a 256-CU device)."""
     d, h, w = wl.extent
     rng = np.random.default_rng(seed)
@@ -307,7 +307,7 @@ def sampled_boxes(wl, count, size, depth=1, seed=5):
     while len(out) < count:
         kind = k % 4
         k += 1
-        z = pick(d, 100) - dz // 2 if wl.ndim == 3 and kind < 3 else int(rng.integers(0, zmax + 1))
+        z = pick(d, 202) - dz // 2 if wl.ndim == 3 and kind < 3 else int(rng.integers(0, zmax + 1))
         if kind == 0:
             b = box(z, pick(h, 128) - size // 2, pick(w, 30) - size // 2)
         elif kind == 1:

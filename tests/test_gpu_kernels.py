@@ -317,9 +317,9 @@ def oracle_window_steps(s, w, n_in, ndim, level, steps, seed, rate, dt, box):
                                        ("f32", (300, 8, 24572)), ("f32", (300, 8, 24576))])
 def test_long_3d_runs_match_oracle_on_windows(gpu, dt, extent):
     """Levels deep and wide enough that the 3D step streams runs of more than
-    32 output planes (the launch's load model picks about 100 planes for fp16
-    and 76 for fp32 on these extents, with 768 columns), rows on and off the
-    8-cell grid (up to 32 fire evaluations per run): three steps against the
+    32 output planes (the launch's load model picks 151 planes for fp16 and 76
+    for fp32 on these extents, with 768 columns), rows on and off the 8-cell
+    grid (up to 38 fire evaluations per run): three steps against the
     oracle on windows at the grid's faces, at run boundaries of several run
     lengths and across a strip boundary."""
     rng = np.random.default_rng(31)
